@@ -1,0 +1,232 @@
+"""Benchmark of the ISPA hot path on one MI355X.
+
+One step is one pass of the whole hot path for one warmup chunk of one layer
+at the Wan-1.3B shape (12 heads x 128, d = 1536, chunk = 4680 queries):
+
+  1. F-Layer attention, dual stream: full cache of 7 chunks (32760 keys) and
+     the local window of 2 chunks (9360 keys) from one pass;
+  2. L-Layer attention over the local window only;
+  3. statistics of the chunk: R = bf16(A_full - A_loc), G += X^T X,
+     C += X^T R with X = bf16(A_loc) (4680 rows);
+  4. the closed-form solve dW = (G + 1e-3 I)^-1 C (d = 1536), which waits for
+     the device.
+
+Inputs are seeded synthetic N(0, 1) bf16 tensors already resident in HBM.
+`value` is the algorithmic TFLOP/s of the whole step (visible keys only for
+attention, the symmetric half of X^T X, D^3/3 + 2 D^2 D_out for the solve)
+divided by the measured step time. The roofline object covers the dominant
+kernel (the dual-stream attention), timed with HIP events on the stream it
+runs on. `cpu_baseline` times the CPU oracle on a bounded sample of the same
+step. `--workload 14b` runs the 14B-like shape instead (40 heads, 98280 keys).
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+WORKLOADS = {
+    "1.3b": dict(name="wan1.3b-chunk-warmup-step", heads=12, head_dim=128, n_q=4680, cache_len=32760,
+                 window=9360, sink=0, lam=1e-3),
+    "14b": dict(name="14b-chunk-warmup-step", heads=40, head_dim=128, n_q=4680, cache_len=98280,
+                window=9360, sink=0, lam=1e-3),
+}
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
+PEAK_HBM_GBS = 8000.0
+
+
+def flops(w):
+    D = w["heads"] * w["head_dim"]
+    n_q, N, win = w["n_q"], w["cache_len"], w["window"]
+    vis_local = min(N, win + min(w["sink"], N))
+    f = {
+        "attn_dual": 4.0 * n_q * N * D,
+        "attn_local": 4.0 * n_q * vis_local * D,
+        "gram": float(n_q) * D * (D + 1) + 2.0 * n_q * D * D,
+        "solve": D ** 3 / 3.0 + 2.0 * D * D * D,
+    }
+    return f
+
+
+def gpu_run(w, steps, warmup):
+    import synth
+    import paper_2607_00712_amd as ispa
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    H, d = w["heads"], w["head_dim"]
+    D = H * d
+    q, k, v = synth.chunk_qkv(2607, 0, 0, w["n_q"], w["cache_len"], D, dev)
+    out = torch.empty((w["n_q"], D), dtype=torch.float32, device=dev)
+    out_l = torch.empty_like(out)
+    out_L = torch.empty_like(out)
+    lse = torch.empty((H, w["n_q"]), dtype=torch.float32, device=dev)
+    lse_l = torch.empty_like(lse)
+    lse_L = torch.empty_like(lse)
+    stats = ispa.Stats(D, D, max_rows=w["n_q"], device=dev)
+    dw = torch.empty((D, D), dtype=torch.float32, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"], dual=True,
+                        out=out, lse=lse, out_local=out_l, lse_local=lse_l)
+        if ev is not None:
+            ev[1].record()
+        ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"],
+                        out=out_L, lse=lse_L)
+        if ev is not None:
+            ev[2].record()
+        stats.accum(out_l, out, out_l)
+        if ev is not None:
+            ev[3].record()
+        stats.solve(w["lam"], delta_w=dw)
+        if ev is not None:
+            ev[4].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    parts = {"attn_dual": [], "attn_local": [], "accum_stats": [], "solve": []}
+    for ev in events:
+        parts["attn_dual"].append(ev[0].elapsed_time(ev[1]))
+        parts["attn_local"].append(ev[1].elapsed_time(ev[2]))
+        parts["accum_stats"].append(ev[2].elapsed_time(ev[3]))
+        parts["solve"].append(ev[3].elapsed_time(ev[4]))
+    avg = {k2: sum(v2) / len(v2) for k2, v2 in parts.items()}
+    ms_step = (t1 - t0) * 1e3 / steps
+    return ms_step, avg
+
+
+def cpu_baseline(w, budget_rows=512):
+    """The oracle on a bounded sample of one step, scaled to TFLOP/s."""
+    import numpy as np
+    import oracle
+    import synth
+
+    H, d = w["heads"], w["head_dim"]
+    D = H * d
+    cores = len(os.sched_getaffinity(0))
+    q, k, v = synth.chunk_qkv(2607, 0, 0, w["n_q"], w["cache_len"], D, "cpu")
+    rows = np.arange(budget_rows)
+    qn = q.double().numpy()
+    kn = k.double().numpy()
+    vn = v.double().numpy()
+    f = flops(w)
+    frac = budget_rows / w["n_q"]
+    t = time.perf_counter()
+    o = oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], H, sink_len=w["sink"],
+                               branches=("full", "local"), query_rows=rows)
+    oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], H, sink_len=w["sink"],
+                           branches=("local",), query_rows=rows)
+    t_attn = time.perf_counter() - t
+    del kn, vn
+    st = oracle.Stats(D, D)
+    xs = oracle.bf16_round(o["local"][0].astype(np.float32))
+    t = time.perf_counter()
+    st.accumulate(xs, o["full"][0].astype(np.float32), o["local"][0].astype(np.float32))
+    t_stats = time.perf_counter() - t
+    G = st.G + np.eye(D) * 10.0  # sample rows < D: keep the system well posed for timing
+    t = time.perf_counter()
+    oracle.solve_modulation(G, st.C, w["lam"])
+    t_solve = time.perf_counter() - t
+    # scale each sampled part to a whole step
+    t_step = (t_attn / frac) + (t_stats / frac) + t_solve
+    total_flops = sum(f.values())
+    return {
+        "value": total_flops / t_step / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"fp64 numpy oracle: F-Layer dual + L-Layer attention and statistics for {budget_rows} "
+                   f"of {w['n_q']} query rows (all {H} heads, all keys), full {D}x{D} Cholesky solve; "
+                   f"attention and statistics time scaled by {w['n_q']}/{budget_rows}; measured "
+                   f"{t_attn:.2f}s + {t_stats:.2f}s + {t_solve:.2f}s"),
+        "ms_per_step_extrapolated": t_step * 1e3,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="1.3b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the ISPA hot path here has no multi-GPU "
+              "path (heads or layers would shard with no exchange; see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+    w = WORKLOADS[args.workload]
+    f = flops(w)
+    ms_step, avg = gpu_run(w, args.steps, args.warmup)
+    total = sum(f.values())
+    value = total / (ms_step * 1e-3) / 1e12
+    attn_ms = avg["attn_dual"]
+    achieved = f["attn_dual"] / (attn_ms * 1e-3) / 1e12
+    rec = {
+        "metric": "chunk attention TFLOP/s (F vs L layer) + stats/solve ms, 1.3B/14B shapes",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w["name"],
+            "heads": w["heads"], "head_dim": w["head_dim"], "chunk_queries": w["n_q"],
+            "cache_len": w["cache_len"], "window": w["window"], "sink": w["sink"],
+            "d": w["heads"] * w["head_dim"], "lambda": w["lam"],
+            "step": "F-Layer dual attention + L-Layer attention + accum_stats + solve",
+            "accumulate": "fp32 (attention, Gram); solve fp32",
+        },
+        "roofline": {
+            "kernel": "attn_chunk_kernel<128> (F-Layer, dual stream)",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+        },
+        "breakdown": {
+            "attn_dual_ms": round(avg["attn_dual"], 4),
+            "attn_dual_tflops": round(f["attn_dual"] / avg["attn_dual"] / 1e9, 1),
+            "attn_local_ms": round(avg["attn_local"], 4),
+            "attn_local_tflops": round(f["attn_local"] / avg["attn_local"] / 1e9, 1),
+            "accum_stats_ms": round(avg["accum_stats"], 4),
+            "gram_tflops": round(f["gram"] / avg["accum_stats"] / 1e9, 1),
+            "solve_ms": round(avg["solve"], 4),
+            "solve_tflops": round(f["solve"] / avg["solve"] / 1e9, 2),
+            "flop": {k2: v2 for k2, v2 in f.items()},
+        },
+    }
+    if not args.no_cpu_baseline and args.workload == "1.3b":
+        rec["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

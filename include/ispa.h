@@ -1,0 +1,177 @@
+/*
+ * ispa.h -- C ABI of libispa: the data-parallel hot path of Instance-Specific
+ * Parametric Absorption (ISPA, arXiv 2607.00712) on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Three operations, each defined by the paper:
+ *   ispa_attn_chunk        chunk attention of an F-Layer (full cache) or an
+ *                          L-Layer (sink + sliding window), optionally both
+ *                          from one pass (Sec. 2 Eq. 3; Sec. 3.4 Eq. 7-12)
+ *   ispa_accum_stats       warmup statistics: residual R = y_full - y_local,
+ *                          G += X^T X, C += X^T R, ||R||^2 (Sec. 3.2, Eq. 4-5
+ *                          and the last paragraph of Sec. 3.2)
+ *   ispa_solve_modulation  dW = (G + lambda I)^-1 C and the feasibility score
+ *                          eps (Sec. 3.2, Eq. 5-6)
+ *
+ * Conventions shared by every call
+ *   - Matrices are row-major with the last dimension contiguous.
+ *   - Device pointers point to device memory of the current HIP device and
+ *     must be 16-byte aligned. The caller owns every buffer: the library never
+ *     allocates or frees device memory and keeps no pointer beyond the work it
+ *     enqueues, except the statistics workspace, which the handle uses until
+ *     ispa_stats_destroy.
+ *   - Work is enqueued on the caller's HIP stream (0 = the null stream) and
+ *     runs asynchronously; only ispa_solve_modulation waits for the device.
+ *   - Argument errors are reported before anything is enqueued, so a failing
+ *     call writes nothing.
+ *   - The return value is a status code (ISPA_OK or a negative ISPA_ERR_*).
+ */
+#ifndef ISPA_H
+#define ISPA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+#define ISPA_OK                0
+#define ISPA_ERR_INVALID_ARG (-1) /* null/misaligned pointer, size out of range */
+#define ISPA_ERR_UNSUPPORTED (-2) /* head_dim or dtype not supported            */
+#define ISPA_ERR_NOT_SPD     (-3) /* G + lambda I has a non-positive pivot      */
+#define ISPA_ERR_HIP         (-4) /* a HIP launch or runtime call failed        */
+#define ISPA_ERR_STATE       (-5) /* bad handle or workspace                    */
+
+/* element types of ispa_accum_stats inputs */
+#define ISPA_DTYPE_BF16 0
+#define ISPA_DTYPE_F32  1
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* ispa_status_string(int status);
+
+/* ABI version of this header (major * 100 + minor). */
+int ispa_abi_version(void);
+
+/* ------------------------------------------------------------ attention */
+/*
+ * Attention of one chunk's queries against one layer's KV cache.
+ *
+ * Sec. 2, Eq. 3: Q comes from the current chunk; K and V are the cached past
+ * followed by the current chunk, so the last n_q of the cache_len cached keys
+ * are the current chunk, and every query sees all keys of its set (no mask
+ * inside a chunk). Sec. 3.4, Eq. 7-8: the local set is the sink prefix plus the
+ * most recent keys, the history is everything between them:
+ *
+ *   local = [0, min(sink_len, N)) U [max(N - window, 0), N)      N = cache_len
+ *   hist  = [0, N) minus local
+ *
+ * Each set is attended with ordinary softmax attention returning the output and
+ * its natural-log log-sum-exp (Eq. 9-10); full = local U hist (Eq. 11-12).
+ *
+ *   q          bf16 [n_q, n_heads * head_dim]   current chunk's queries
+ *   k_cache    bf16 [>= cache_len, n_heads * head_dim]  keys; rows >= cache_len
+ *              are never read
+ *   v_cache    bf16 [>= cache_len, n_heads * head_dim]  values, same layout
+ *   cache_len  N: keys in the cache, the current chunk included; n_q <= N
+ *   window     w >= 1: number of most recent keys in the local set
+ *              (window >= cache_len - sink_len makes the local set the full
+ *              cache: an F-Layer)
+ *   sink_len   s >= 0: number of leading (sink) keys in the local set
+ *   n_q        >= 1 queries; n_heads >= 1; head_dim in {64, 128}
+ *   scale      logit scale; <= 0 selects 1/sqrt(head_dim)
+ *   out        fp32 [n_q, n_heads * head_dim]
+ *   lse        fp32 [n_heads, n_q] or NULL
+ *   out_local  fp32 [n_q, n_heads * head_dim] or NULL
+ *   lse_local  fp32 [n_heads, n_q] or NULL (needs out_local)
+ *
+ * Single-stream form (out_local == NULL): out/lse receive attention over the
+ * local set (an L-Layer; an F-Layer when the window covers the cache).
+ * Dual-stream form (out_local != NULL, the warmup of Sec. 3.1 step 1): one pass
+ * writes the local-set result to out_local/lse_local and the full-set result to
+ * out/lse, which equals the LSE fusion of Eq. 11-12 of the local and history
+ * branches. Outputs must not overlap the inputs or each other.
+ */
+int ispa_attn_chunk(const void* q, const void* k_cache, const void* v_cache,
+                    int64_t cache_len, int64_t window, int64_t sink_len,
+                    int32_t n_q, int32_t n_heads, int32_t head_dim, float scale,
+                    float* out, float* lse, float* out_local, float* lse_local,
+                    hipStream_t stream);
+
+/* ---------------------------------------------------------- statistics */
+/*
+ * Sufficient statistics of one layer's absorption problem (Sec. 3.2): the
+ * method sums A_loc^T A_loc and A_loc^T R over the warmup rows and solves one
+ * D x D system at the end of warmup. A handle is host-side state over a
+ * caller-owned device workspace that holds every device-side quantity:
+ *   G      fp32 [d_in, d_in]    sum of X^T X (lower block triangle valid)
+ *   C      fp32 [d_in, d_out]   sum of X^T R
+ *   s      fp64                 sum of ||R||_F^2
+ *   plus staging for up to max_rows rows of bf16 X and R, and the factor of
+ *   the solve.
+ * A handle is not thread-safe; different handles are independent.
+ */
+typedef struct ispa_stats ispa_stats;
+
+/* Bytes of device workspace a handle needs (0 if the sizes are invalid:
+ * d_in, d_out in [1, 16384], d_in a multiple of 64, max_rows >= 1). */
+size_t ispa_stats_workspace_bytes(int32_t d_in, int32_t d_out, int64_t max_rows);
+
+/* Creates a handle over `workspace` (device, 256-byte aligned, at least
+ * ispa_stats_workspace_bytes bytes, owned by the caller and kept alive until
+ * ispa_stats_destroy) and zeroes the statistics on `stream`. */
+int ispa_stats_create(ispa_stats** handle, void* workspace, size_t workspace_bytes,
+                      int32_t d_in, int32_t d_out, int64_t max_rows, hipStream_t stream);
+
+/* Zeroes G, C, s and the row count (a new warmup, e.g. the event-triggered
+ * recalibration of Sec. 3.3). Asynchronous on the handle's stream. */
+int ispa_stats_reset(ispa_stats* handle);
+
+/* Releases the host handle; the workspace is the caller's to free afterwards. */
+int ispa_stats_destroy(ispa_stats* handle);
+
+/* Device addresses of G, C and s inside the workspace, and the number of rows
+ * accumulated so far (host). Any output pointer may be NULL. */
+int ispa_stats_views(const ispa_stats* handle, float** G, float** C, double** sq_norm_r,
+                     int64_t* n_rows);
+
+/*
+ * Adds n_rows warmup rows (Sec. 3.2):
+ *   R  = bf16_rne(fp32(y_full) - fp32(y_local))       [n_rows, d_out]
+ *   G += X^T X,  C += X^T R,  s += ||R||_F^2,  n += n_rows
+ * with X = bf16_rne(x) when x is fp32. X holds A_loc (the input of the output
+ * projection, heads concatenated); y_full/y_local are the full- and local-stream
+ * outputs whose difference is to be absorbed: post-projection outputs A W give
+ * the paper's dW directly, the attention outputs themselves give dW' with
+ * dW = dW' W.
+ *   x        [n_rows, d_in]  of x_dtype  (ISPA_DTYPE_BF16 or ISPA_DTYPE_F32)
+ *   y_full   [n_rows, d_out] of y_dtype
+ *   y_local  [n_rows, d_out] of y_dtype
+ * Any n_rows >= 0 is accepted; rows are staged max_rows at a time.
+ * Enqueued on the handle's stream.
+ */
+int ispa_accum_stats(ispa_stats* handle, const void* x, int32_t x_dtype,
+                     const void* y_full, const void* y_local, int32_t y_dtype,
+                     int64_t n_rows);
+
+/*
+ * Closed-form modulation (Sec. 3.2, Eq. 5): dW = (G + lambda I)^-1 C, by a
+ * Cholesky factorisation of G + lambda I and two triangular solves, in fp32.
+ *   lambda    ridge weight added to the summed Gram matrix (the paper uses
+ *             1e-3); lambda >= 0
+ *   delta_w   fp32 [d_in, d_out] output (device)
+ *   eps_out   host double or NULL: the feasibility score of Eq. 6,
+ *             ||X dW - R||_F^2 = s - <dW, C> - lambda ||dW||_F^2
+ * G and C are left unchanged, so the caller may solve again with another
+ * lambda or keep accumulating. Waits for the handle's stream to finish; returns
+ * ISPA_ERR_NOT_SPD (delta_w then unspecified) if a pivot is not positive.
+ */
+int ispa_solve_modulation(ispa_stats* handle, float lambda, float* delta_w, double* eps_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISPA_H */

@@ -1,0 +1,243 @@
+"""ISPA hot path on MI355X: thin ctypes binding over libispa.so.
+
+Every computation runs in the HIP kernels of libispa; this module only checks
+tensor dtypes/devices/layouts, allocates outputs with torch and passes raw
+pointers plus the current HIP stream. There is no CPU fallback: importing
+works without the library, but every call raises if it is not built.
+
+    attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0,
+               dual=False) -> (out, lse) or (out, lse, out_local, lse_local)
+    Stats(d_in, d_out, max_rows).accum(x, y_full, y_local)
+    Stats.solve(lam) -> (delta_w, eps)
+"""
+
+import ctypes
+import os
+
+import torch
+
+__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "Stats", "status_string",
+           "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
+           "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libispa.so")
+
+ISPA_OK = 0
+ISPA_ERR_INVALID_ARG = -1
+ISPA_ERR_UNSUPPORTED = -2
+ISPA_ERR_NOT_SPD = -3
+ISPA_ERR_HIP = -4
+ISPA_ERR_STATE = -5
+
+DTYPE_BF16 = 0
+DTYPE_F32 = 1
+
+_c_i32, _c_i64, _c_f32, _c_p, _c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+
+_SIGNATURES = {
+    "ispa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "ispa_abi_version": (ctypes.c_int, []),
+    "ispa_attn_chunk": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
+                                       _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "ispa_stats_workspace_bytes": (_c_sz, [_c_i32, _c_i32, _c_i64]),
+    "ispa_stats_create": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_p, _c_sz, _c_i32, _c_i32, _c_i64, _c_p]),
+    "ispa_stats_reset": (ctypes.c_int, [_c_p]),
+    "ispa_stats_destroy": (ctypes.c_int, [_c_p]),
+    "ispa_stats_views": (ctypes.c_int, [_c_p, ctypes.POINTER(_c_p), ctypes.POINTER(_c_p),
+                                        ctypes.POINTER(_c_p), ctypes.POINTER(_c_i64)]),
+    "ispa_accum_stats": (ctypes.c_int, [_c_p, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64]),
+    "ispa_solve_modulation": (ctypes.c_int, [_c_p, _c_f32, _c_p, ctypes.POINTER(ctypes.c_double)]),
+}
+
+_lib = None
+
+
+class IspaError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+class NotSPDError(IspaError):
+    pass
+
+
+def lib():
+    """The loaded libispa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libispa.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def status_string(status):
+    return lib().ispa_status_string(int(status)).decode()
+
+
+def _check(status, where):
+    if status != ISPA_OK:
+        if status == ISPA_ERR_NOT_SPD:
+            raise NotSPDError(status, where)
+        raise IspaError(status, where)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _require(t, name, dtype, device=None, ndim=2):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dim() != ndim or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {ndim}-d tensor")
+
+
+def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scale=0.0,
+               dual=False, out=None, lse=None, out_local=None, lse_local=None, need_lse=True):
+    """Chunk attention (see ispa_attn_chunk in include/ispa.h).
+
+    q [n_q, H*d] bf16; k_cache, v_cache [>= cache_len, H*d] bf16 on one device.
+    Returns (out, lse), or (out, lse, out_local, lse_local) when dual: out is then
+    the full-cache result and out_local the sink + window result.
+    """
+    L = lib()
+    _require(q, "q", torch.bfloat16)
+    dev = q.device
+    _require(k_cache, "k_cache", torch.bfloat16, dev)
+    _require(v_cache, "v_cache", torch.bfloat16, dev)
+    n_q, hidden = q.shape
+    if hidden % n_heads:
+        raise ValueError("hidden size is not a multiple of n_heads")
+    head_dim = hidden // n_heads
+    if k_cache.shape[1] != hidden or v_cache.shape[1] != hidden:
+        raise ValueError("k/v hidden size differs from q")
+    if k_cache.shape[0] < cache_len or v_cache.shape[0] < cache_len:
+        raise ValueError("cache tensors hold fewer than cache_len rows")
+    if out is None:
+        out = torch.empty((n_q, hidden), dtype=torch.float32, device=dev)
+    if lse is None and need_lse:
+        lse = torch.empty((n_heads, n_q), dtype=torch.float32, device=dev)
+    if dual:
+        if out_local is None:
+            out_local = torch.empty((n_q, hidden), dtype=torch.float32, device=dev)
+        if lse_local is None and need_lse:
+            lse_local = torch.empty((n_heads, n_q), dtype=torch.float32, device=dev)
+    for name, t, shape in (("out", out, (n_q, hidden)), ("out_local", out_local, (n_q, hidden)),
+                           ("lse", lse, (n_heads, n_q)), ("lse_local", lse_local, (n_heads, n_q))):
+        if t is not None:
+            _require(t, name, torch.float32, dev)
+            if tuple(t.shape) != shape:
+                raise ValueError(f"{name} must have shape {shape}")
+    st = L.ispa_attn_chunk(_ptr(q), _ptr(k_cache), _ptr(v_cache), int(cache_len), int(window), int(sink_len),
+                           int(n_q), int(n_heads), int(head_dim), float(scale), _ptr(out), _ptr(lse),
+                           _ptr(out_local if dual else None), _ptr(lse_local if dual else None), _stream(dev))
+    _check(st, "ispa_attn_chunk")
+    return (out, lse, out_local, lse_local) if dual else (out, lse)
+
+
+_DT = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}
+
+
+class Stats:
+    """Warmup statistics of one layer and the closed-form solve (ispa_stats_*).
+
+    The device workspace is a torch uint8 tensor owned by this object.
+    """
+
+    def __init__(self, d_in, d_out, max_rows=4680, device=None):
+        L = lib()
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        if dev.type != "cuda":
+            raise ValueError("Stats lives on a HIP device")
+        self.device = dev if dev.index is not None else torch.device("cuda", torch.cuda.current_device())
+        self.d_in, self.d_out, self.max_rows = int(d_in), int(d_out), int(max_rows)
+        nbytes = L.ispa_stats_workspace_bytes(self.d_in, self.d_out, self.max_rows)
+        if nbytes == 0:
+            raise IspaError(ISPA_ERR_INVALID_ARG, "ispa_stats_workspace_bytes")
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+        pad = (-self.workspace.data_ptr()) % 256
+        self._ws = self.workspace[pad:pad + nbytes]
+        self._h = ctypes.c_void_p(0)
+        _check(L.ispa_stats_create(ctypes.byref(self._h), _ptr(self._ws), nbytes, self.d_in, self.d_out,
+                                   self.max_rows, _stream(self.device)), "ispa_stats_create")
+
+    def _handle(self):
+        if not self._h:
+            raise IspaError(ISPA_ERR_STATE, "Stats (destroyed)")
+        return self._h
+
+    def reset(self):
+        _check(lib().ispa_stats_reset(self._handle()), "ispa_stats_reset")
+
+    def accum(self, x, y_full, y_local):
+        """Add rows: x [n, d_in] (bf16 or fp32); y_full, y_local [n, d_out] (same dtype)."""
+        for name, t, cols in (("x", x, self.d_in), ("y_full", y_full, self.d_out), ("y_local", y_local, self.d_out)):
+            if t.dtype not in _DT:
+                raise TypeError(f"{name} must be bf16 or fp32")
+            _require(t, name, t.dtype, self.device)
+            if t.shape[1] != cols:
+                raise ValueError(f"{name} must have {cols} columns")
+        if y_full.dtype != y_local.dtype:
+            raise TypeError("y_full and y_local must share a dtype")
+        n = x.shape[0]
+        if y_full.shape[0] != n or y_local.shape[0] != n:
+            raise ValueError("row counts differ")
+        _check(lib().ispa_accum_stats(self._handle(), _ptr(x), _DT[x.dtype], _ptr(y_full), _ptr(y_local),
+                                      _DT[y_full.dtype], int(n)), "ispa_accum_stats")
+
+    def views(self):
+        """(G, C, s, n): G [d_in, d_in] (lower block triangle valid), C [d_in, d_out]
+        fp32 views of the workspace, s a 1-element fp64 view, n the row count."""
+        g, c, s = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+        n = ctypes.c_int64()
+        _check(lib().ispa_stats_views(self._handle(), ctypes.byref(g), ctypes.byref(c), ctypes.byref(s),
+                                      ctypes.byref(n)), "ispa_stats_views")
+        base = self._ws.data_ptr()
+
+        def view(ptr, count, dtype, shape):
+            off = ptr - base
+            size = torch.tensor([], dtype=dtype).element_size()
+            return self._ws[off:off + count * size].view(dtype).view(*shape)
+
+        G = view(g.value, self.d_in * self.d_in, torch.float32, (self.d_in, self.d_in))
+        C = view(c.value, self.d_in * self.d_out, torch.float32, (self.d_in, self.d_out))
+        S = view(s.value, 1, torch.float64, (1,))
+        return G, C, S, n.value
+
+    def solve(self, lam=1e-3, delta_w=None):
+        """dW = (G + lam I)^-1 C and eps (Eq. 5-6). Synchronises the stream."""
+        if delta_w is None:
+            delta_w = torch.empty((self.d_in, self.d_out), dtype=torch.float32, device=self.device)
+        _require(delta_w, "delta_w", torch.float32, self.device)
+        eps = ctypes.c_double()
+        _check(lib().ispa_solve_modulation(self._handle(), float(lam), _ptr(delta_w), ctypes.byref(eps)),
+               "ispa_solve_modulation")
+        return delta_w, eps.value
+
+    def close(self):
+        if self._h:
+            lib().ispa_stats_destroy(self._h)
+            self._h = ctypes.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,247 @@
+// Host side of libispa: argument validation, key-range arithmetic, the
+// statistics handle over a caller-owned workspace, and kernel launches.
+// Every argument error is reported before anything is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <new>
+#include <stdint.h>
+#include <string.h>
+
+#include "ispa.h"
+#include "ispa_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxDim = 16384;
+constexpr size_t kWsAlign = 256;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Workspace layout of a statistics handle (offsets in bytes, 256-aligned).
+struct Layout {
+  size_t G, C, L, X, R, scalars, status, total;
+};
+
+bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
+  if (d_in < 1 || d_out < 1 || d_in > kMaxDim || d_out > kMaxDim) return false;
+  if (d_in % 8 != 0 || d_out % 8 != 0) return false;
+  if (max_rows < 1 || max_rows > (int64_t)1 << 24) return false;
+  Layout l;
+  size_t off = 0;
+  l.G = off; off = round_up(off + (size_t)d_in * d_in * 4, kWsAlign);
+  l.C = off; off = round_up(off + (size_t)d_in * d_out * 4, kWsAlign);
+  l.L = off; off = round_up(off + (size_t)d_in * d_in * 4, kWsAlign);
+  l.X = off; off = round_up(off + (size_t)max_rows * d_in * 2, kWsAlign);
+  l.R = off; off = round_up(off + (size_t)max_rows * d_out * 2, kWsAlign);
+  l.scalars = off; off = round_up(off + 4 * sizeof(double), kWsAlign);
+  l.status = off; off = round_up(off + sizeof(int), kWsAlign);
+  l.total = off;
+  *out = l;
+  return true;
+}
+
+}  // namespace
+
+struct ispa_stats {
+  uint32_t magic;
+  char* ws;
+  size_t ws_bytes;
+  int32_t d_in, d_out;
+  int64_t max_rows;
+  int64_t n_rows;
+  hipStream_t stream;
+  Layout lay;
+};
+
+static constexpr uint32_t kMagic = 0x49535041u;  // "ISPA"
+
+static bool valid_handle(const ispa_stats* h) { return h != nullptr && h->magic == kMagic; }
+
+extern "C" {
+
+const char* ispa_status_string(int status) {
+  switch (status) {
+    case ISPA_OK: return "ISPA_OK";
+    case ISPA_ERR_INVALID_ARG: return "ISPA_ERR_INVALID_ARG: invalid argument";
+    case ISPA_ERR_UNSUPPORTED: return "ISPA_ERR_UNSUPPORTED: unsupported head_dim or dtype";
+    case ISPA_ERR_NOT_SPD: return "ISPA_ERR_NOT_SPD: G + lambda I is not positive definite";
+    case ISPA_ERR_HIP: return "ISPA_ERR_HIP: HIP runtime or launch failure";
+    case ISPA_ERR_STATE: return "ISPA_ERR_STATE: bad handle or workspace";
+    default: return "ISPA: unknown status";
+  }
+}
+
+int ispa_abi_version(void) { return 100; }
+
+int ispa_attn_chunk(const void* q, const void* k_cache, const void* v_cache, int64_t cache_len,
+                    int64_t window, int64_t sink_len, int32_t n_q, int32_t n_heads, int32_t head_dim,
+                    float scale, float* out, float* lse, float* out_local, float* lse_local,
+                    hipStream_t stream) {
+  if (head_dim != 64 && head_dim != 128) return ISPA_ERR_UNSUPPORTED;
+  if (!q || !k_cache || !v_cache || !out) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return ISPA_ERR_INVALID_ARG;
+  if (out_local && !aligned16(out_local)) return ISPA_ERR_INVALID_ARG;
+  if (((uintptr_t)lse & 3u) || ((uintptr_t)lse_local & 3u)) return ISPA_ERR_INVALID_ARG;
+  if (lse_local && !out_local) return ISPA_ERR_INVALID_ARG;
+  if (n_q < 1 || n_heads < 1 || n_heads > 65535) return ISPA_ERR_INVALID_ARG;
+  if (cache_len < n_q || cache_len > ((int64_t)1 << 31)) return ISPA_ERR_INVALID_ARG;
+  if (window < 1 || sink_len < 0) return ISPA_ERR_INVALID_ARG;
+  if (!(scale == scale) || isinf(scale)) return ISPA_ERR_INVALID_ARG;
+  if ((int64_t)n_heads * head_dim > ((int64_t)1 << 20)) return ISPA_ERR_INVALID_ARG;
+
+  const float s = scale > 0.f ? scale : 1.0f / sqrtf((float)head_dim);
+  ispa::AttnArgs a;
+  a.q = (const uint16_t*)q;
+  a.k = (const uint16_t*)k_cache;
+  a.v = (const uint16_t*)v_cache;
+  a.out = out;
+  a.lse = lse;
+  a.out_local = out_local;
+  a.lse_local = lse_local;
+  a.ld = (int64_t)n_heads * head_dim;
+  a.n_q = n_q;
+  a.n_heads = n_heads;
+  a.scale = s;
+  a.scale_log2 = s * 1.4426950408889634f;
+
+  // Key sets of Sec. 3.4, Eq. 7-8: local = [0, s') U [lo, N), hist = [s', lo).
+  const int64_t N = cache_len;
+  const int64_t s1 = sink_len < N ? sink_len : N;
+  const int64_t lo = N - window > 0 ? N - window : 0;
+  ispa::AttnRanges& r = a.r;
+  if (lo <= s1) {
+    r.begin[0] = 0; r.end[0] = N;
+    r.n_local = 1;
+    r.n_total = 1;
+  } else {
+    int i = 0;
+    if (s1 > 0) { r.begin[i] = 0; r.end[i] = s1; ++i; }
+    r.begin[i] = lo; r.end[i] = N; ++i;
+    r.n_local = i;
+    r.n_total = i;
+    if (out_local) { r.begin[i] = s1; r.end[i] = lo; ++i; r.n_total = i; }
+  }
+  for (int i = r.n_total; i < 3; ++i) { r.begin[i] = 0; r.end[i] = 0; }
+  return ispa::launch_attn_chunk(a, head_dim, stream) == hipSuccess ? ISPA_OK : ISPA_ERR_HIP;
+}
+
+size_t ispa_stats_workspace_bytes(int32_t d_in, int32_t d_out, int64_t max_rows) {
+  Layout l;
+  return layout_of(d_in, d_out, max_rows, &l) ? l.total : 0;
+}
+
+int ispa_stats_create(ispa_stats** handle, void* workspace, size_t workspace_bytes, int32_t d_in,
+                      int32_t d_out, int64_t max_rows, hipStream_t stream) {
+  if (!handle) return ISPA_ERR_INVALID_ARG;
+  *handle = nullptr;
+  Layout l;
+  if (!layout_of(d_in, d_out, max_rows, &l)) return ISPA_ERR_INVALID_ARG;
+  if (!workspace || ((uintptr_t)workspace % kWsAlign) != 0) return ISPA_ERR_INVALID_ARG;
+  if (workspace_bytes < l.total) return ISPA_ERR_STATE;
+  ispa_stats* h = new (std::nothrow) ispa_stats;
+  if (!h) return ISPA_ERR_STATE;
+  h->magic = kMagic;
+  h->ws = (char*)workspace;
+  h->ws_bytes = workspace_bytes;
+  h->d_in = d_in;
+  h->d_out = d_out;
+  h->max_rows = max_rows;
+  h->n_rows = 0;
+  h->stream = stream;
+  h->lay = l;
+  const int rc = ispa_stats_reset(h);
+  if (rc != ISPA_OK) {
+    h->magic = 0;
+    delete h;
+    return rc;
+  }
+  *handle = h;
+  return ISPA_OK;
+}
+
+int ispa_stats_reset(ispa_stats* h) {
+  if (!valid_handle(h)) return ISPA_ERR_STATE;
+  h->n_rows = 0;
+  // G, C (contiguous at the start of the workspace) and the scalars
+  if (ispa::launch_zero(h->ws + h->lay.G, h->lay.L, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  if (ispa::launch_zero(h->ws + h->lay.scalars, 4 * sizeof(double), h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  return ISPA_OK;
+}
+
+int ispa_stats_destroy(ispa_stats* h) {
+  if (!valid_handle(h)) return ISPA_ERR_STATE;
+  h->magic = 0;
+  delete h;
+  return ISPA_OK;
+}
+
+int ispa_stats_views(const ispa_stats* h, float** G, float** C, double** sq_norm_r, int64_t* n_rows) {
+  if (!valid_handle(h)) return ISPA_ERR_STATE;
+  if (G) *G = (float*)(h->ws + h->lay.G);
+  if (C) *C = (float*)(h->ws + h->lay.C);
+  if (sq_norm_r) *sq_norm_r = (double*)(h->ws + h->lay.scalars);
+  if (n_rows) *n_rows = h->n_rows;
+  return ISPA_OK;
+}
+
+int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* y_full,
+                     const void* y_local, int32_t y_dtype, int64_t n_rows) {
+  if (!valid_handle(h)) return ISPA_ERR_STATE;
+  if (x_dtype != ISPA_DTYPE_BF16 && x_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (y_dtype != ISPA_DTYPE_BF16 && y_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (n_rows < 0) return ISPA_ERR_INVALID_ARG;
+  if (n_rows == 0) return ISPA_OK;
+  if (!x || !y_full || !y_local) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(y_full) || !aligned16(y_local)) return ISPA_ERR_INVALID_ARG;
+
+  const size_t xs = x_dtype == ISPA_DTYPE_F32 ? 4 : 2;
+  const size_t ys = y_dtype == ISPA_DTYPE_F32 ? 4 : 2;
+  uint16_t* xb = (uint16_t*)(h->ws + h->lay.X);
+  uint16_t* rb = (uint16_t*)(h->ws + h->lay.R);
+  float* G = (float*)(h->ws + h->lay.G);
+  float* C = (float*)(h->ws + h->lay.C);
+  double* sq = (double*)(h->ws + h->lay.scalars);
+  for (int64_t r0 = 0; r0 < n_rows; r0 += h->max_rows) {
+    const int64_t rows = n_rows - r0 < h->max_rows ? n_rows - r0 : h->max_rows;
+    const char* xp = (const char*)x + (size_t)r0 * h->d_in * xs;
+    const char* yf = (const char*)y_full + (size_t)r0 * h->d_out * ys;
+    const char* yl = (const char*)y_local + (size_t)r0 * h->d_out * ys;
+    // keep the aliasing of x and y_local visible to the kernel for every block
+    const void* xarg = (x == y_local) ? (const void*)yl : (const void*)xp;
+    if (ispa::launch_discrepancy(xarg, x_dtype, yf, yl, y_dtype, rows, h->d_in, h->d_out, xb, rb, sq,
+                                 h->stream) != hipSuccess)
+      return ISPA_ERR_HIP;
+    const uint16_t* xg = x_dtype == ISPA_DTYPE_BF16 ? (const uint16_t*)xp : xb;
+    if (ispa::launch_gram(xg, rb, rows, h->d_in, h->d_out, G, C, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  }
+  h->n_rows += n_rows;
+  return ISPA_OK;
+}
+
+int ispa_solve_modulation(ispa_stats* h, float lambda, float* delta_w, double* eps_out) {
+  if (!valid_handle(h)) return ISPA_ERR_STATE;
+  if (!delta_w || !aligned16(delta_w)) return ISPA_ERR_INVALID_ARG;
+  if (!(lambda >= 0.f) || isinf(lambda)) return ISPA_ERR_INVALID_ARG;
+  ispa::SolveWork w;
+  w.L = (float*)(h->ws + h->lay.L);
+  w.status = (int*)(h->ws + h->lay.status);
+  w.scalars = (double*)(h->ws + h->lay.scalars) + 2;
+  const float* G = (const float*)(h->ws + h->lay.G);
+  const float* C = (const float*)(h->ws + h->lay.C);
+  if (ispa::launch_solve(G, C, h->d_in, h->d_out, lambda, delta_w, w, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  // scalars: [0] s = sum ||R||^2, [1] unused, [2] <dW, C>, [3] ||dW||^2
+  int status = 0;
+  double sc[4] = {0, 0, 0, 0};
+  if (hipMemcpyAsync(&status, w.status, sizeof(int), hipMemcpyDeviceToHost, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  if (hipMemcpyAsync(sc, h->ws + h->lay.scalars, sizeof(sc), hipMemcpyDeviceToHost, h->stream) != hipSuccess)
+    return ISPA_ERR_HIP;
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  if (status != 0) return ISPA_ERR_NOT_SPD;
+  if (eps_out) *eps_out = sc[0] - sc[2] - (double)lambda * sc[3];
+  return ISPA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,113 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments before touching the device."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_00712_amd as ispa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ispa.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ispa_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(ispa.LIB_PATH):
+        pytest.fail("libispa.so missing: run __graft_entry__.build() first")
+    return ispa.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 10, names
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in include/ispa.h but not exported"
+    assert set(names) == set(ispa._SIGNATURES), "binding signatures and header disagree"
+
+
+def test_status_strings(L):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert ispa.status_string(code).startswith("ISPA")
+    assert "unknown" in ispa.status_string(7)
+    assert L.ispa_abi_version() == 100
+
+
+def _attn(L, **kw):
+    args = dict(q=16, k=32, v=48, cache_len=256, window=64, sink=0, n_q=64, heads=2, hd=64, scale=0.0,
+                out=64, lse=128, out_local=0, lse_local=0)
+    args.update(kw)
+    p = lambda v: ctypes.c_void_p(v) if v else ctypes.c_void_p(0)
+    # pointers are fake (never dereferenced): validation must fail first
+    return L.ispa_attn_chunk(p(args["q"]), p(args["k"]), p(args["v"]), args["cache_len"], args["window"],
+                             args["sink"], args["n_q"], args["heads"], args["hd"], args["scale"], p(args["out"]),
+                             p(args["lse"]), p(args["out_local"]), p(args["lse_local"]), p(0))
+
+
+def test_attention_argument_errors(L):
+    E, U = ispa.ISPA_ERR_INVALID_ARG, ispa.ISPA_ERR_UNSUPPORTED
+    assert _attn(L, hd=96) == U
+    assert _attn(L, hd=32) == U
+    assert _attn(L, q=0) == E
+    assert _attn(L, out=0) == E
+    assert _attn(L, k=33) == E                 # misaligned
+    assert _attn(L, out_local=72) == E         # misaligned
+    assert _attn(L, lse=130) == E              # misaligned float
+    assert _attn(L, lse_local=256) == E        # lse_local without out_local
+    assert _attn(L, window=0) == E
+    assert _attn(L, sink=-1) == E
+    assert _attn(L, cache_len=63) == E         # fewer keys than queries
+    assert _attn(L, n_q=0, cache_len=0) == E
+    assert _attn(L, heads=0) == E
+    assert _attn(L, scale=float("nan")) == E
+    assert _attn(L, scale=float("inf")) == E
+
+
+def test_workspace_sizes(L):
+    assert L.ispa_stats_workspace_bytes(0, 8, 1) == 0
+    assert L.ispa_stats_workspace_bytes(12, 8, 1) == 0      # not a multiple of 8
+    assert L.ispa_stats_workspace_bytes(8, 8, 0) == 0
+    assert L.ispa_stats_workspace_bytes(16392, 8, 1) == 0
+    d, m = 1536, 4680
+    b = L.ispa_stats_workspace_bytes(d, d, m)
+    # G, C, L in fp32 plus bf16 X and R staging, each 256-byte aligned
+    assert b >= 3 * d * d * 4 + 2 * m * d * 2
+    assert b % 256 == 0
+
+
+def test_stats_handle_errors(L):
+    h = ctypes.c_void_p(0)
+    assert L.ispa_stats_create(None, ctypes.c_void_p(256), 1 << 20, 8, 8, 1, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_stats_create(ctypes.byref(h), ctypes.c_void_p(0), 1 << 20, 8, 8, 1, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_stats_create(ctypes.byref(h), ctypes.c_void_p(128), 1 << 20, 8, 8, 1, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_stats_create(ctypes.byref(h), ctypes.c_void_p(256), 16, 8, 8, 1, None) == ispa.ISPA_ERR_STATE
+    assert not h.value
+    assert L.ispa_stats_reset(None) == ispa.ISPA_ERR_STATE
+    assert L.ispa_stats_destroy(None) == ispa.ISPA_ERR_STATE
+    assert L.ispa_accum_stats(None, None, 0, None, None, 0, 1) == ispa.ISPA_ERR_STATE
+    assert L.ispa_solve_modulation(None, ctypes.c_float(1e-3), None, None) == ispa.ISPA_ERR_STATE
+    assert L.ispa_stats_views(None, None, None, None, None) == ispa.ISPA_ERR_STATE
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(ispa, "_lib", None)
+    monkeypatch.setattr(ispa, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        ispa.lib()
+
+
+def test_product_never_imports_oracle():
+    pkg = os.path.join(ROOT, "paper_2607_00712_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in src.replace("the oracle", ""), f"{f} mentions the oracle"

@@ -1,0 +1,139 @@
+"""GPU parity of ispa_attn_chunk against the oracle on identical seeded bf16
+inputs (through the C ABI via the ctypes binding)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2607_00712_amd as ispa
+from parity_util import assert_attn, assert_lse, f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def run_and_check(n_q, cache_len, window, sink, heads, hd, dual, wid, capacity=None, q_scale=1.0,
+                  rows=None):
+    print(f"[attn] n_q={n_q} N={cache_len} w={window} s={sink} H={heads} d={hd} dual={dual} "
+          f"wid={wid}", flush=True)
+    q, k, v = synth.chunk_qkv(wid, 0, 0, n_q, cache_len, heads * hd, DEV, q_scale=q_scale,
+                              capacity=capacity)
+    res = ispa.attn_chunk(q, k, v, cache_len, window, heads, sink_len=sink, dual=dual)
+    torch.cuda.synchronize()
+    if rows is None:
+        qn, sel = f64(q), None
+    else:
+        sel = np.asarray(rows)
+        qn = f64(q)
+    ref = oracle.chunk_attention(qn, f64(k[:cache_len]), f64(v[:cache_len]), cache_len, window, heads,
+                                 sink_len=sink, branches=("full", "local") if dual else ("local",),
+                                 query_rows=sel)
+    pick = (lambda t: f64(t)) if sel is None else (lambda t: f64(t)[sel])
+    pick_lse = (lambda t: f64(t)) if sel is None else (lambda t: f64(t)[:, sel])
+    errs = {}
+    if dual:
+        out, lse, out_l, lse_l = res
+        errs["full"] = assert_attn(pick(out), ref["full"][0], "full")
+        assert_lse(pick_lse(lse), ref["full"][1], "full lse")
+        errs["local"] = assert_attn(pick(out_l), ref["local"][0], "local")
+        assert_lse(pick_lse(lse_l), ref["local"][1], "local lse")
+    else:
+        out, lse = res
+        errs["local"] = assert_attn(pick(out), ref["local"][0], "single")
+        assert_lse(pick_lse(lse), ref["local"][1], "single lse")
+    return res, errs
+
+
+# the tiny single-layer workload: 2 heads x 64, chunk of 64 queries, 4 chunks of cache,
+# window of one chunk, with and without a one-chunk sink
+@pytest.mark.parametrize("sink", [0, 64])
+@pytest.mark.parametrize("dual", [False, True])
+def test_tiny_layer(sink, dual):
+    run_and_check(64, 256, 64, sink, 2, 64, dual, wid=1)
+
+
+@pytest.mark.parametrize("case", [
+    # n_q, N, w, s, H, d, dual
+    (100, 333, 97, 13, 3, 128, True),     # ragged everywhere
+    (300, 1000, 200, 0, 2, 128, True),    # several query and key tiles
+    (129, 129, 64, 0, 1, 128, True),      # N == n_q, one query past a tile
+    (64, 640, 1, 0, 2, 64, True),         # single visible key
+    (64, 640, 64, 700, 2, 64, True),      # sink covers the cache
+    (40, 4000, 130, 1, 4, 64, True),      # one sink key, long history
+    (257, 1500, 1500, 0, 2, 128, False),  # F-Layer: window = cache
+    (96, 700, 5000, 0, 2, 128, True),     # window beyond the cache: hist empty
+    (33, 200, 70, 70, 1, 64, False),      # L-Layer with sink, single stream
+])
+def test_ragged_and_degenerate(case):
+    n_q, N, w, s, H, d, dual = case
+    res, _ = run_and_check(n_q, N, w, s, H, d, dual, wid=2)
+    if dual and (N <= w + min(s, N)):
+        out, lse, out_l, lse_l = res
+        # no history: the two streams are the same numbers
+        assert torch.equal(out, out_l) and torch.equal(lse, lse_l)
+
+
+def test_rows_beyond_cache_len_are_not_read():
+    # rows past cache_len hold 1e4 values; any read would wreck parity
+    run_and_check(128, 777, 256, 64, 2, 128, True, wid=3, capacity=1024)
+
+
+def test_sharp_softmax():
+    run_and_check(128, 1024, 300, 0, 2, 128, True, wid=4, q_scale=4.0)
+
+
+def test_without_lse_outputs():
+    q, k, v = synth.chunk_qkv(5, 0, 0, 64, 300, 256, DEV)
+    out, lse = ispa.attn_chunk(q, k, v, 300, 100, 2, need_lse=False)
+    assert lse is None
+    out2, _ = ispa.attn_chunk(q, k, v, 300, 100, 2)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2)
+
+
+def test_deterministic():
+    q, k, v = synth.chunk_qkv(6, 0, 0, 200, 900, 256, DEV)
+    a = ispa.attn_chunk(q, k, v, 900, 300, 2, sink_len=10, dual=True)
+    b = ispa.attn_chunk(q, k, v, 900, 300, 2, sink_len=10, dual=True)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_binding_rejects_bad_tensors():
+    q, k, v = synth.chunk_qkv(7, 0, 0, 64, 256, 128, DEV)
+    with pytest.raises(TypeError):
+        ispa.attn_chunk(q.float(), k, v, 256, 64, 2)
+    with pytest.raises(ValueError):
+        ispa.attn_chunk(q, k, v, 300, 64, 2)
+    with pytest.raises(ispa.IspaError):
+        ispa.attn_chunk(q, k, v, 256, 0, 2)
+
+
+# full-size shapes: sampled query rows checked one by one against the oracle
+SAMPLE_ROWS = [0, 1, 31, 32, 127, 128, 129, 1000, 2047, 2048, 4095, 4096, 4600, 4679]
+
+
+@pytest.mark.parametrize("sink", [0, 4680])
+def test_wan13b_chunk_sampled(sink):
+    # 12 heads x 128, chunk of 4680 queries, 7 chunks of cache, window of 2 chunks
+    run_and_check(4680, 32760, 9360, sink, 12, 128, True, wid=10, rows=SAMPLE_ROWS)
+
+
+def test_14b_chunk_sampled_heads():
+    # 40 heads x 128, 21 chunks of cache; the oracle checks 4 of the 40 heads
+    n_q, N, w, H, d = 4680, 98280, 9360, 40, 128
+    print(f"[attn] 14B-shaped n_q={n_q} N={N} w={w}", flush=True)
+    q, k, v = synth.chunk_qkv(11, 0, 0, n_q, N, H * d, DEV)
+    out, lse, out_l, lse_l = ispa.attn_chunk(q, k, v, N, w, H, dual=True)
+    torch.cuda.synchronize()
+    for h in (0, 13, 26, 39):
+        cols = slice(h * d, (h + 1) * d)
+        ref = oracle.chunk_attention(f64(q[:, cols]), f64(k[:, cols]), f64(v[:, cols]), N, w, 1,
+                                     branches=("full", "local"), query_rows=SAMPLE_ROWS)
+        assert_attn(f64(out[:, cols])[SAMPLE_ROWS], ref["full"][0], f"head {h} full")
+        assert_attn(f64(out_l[:, cols])[SAMPLE_ROWS], ref["local"][0], f"head {h} local")
+        assert_lse(f64(lse[h])[SAMPLE_ROWS], ref["full"][1][0], f"head {h} lse")
