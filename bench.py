@@ -57,7 +57,7 @@ def flops(w):
     return f
 
 
-def gpu_run(w, steps, warmup):
+def gpu_run(w, steps, warmup, only="all"):
     import synth
     import paper_2607_00712_amd as ispa
 
@@ -75,21 +75,27 @@ def gpu_run(w, steps, warmup):
     stats = ispa.Stats(D, D, max_rows=w["n_q"], device=dev)
     dw = torch.empty((D, D), dtype=torch.float32, device=dev)
 
+    run = {p: only in ("all", p) for p in ("attn_dual", "attn_local", "accum_stats", "solve")}
+
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"], dual=True,
-                        out=out, lse=lse, out_local=out_l, lse_local=lse_l)
+        if run["attn_dual"]:
+            ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"], dual=True,
+                            out=out, lse=lse, out_local=out_l, lse_local=lse_l)
         if ev is not None:
             ev[1].record()
-        ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"],
-                        out=out_L, lse=lse_L)
+        if run["attn_local"]:
+            ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"],
+                            out=out_L, lse=lse_L)
         if ev is not None:
             ev[2].record()
-        stats.accum(out_l, out, out_l)
+        if run["accum_stats"]:
+            stats.accum(out_l, out, out_l)
         if ev is not None:
             ev[3].record()
-        stats.solve(w["lam"], delta_w=dw)
+        if run["solve"]:
+            stats.solve(w["lam"], delta_w=dw)
         if ev is not None:
             ev[4].record()
 
@@ -169,6 +175,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="1.3b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve"], default="all",
+                    help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the ISPA hot path here has no multi-GPU "
@@ -176,7 +184,7 @@ def main():
         sys.exit(2)
     w = WORKLOADS[args.workload]
     f = flops(w)
-    ms_step, avg = gpu_run(w, args.steps, args.warmup)
+    ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only)
     total = sum(f.values())
     value = total / (ms_step * 1e-3) / 1e12
     attn_ms = avg["attn_dual"]
@@ -223,7 +231,9 @@ def main():
             "flop": {k2: v2 for k2, v2 in f.items()},
         },
     }
-    if not args.no_cpu_baseline and args.workload == "1.3b":
+    if args.only != "all":
+        rec["only"] = args.only
+    if not args.no_cpu_baseline and args.workload == "1.3b" and args.only == "all":
         rec["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(rec), flush=True)
 

@@ -52,6 +52,13 @@ def build(verbose=False):
         raise subprocess.CalledProcessError(res.returncode, cmd, out)
     if verbose and out.strip():
         print(out)
+    # the host pass can silently drop a kernel's launch stub (the device code
+    # still builds): refuse a library with unresolved stubs
+    nm = subprocess.run(["nm", "-D", "--undefined-only", tmp], stdout=subprocess.PIPE, text=True)
+    missing = [ln for ln in nm.stdout.splitlines() if "__device_stub" in ln]
+    if missing:
+        os.remove(tmp)
+        raise RuntimeError("libispa.so has unresolved kernel stubs:\n" + "\n".join(missing))
     os.replace(tmp, LIB)
     return LIB
 

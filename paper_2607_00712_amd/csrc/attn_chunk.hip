@@ -10,12 +10,21 @@
 //
 // Work decomposition
 //   workgroup = 4 waves = 128 queries of one head; each wave owns 32 queries.
-//   Keys are visited in tiles of 64 rows, staged in LDS (double buffered, one
-//   barrier per tile). Only tiles that intersect the key set are visited; the
-//   tile at the end of each contiguous range is masked element-wise.
+//   Keys are visited in tiles of 64 rows. Only tiles that intersect the key set
+//   are visited; the tile at the end of each contiguous range is masked
+//   element-wise.
+// Staging: K and V tiles go straight from HBM to LDS with buffer loads
+//   (buffer_load_dwordx4 ... lds), double buffered, one barrier per tile. The
+//   buffer descriptor of a tile starts at its first key and covers only its
+//   valid rows, so rows past the end of a range read as zero in hardware. A
+//   direct load writes 64 consecutive 16-byte slots per wave, so LDS rows are
+//   unpadded and the 16-byte chunk index is XOR-swizzled with the row
+//   (slot = chunk ^ row) to keep the MFMA operand reads and the transpose reads
+//   free of bank conflicts.
 //
-// Per tile and wave (bf16 MFMA 32x32x16, fp32 accumulation):
-//   S^T[64 keys x 32 q] = K_tile . Q^T   -- A = K rows from LDS, B = Q^T in VGPRs.
+// Per tile and wave (bf16 MFMA 32x32x16, fp32 accumulation), in two halves of
+// 32 keys, each a complete online-softmax step:
+//   S^T[32 keys x 32 q] = K_half . Q^T   -- A = K rows from LDS, B = Q^T in VGPRs.
 //     The accumulator layout gives each lane the scores of ONE query (lane%32)
 //     for 32 keys; the other 32 keys of that query sit in lane^32. Row max
 //     needs one cross-lane exchange; row sums stay per lane until the end.
@@ -50,16 +59,39 @@ constexpr int kXcds = 8;
 
 template <int D>
 struct Cfg {
-  static constexpr int kStride = D + 8;    // K row stride in LDS (elements)
-  static constexpr int vStride = D + 16;   // V row stride in LDS (elements)
-  static constexpr int kTile = kBk * kStride;
-  static constexpr int vTile = kBk * vStride;
+  static constexpr int rowBytes = D * 2;                     // unpadded LDS row
   static constexpr int chunksPerRow = D / 8;                 // 16-byte chunks
-  static constexpr int chunksPerThread = kBk * chunksPerRow / kThreads;
+  static constexpr int swz = chunksPerRow - 1;               // XOR mask
+  static constexpr int tileBytes = kBk * rowBytes;           // one K or V tile
+  static constexpr int loadsPerThread = kBk * chunksPerRow / kThreads;
   static constexpr int kSlices = D / 16;                     // QK^T k-steps
   static constexpr int dBlocks = D / 32;                     // O^T row blocks
   static_assert(kBk * chunksPerRow % kThreads == 0, "tile load split");
 };
+
+// XOR swizzles of the 16-byte chunk index, per tile and row.
+// K is read as MFMA A operands: 16 lanes read 16 consecutive rows at the same
+// logical chunk, so chunk ^ (row mod 16) spreads them over all banks.
+// V is read with transpose reads: 16 lanes read 4 consecutive rows x 2 adjacent
+// chunks, and the two 16-lane groups that share a lane half read the next two
+// chunks of the same rows; chunk ^ (4 * (row mod 4)) gives those 32 lanes 16
+// distinct chunk positions, and the extra ^2 for rows 4..7 (mod 8) separates
+// the other lane half.
+template <int D>
+__device__ __forceinline__ int swz_k(int row) { return row & Cfg<D>::swz; }
+template <int D>
+__device__ __forceinline__ int swz_v(int row) {
+  return D == 128 ? ((4 * (row & 3)) ^ (2 * ((row >> 2) & 1))) : (row & Cfg<D>::swz);
+}
+// byte offset of logical chunk `c` of row `row` for a given swizzle value
+template <int D>
+__device__ __forceinline__ int chunk_off(int row, int c, int sw) {
+  return row * Cfg<D>::rowBytes + ((c ^ sw) << 4);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, nbytes, 0x00020000);
+}
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -67,8 +99,37 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((ISPA_LDS i16x4*)(p));
+// LDS transpose reads of one 16-key slice for all dBlocks column blocks (two
+// reads per block), issued as inline asm and completed by an explicit wait that
+// is tied to their results. Through the builtin the compiler cannot tell these
+// reads from reads of the buffer the direct loads are filling, and would wait
+// for those loads (vmcnt 0) before every slice. LDS operations complete in
+// order, so the compiler's own lgkmcnt waits stay correct around these.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)(uintptr_t)(ISPA_LDS const char*)p;
+}
+template <int NB>
+__device__ __forceinline__ void lds_read_tr_slice(const char* base, const int (*off)[NB], bf16x8* out) {
+  u32x2 r0[NB], r1[NB];
+#pragma unroll
+  for (int db = 0; db < NB; ++db) {
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r0[db]) : "v"(lds_addr(base + off[0][db])));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r1[db]) : "v"(lds_addr(base + off[1][db])));
+  }
+#pragma unroll
+  for (int db = 0; db < NB; ++db) asm volatile("" : "+v"(r0[db]), "+v"(r1[db]));
+  if constexpr (NB == 4) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(r0[0]), "+v"(r1[0]), "+v"(r0[1]), "+v"(r1[1]), "+v"(r0[2]), "+v"(r1[2]), "+v"(r0[3]),
+                   "+v"(r1[3]));
+  } else {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r0[0]), "+v"(r1[0]), "+v"(r0[1]), "+v"(r1[1]));
+  }
+#pragma unroll
+  for (int db = 0; db < NB; ++db) {
+    const u32x4 w{r0[db][0], r0[db][1], r1[db][0], r1[db][1]};
+    out[db] = __builtin_bit_cast(bf16x8, w);
+  }
 }
 
 // Tile t of the flattened range list: first key and number of valid keys.
@@ -85,10 +146,31 @@ __device__ __forceinline__ void tile_of(const AttnRanges& r, int tb1, int tb2, i
   nvalid = left < kBk ? (int)left : kBk;
 }
 
+// Direct HBM -> LDS loads of one K tile and one V tile (kBk rows starting at
+// element offset `base`, `nv` of them valid) into dst = [K tile | V tile].
+// (A plain function: the host compilation pass drops a kernel whose lambdas
+// use the LDS-load builtin.)
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_chunk_kernel(AttnArgs a, int q_tiles) {
+__device__ __forceinline__ void stage_tile(const AttnArgs& a, int64_t base, int nv, char* dst,
+                                           const int* voffk, const int* voffv, int wave) {
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (C::kTile + C::vTile)];
+  const int nbytes = (int)(((int64_t)(nv - 1) * a.ld + D) * 2);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(a.k + base, nbytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(a.v + base, nbytes);
+#pragma unroll
+  for (int q = 0; q < C::loadsPerThread; ++q) {
+    const int wslot = (q * kWaves + wave) * 64 * 16;  // wave-uniform LDS destination
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (ISPA_LDS void*)(dst + wslot), 16, voffk[q], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (ISPA_LDS void*)(dst + C::tileBytes + wslot), 16, voffv[q], 0,
+                                             0, 0);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_kernel(AttnArgs a,
+                                                                                                  int q_tiles) {
+  using C = Cfg<D>;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * C::tileBytes];  // [buf][K|V]
 
   // ---- XCD-aware work mapping ------------------------------------------
   const int n_work = q_tiles * a.n_heads;
@@ -139,39 +221,41 @@ __global__ __launch_bounds__(kThreads) void attn_chunk_kernel(AttnArgs a, int q_
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  // ---- global -> register -> LDS staging ------------------------------------------
-  u32x4 kreg[C::chunksPerThread], vreg[C::chunksPerThread];
-  auto gload = [&](int t) {
+  // ---- HBM -> LDS staging ------------------------------------------------
+  // Load q of this thread covers 16-byte slot (q * kWaves + wave) * 64 + lane of
+  // the tile: row = slot / chunksPerRow, stored chunk = slot % chunksPerRow,
+  // which holds logical chunk (stored ^ (row & swz)) of that key row.
+  int voffk[C::loadsPerThread], voffv[C::loadsPerThread];
+#pragma unroll
+  for (int q = 0; q < C::loadsPerThread; ++q) {
+    const int slot = (q * kWaves + wave) * 64 + lane;
+    const int row = slot / C::chunksPerRow;
+    const int stored = slot % C::chunksPerRow;
+    voffk[q] = (int)((row * ld + (stored ^ swz_k<D>(row)) * 8) * 2);
+    voffv[q] = (int)((row * ld + (stored ^ swz_v<D>(row)) * 8) * 2);
+  }
+  auto gload = [&](int t, int buf) {
     int64_t key0;
     int nv;
     tile_of(a.r, tb1, tb2, t, key0, nv);
-#pragma unroll
-    for (int c = 0; c < C::chunksPerThread; ++c) {
-      const int idx = tid + c * kThreads;
-      const int row = idx / C::chunksPerRow;
-      const int col = (idx % C::chunksPerRow) * 8;
-      if (row < nv) {
-        const int64_t off = (key0 + row) * ld + hoff + col;
-        kreg[c] = *(const u32x4*)(a.k + off);
-        vreg[c] = *(const u32x4*)(a.v + off);
-      } else {
-        kreg[c] = u32x4{0, 0, 0, 0};
-        vreg[c] = u32x4{0, 0, 0, 0};
-      }
-    }
+    stage_tile<D>(a, key0 * ld + hoff, nv, smem + buf * 2 * C::tileBytes, voffk, voffv, wave);
   };
-  auto sstore = [&](int buf) {
-    uint16_t* ks = smem + buf * (C::kTile + C::vTile);
-    uint16_t* vs = ks + C::kTile;
+
+  // per-lane LDS byte offsets of the MFMA operands (tile-relative)
+  int koff[C::kSlices];
 #pragma unroll
-    for (int c = 0; c < C::chunksPerThread; ++c) {
-      const int idx = tid + c * kThreads;
-      const int row = idx / C::chunksPerRow;
-      const int col = (idx % C::chunksPerRow) * 8;
-      *(u32x4*)(ks + row * C::kStride + col) = kreg[c];
-      *(u32x4*)(vs + row * C::vStride + col) = vreg[c];
+  for (int kk = 0; kk < C::kSlices; ++kk) koff[kk] = chunk_off<D>(ql, 2 * kk + hh, swz_k<D>(ql));
+  const int g = lane >> 4;
+  const int sl = lane & 15;
+  int voffr[2][C::dBlocks];
+#pragma unroll
+  for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+    for (int db = 0; db < C::dBlocks; ++db) {
+      const int row = 8 * h2 + 4 * (g >> 1) + (sl >> 2);
+      const int chunk = 4 * db + 2 * (g & 1) + ((sl & 3) >> 1);
+      voffr[h2][db] = chunk_off<D>(row, chunk, swz_v<D>(row)) + ((sl & 1) << 3);
     }
-  };
 
   auto finish = [&](float* out, float* lse) {
     const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -194,10 +278,8 @@ __global__ __launch_bounds__(kThreads) void attn_chunk_kernel(AttnArgs a, int q_
     }
   };
 
-  if (n_tiles > 0) {
-    gload(0);
-    sstore(0);
-  }
+  if (n_tiles > 0) gload(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
   __syncthreads();
 
   for (int t = 0; t < n_tiles; ++t) {
@@ -206,85 +288,74 @@ __global__ __launch_bounds__(kThreads) void attn_chunk_kernel(AttnArgs a, int q_
     int64_t key0;
     int nv;
     tile_of(a.r, tb1, tb2, t, key0, nv);
-    if (t + 1 < n_tiles) gload(t + 1);
+    if (t + 1 < n_tiles) gload(t + 1, buf ^ 1);
 
-    const uint16_t* ks = smem + buf * (C::kTile + C::vTile);
-    const uint16_t* vs = ks + C::kTile;
+    const char* ks = smem + buf * 2 * C::tileBytes;
+    const char* vs = ks + C::tileBytes;
 
-    // S^T = K . Q^T for two 32-key blocks
-    f32x16 s[2];
+    // The tile is processed as two halves of 32 keys; each half is a complete
+    // online-softmax step (scores, max, lazy rescale, exp, P.V), which keeps
+    // only 16 score registers live.
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-      s[b] = f32x16{};
-      const uint16_t* kp = ks + (32 * b + ql) * C::kStride + 8 * hh;
+      // S^T = K . Q^T for keys 32b .. 32b+31 (rows 32b + ql share the swizzle of row ql)
+      f32x16 sc = f32x16{};
+      const char* kp = ks + 32 * b * C::rowBytes;
 #pragma unroll
       for (int kk = 0; kk < C::kSlices; ++kk) {
-        const bf16x8 kf = *(const bf16x8*)(kp + 16 * kk);
-        s[b] = mfma32(kf, qf[kk], s[b]);
+        const bf16x8 kf = *(const bf16x8*)(kp + koff[kk]);
+        sc = mfma32(kf, qf[kk], sc);
       }
-    }
-
-    // mask keys beyond the end of a range (only the last tile of each range)
-    if (nv < kBk) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
+      // mask keys beyond the end of a range (only the last tile of each range)
+      if (nv < 32 * (b + 1)) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = 32 * b + 8 * (r >> 2) + 4 * hh + (r & 3);
-          if (key >= nv) s[b][r] = -INFINITY;
+          if (key >= nv) sc[r] = -INFINITY;
         }
-    }
-
-    // online softmax
-    float tmax = s[0][0];
+      }
+      float tmax = fmaxf(sc[0], sc[1]);
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+      for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, sc[r]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      // O and l are rescaled only when some row's running max grew: after the
+      // first few tiles most halves skip the 64 multiplies. The reference stays
+      // the exact running max, so the largest weight of a row is exactly 1 and
+      // carries no bf16 rounding error (a stale reference would put rounding
+      // error on the dominant terms).
+      if (__any(tmax > m_run)) {
+        const float m_new = fmaxf(m_run, tmax);
+        const float alpha = exp2_hw((m_run - m_new) * a.scale_log2);
+        l_run *= alpha;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[b][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = exp2_hw((m_run - m_new) * a.scale_log2);
-    const float mc = m_new * a.scale_log2;
-    float psum = 0.f;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
+        for (int db = 0; db < C::dBlocks; ++db) acc[db] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = m_run * a.scale_log2;
+      float psum = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2_hw(fmaf(s[b][r], a.scale_log2, -mc));
-        s[b][r] = p;
+        const float p = exp2_hw(fmaf(sc[r], a.scale_log2, -mc));
+        sc[r] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < C::dBlocks; ++db) acc[db] *= alpha;
-
-    // O^T += V^T . P^T over four 16-key slices
-    const int g = lane >> 4;
-    const int sl = lane & 15;
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
+      l_run += psum;
+      // O^T += V^T . P^T over the two 16-key slices of this half
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) {
         bf16x8 pf;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[b][8 * t2 + e];
-        const int slice = 2 * b + t2;
-        const uint16_t* vp0 = vs + (16 * slice + 4 * (g >> 1) + (sl >> 2)) * C::vStride +
-                              16 * (g & 1) + 4 * (sl & 3);
-        const uint16_t* vp1 = vp0 + 8 * C::vStride;
+        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sc[8 * t2 + e];
+        // rows 16 * slice + ...: both swizzles repeat every 16 rows
+        const char* vp = vs + 16 * (2 * b + t2) * C::rowBytes;
+        bf16x8 vf[C::dBlocks];
+        lds_read_tr_slice<C::dBlocks>(vp, voffr, vf);
 #pragma unroll
-        for (int db = 0; db < C::dBlocks; ++db) {
-          const i16x4 v0 = lds_read_tr(vp0 + 32 * db);
-          const i16x4 v1 = lds_read_tr(vp1 + 32 * db);
-          const bf16x8 vf = __builtin_bit_cast(
-              bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-          acc[db] = mfma32(vf, pf, acc[db]);
-        }
+        for (int db = 0; db < C::dBlocks; ++db) acc[db] = mfma32(vf[db], pf, acc[db]);
       }
     }
 
-    if (t + 1 < n_tiles) sstore(buf ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct loads have landed
     __syncthreads();
   }
 

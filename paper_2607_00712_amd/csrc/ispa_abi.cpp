@@ -22,7 +22,7 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Workspace layout of a statistics handle (offsets in bytes, 256-aligned).
 struct Layout {
-  size_t G, C, L, X, R, scalars, status, total;
+  size_t G, C, L, W, Dinv, X, R, scalars, status, total;
 };
 
 bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
@@ -34,6 +34,8 @@ bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
   l.G = off; off = round_up(off + (size_t)d_in * d_in * 4, kWsAlign);
   l.C = off; off = round_up(off + (size_t)d_in * d_out * 4, kWsAlign);
   l.L = off; off = round_up(off + (size_t)d_in * d_in * 4, kWsAlign);
+  l.W = off; off = round_up(off + (size_t)d_in * d_out * 4, kWsAlign);
+  l.Dinv = off; off = round_up(off + ispa::solve_dinv_bytes(d_in), kWsAlign);
   l.X = off; off = round_up(off + (size_t)max_rows * d_in * 2, kWsAlign);
   l.R = off; off = round_up(off + (size_t)max_rows * d_out * 2, kWsAlign);
   l.scalars = off; off = round_up(off + 4 * sizeof(double), kWsAlign);
@@ -227,6 +229,8 @@ int ispa_solve_modulation(ispa_stats* h, float lambda, float* delta_w, double* e
   if (!(lambda >= 0.f) || isinf(lambda)) return ISPA_ERR_INVALID_ARG;
   ispa::SolveWork w;
   w.L = (float*)(h->ws + h->lay.L);
+  w.work = (float*)(h->ws + h->lay.W);
+  w.dinv = (float*)(h->ws + h->lay.Dinv);
   w.status = (int*)(h->ws + h->lay.status);
   w.scalars = (double*)(h->ws + h->lay.scalars) + 2;
   const float* G = (const float*)(h->ws + h->lay.G);

@@ -60,9 +60,12 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
 // ---- solve (solve.hip) ----
 struct SolveWork {
   float* L;          // [d, d] factor (lower triangle)
+  float* work;       // [d, d_out] right-hand side being reduced
+  float* dinv;       // [ceil(d/64), 64, 64] inverses of the diagonal blocks of L
   int* status;       // device int: 0 ok, 1 not SPD
   double* scalars;   // device: [0] <dW, C>, [1] ||dW||^2
 };
+size_t solve_dinv_bytes(int d);
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda,
                         float* delta_w, const SolveWork& w, hipStream_t stream);
 
