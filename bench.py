@@ -43,6 +43,21 @@ WORKLOADS = {
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0
 
+# HBM bytes per launch of the dual-stream attention kernel, from rocprofv3
+# FETCH_SIZE and WRITE_SIZE scaled by the plain-copy calibration
+# (profiles/attn_chunk_wan13b_dual.md, profiles/hbm_copy_calibration.md). Valid
+# only for the kernel source they were taken on; reported as null otherwise.
+MEASURED_TRAFFIC = {
+    "1.3b": {"attn_chunk_sha256_16": "83849adac12fa8fe", "bytes_per_launch": 528.9e6},
+}
+
+
+def attn_source_hash():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2607_00712_amd", "csrc", "attn_chunk.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
 
 def flops(w):
     D = w["heads"] * w["head_dim"]
@@ -120,6 +135,25 @@ def gpu_run(w, steps, warmup, only="all"):
     return ms_step, avg
 
 
+def hbm_copy(steps, warmup, nbytes=1 << 30):
+    """A plain 1 GiB device-to-device copy (torch's copy kernel), the yardstick
+    for the HBM byte counters: FETCH_SIZE / WRITE_SIZE of this copy against the
+    known 1 GiB read and 1 GiB written give the counters' scale."""
+    dev = torch.device("cuda", 0)
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"only": "hbm_copy", "bytes_read": nbytes, "bytes_written": nbytes, "ms": round(ms, 4),
+            "GB/s": round(2 * nbytes / ms / 1e6, 1)}
+
+
 def cpu_baseline(w, budget_rows=512):
     """The oracle on a bounded sample of one step, scaled to TFLOP/s."""
     import numpy as np
@@ -175,19 +209,25 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="1.3b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve"], default="all",
+    ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy"],
+                    default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the ISPA hot path here has no multi-GPU "
               "path (heads or layers would shard with no exchange; see DESIGN.md).", file=sys.stderr)
         sys.exit(2)
+    if args.only == "hbm_copy":
+        print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)
+        return
     w = WORKLOADS[args.workload]
     f = flops(w)
     ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only)
     total = sum(f.values())
     value = total / (ms_step * 1e-3) / 1e12
     attn_ms = avg["attn_dual"]
+    mt = MEASURED_TRAFFIC.get(args.workload)
+    traffic = mt["bytes_per_launch"] if mt and mt["attn_chunk_sha256_16"] == attn_source_hash() else None
     achieved = f["attn_dual"] / (attn_ms * 1e-3) / 1e12
     rec = {
         "metric": "chunk attention TFLOP/s (F vs L layer) + stats/solve ms, 1.3B/14B shapes",
@@ -217,7 +257,8 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
         },
         "breakdown": {
             "attn_dual_ms": round(avg["attn_dual"], 4),
