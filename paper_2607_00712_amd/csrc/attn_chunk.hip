@@ -99,37 +99,66 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// LDS transpose reads of one 16-key slice for all dBlocks column blocks (two
-// reads per block), issued as inline asm and completed by an explicit wait that
-// is tied to their results. Through the builtin the compiler cannot tell these
-// reads from reads of the buffer the direct loads are filling, and would wait
-// for those loads (vmcnt 0) before every slice. LDS operations complete in
-// order, so the compiler's own lgkmcnt waits stay correct around these.
+// V^T operands come from LDS transpose reads issued as inline asm and completed
+// by explicit waits tied to their results. Through the builtin the compiler
+// cannot tell these reads from reads of the buffer the direct loads are filling,
+// and would wait for those loads (vmcnt 0) before every slice. LDS operations
+// complete in order, so a wait for "at most n outstanding" retires exactly the
+// reads issued before the last n, and the compiler's own lgkmcnt waits, which
+// do not count these reads, only become more conservative.
 __device__ __forceinline__ uint32_t lds_addr(const char* p) {
   return (uint32_t)(uintptr_t)(ISPA_LDS const char*)p;
 }
-template <int NB>
-__device__ __forceinline__ void lds_read_tr_slice(const char* base, const int (*off)[NB], bf16x8* out) {
-  u32x2 r0[NB], r1[NB];
+
+// The 2 x NB transpose reads of one 16-key slice; IMM is the compile-time byte
+// offset of the slice (buffer, V tile, slice rows) from the per-lane addresses.
+template <int NB, int IMM>
+__device__ __forceinline__ void tr_issue(const uint32_t (&addr)[2][NB], u32x2 (&r)[2][NB]) {
 #pragma unroll
   for (int db = 0; db < NB; ++db) {
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r0[db]) : "v"(lds_addr(base + off[0][db])));
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r1[db]) : "v"(lds_addr(base + off[1][db])));
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r[0][db]) : "v"(addr[0][db]), "i"(IMM));
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r[1][db]) : "v"(addr[1][db]), "i"(IMM));
   }
-#pragma unroll
-  for (int db = 0; db < NB; ++db) asm volatile("" : "+v"(r0[db]), "+v"(r1[db]));
+}
+
+// Wait until at most N LDS operations are outstanding, then hand out the
+// slice's operands.
+template <int N, int NB>
+__device__ __forceinline__ void tr_wait(u32x2 (&r)[2][NB], bf16x8* out) {
   if constexpr (NB == 4) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(r0[0]), "+v"(r1[0]), "+v"(r0[1]), "+v"(r1[1]), "+v"(r0[2]), "+v"(r1[2]), "+v"(r0[3]),
-                   "+v"(r1[3]));
+    asm volatile("s_waitcnt lgkmcnt(%8)"
+                 : "+v"(r[0][0]), "+v"(r[1][0]), "+v"(r[0][1]), "+v"(r[1][1]), "+v"(r[0][2]), "+v"(r[1][2]),
+                   "+v"(r[0][3]), "+v"(r[1][3])
+                 : "i"(N));
   } else {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r0[0]), "+v"(r1[0]), "+v"(r0[1]), "+v"(r1[1]));
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r[0][0]), "+v"(r[1][0]), "+v"(r[0][1]), "+v"(r[1][1]) : "i"(N));
   }
 #pragma unroll
   for (int db = 0; db < NB; ++db) {
-    const u32x4 w{r0[db][0], r0[db][1], r1[db][0], r1[db][1]};
+    const u32x4 w{r[0][db][0], r[0][db][1], r[1][db][0], r[1][db][1]};
     out[db] = __builtin_bit_cast(bf16x8, w);
   }
+}
+
+// Lane-pair (l, l ^ 32) exchange with v_permlane32_swap: it swaps the upper 32
+// lanes of its first operand with the lower 32 lanes of its second, so with
+// A = B = x in two registers it leaves A = [x_lo, x_lo] and B = [x_hi, x_hi].
+// Written as inline asm with two in/out operands: the builtin's second result
+// was observed to be read back from the first operand's register.
+__device__ __forceinline__ void pair_halves(float x, float& lo, float& hi) {
+  lo = x;
+  hi = x;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(lo), "+v"(hi));
+}
+__device__ __forceinline__ float l_run_total(float x) {
+  float lo, hi;
+  pair_halves(x, lo, hi);
+  return lo + hi;
+}
+__device__ __forceinline__ float pair_max(float x) {
+  float lo, hi;
+  pair_halves(x, lo, hi);
+  return fmaxf(lo, hi);
 }
 
 // Tile t of the flattened range list: first key and number of valid keys.
@@ -166,6 +195,135 @@ __device__ __forceinline__ void stage_tile(const AttnArgs& a, int64_t base, int 
   }
 }
 
+// Per-wave state of the online softmax and the per-lane constants of the loop.
+template <int D>
+struct Wave {
+  using C = Cfg<D>;
+  f32x16 acc[C::dBlocks];      // O^T, one 32 x 32 block per 32 head dims
+  float m_run;                 // running max (raw score units) of this lane's query
+  float l_run;                 // running sum of p (this lane's half of the keys)
+  bf16x8 qf[C::kSlices];       // Q^T operand
+  int koff[C::kSlices];        // K operand byte offsets inside a tile
+  uint32_t vaddr[2][C::dBlocks];  // V transpose-read LDS addresses (buffer 0, slice 0)
+  int voffk[C::loadsPerThread], voffv[C::loadsPerThread];  // direct-load offsets
+};
+
+struct Loop {
+  int tb1, tb2, n_tiles, n_tiles_local, hoff, wave, hh;
+  bool dual;
+};
+
+template <int D>
+__device__ __forceinline__ void finish(const AttnArgs& a, Wave<D>& w, const Loop& L, int qrow, int head,
+                                       float* out, float* lse) {
+  using C = Cfg<D>;
+  const float l_tot = l_run_total(w.l_run);
+  const float inv = 1.0f / l_tot;
+  if (qrow < a.n_q) {
+    float* op = out + (int64_t)qrow * a.ld + L.hoff + 4 * L.hh;
+#pragma unroll
+    for (int db = 0; db < C::dBlocks; ++db) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x4 o;
+        o[0] = w.acc[db][4 * i + 0] * inv;
+        o[1] = w.acc[db][4 * i + 1] * inv;
+        o[2] = w.acc[db][4 * i + 2] * inv;
+        o[3] = w.acc[db][4 * i + 3] * inv;
+        *(f32x4*)(op + 32 * db + 8 * i) = o;
+      }
+    }
+    if (lse != nullptr && L.hh == 0) lse[(int64_t)head * a.n_q + qrow] = w.m_run * a.scale + logf(l_tot);
+  }
+}
+
+// One 32-key online-softmax step: keys 32B .. 32B+31 of the tile in LDS buffer BUF.
+template <int D, int BUF, int B>
+__device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const Loop& L, const char* smem, int nv) {
+  using C = Cfg<D>;
+  constexpr int kBase = BUF * 2 * C::tileBytes + 32 * B * C::rowBytes;
+  constexpr int vBase = BUF * 2 * C::tileBytes + C::tileBytes;
+  // S^T = K . Q^T (rows 32B + ql share the swizzle of row ql)
+  f32x16 sc = f32x16{};
+#pragma unroll
+  for (int kk = 0; kk < C::kSlices; ++kk) {
+    const bf16x8 kf = *(const bf16x8*)(smem + kBase + w.koff[kk]);
+    sc = mfma32(kf, w.qf[kk], sc);
+  }
+  // V^T operands of this half's two 16-key slices, in flight during the softmax
+  u32x2 v0[2][C::dBlocks], v1[2][C::dBlocks];
+  tr_issue<C::dBlocks, vBase + 16 * (2 * B) * C::rowBytes>(w.vaddr, v0);
+  tr_issue<C::dBlocks, vBase + 16 * (2 * B + 1) * C::rowBytes>(w.vaddr, v1);
+  // keys past the end of a range (only in the last tile of each range)
+  if (nv < 32 * (B + 1)) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = 32 * B + 8 * (r >> 2) + 4 * L.hh + (r & 3);
+      if (key >= nv) sc[r] = -INFINITY;
+    }
+  }
+  float tmax = fmaxf(sc[0], sc[1]);
+#pragma unroll
+  for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, sc[r]);
+  tmax = pair_max(tmax);
+  // O and l are rescaled only when some row's running max grew: after the
+  // first few tiles most steps skip the multiplies. The reference stays the
+  // exact running max, so the largest weight of a row is exactly 1 and carries
+  // no bf16 rounding error (a stale reference would put rounding error on the
+  // dominant terms).
+  if (__any(tmax > w.m_run)) {
+    const float m_new = fmaxf(w.m_run, tmax);
+    const float alpha = exp2_hw((w.m_run - m_new) * a.scale_log2);
+    w.l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < C::dBlocks; ++db) w.acc[db] *= alpha;
+    w.m_run = m_new;
+  }
+  const float mc = w.m_run * a.scale_log2;
+  float psum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float p = exp2_hw(fmaf(sc[r], a.scale_log2, -mc));
+    sc[r] = p;
+    psum += p;
+  }
+  w.l_run += psum;
+  bf16x8 pf0, pf1;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    pf0[e] = (__bf16)sc[e];
+    pf1[e] = (__bf16)sc[8 + e];
+  }
+  // O^T += V^T . P^T over the two slices
+  bf16x8 vf[C::dBlocks];
+  tr_wait<2 * C::dBlocks, C::dBlocks>(v0, vf);
+#pragma unroll
+  for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf0, w.acc[db]);
+  tr_wait<0, C::dBlocks>(v1, vf);
+#pragma unroll
+  for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf1, w.acc[db]);
+}
+
+// One 64-key tile from LDS buffer BUF; the next tile's direct loads into the
+// other buffer are issued first.
+template <int D, int BUF>
+__device__ __forceinline__ void tile_step(const AttnArgs& a, Wave<D>& w, const Loop& L, char* smem, int t) {
+  using C = Cfg<D>;
+  int64_t key0;
+  int nv;
+  tile_of(a.r, L.tb1, L.tb2, t, key0, nv);
+  if (t + 1 < L.n_tiles) {
+    int64_t k1;
+    int n1;
+    tile_of(a.r, L.tb1, L.tb2, t + 1, k1, n1);
+    stage_tile<D>(a, k1 * a.ld + L.hoff, n1, smem + (BUF ^ 1) * 2 * C::tileBytes, w.voffk, w.voffv, L.wave);
+  }
+  half_step<D, BUF, 0>(a, w, L, smem, nv);
+  half_step<D, BUF, 1>(a, w, L, smem, nv);
+  __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct loads have landed
+  __syncthreads();
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_kernel(AttnArgs a,
                                                                                                   int q_tiles) {
@@ -183,184 +341,83 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  Loop L;
+  L.wave = tid >> 6;
+  L.hh = lane >> 5;  // lane half
+  L.hoff = head * D;
   const int ql = lane & 31;  // this lane's query within the wave
-  const int hh = lane >> 5;  // lane half
-  const int64_t ld = a.ld;
-  const int hoff = head * D;
-  const int qrow = qtile * kBq + wave * kBqWave + ql;
-  const bool q_ok = qrow < a.n_q;
+  const int qrow = qtile * kBq + L.wave * kBqWave + ql;
 
+  Wave<D> w;
   // ---- Q^T operand, resident for the whole key loop ------------------------
-  bf16x8 qf[C::kSlices];
   {
-    const uint16_t* qp = a.q + (int64_t)qrow * ld + hoff + 8 * hh;
+    const uint16_t* qp = a.q + (int64_t)qrow * a.ld + L.hoff + 8 * L.hh;
 #pragma unroll
-    for (int kk = 0; kk < C::kSlices; ++kk) {
-      if (q_ok) {
-        qf[kk] = *(const bf16x8*)(qp + 16 * kk);
-      } else {
-        qf[kk] = bf16x8{};
-      }
-    }
+    for (int kk = 0; kk < C::kSlices; ++kk) w.qf[kk] = qrow < a.n_q ? *(const bf16x8*)(qp + 16 * kk) : bf16x8{};
   }
 
   // ---- tile enumeration -------------------------------------------------------
   const int nt0 = (int)((a.r.end[0] - a.r.begin[0] + kBk - 1) / kBk);
   const int nt1 = a.r.n_total > 1 ? (int)((a.r.end[1] - a.r.begin[1] + kBk - 1) / kBk) : 0;
   const int nt2 = a.r.n_total > 2 ? (int)((a.r.end[2] - a.r.begin[2] + kBk - 1) / kBk) : 0;
-  const int tb1 = nt0, tb2 = nt0 + nt1;
-  const int n_tiles = nt0 + nt1 + nt2;
-  const int n_tiles_local = a.r.n_local == 1 ? nt0 : nt0 + nt1;
-  const bool dual = a.out_local != nullptr;
+  L.tb1 = nt0;
+  L.tb2 = nt0 + nt1;
+  L.n_tiles = nt0 + nt1 + nt2;
+  L.n_tiles_local = a.r.n_local == 1 ? nt0 : nt0 + nt1;
+  L.dual = a.out_local != nullptr;
 
-  // ---- online softmax state ------------------------------------------------------
-  f32x16 acc[C::dBlocks];
-#pragma unroll
-  for (int i = 0; i < C::dBlocks; ++i) acc[i] = f32x16{};
-  float m_run = -INFINITY;
-  float l_run = 0.f;
-
-  // ---- HBM -> LDS staging ------------------------------------------------
-  // Load q of this thread covers 16-byte slot (q * kWaves + wave) * 64 + lane of
-  // the tile: row = slot / chunksPerRow, stored chunk = slot % chunksPerRow,
-  // which holds logical chunk (stored ^ (row & swz)) of that key row.
-  int voffk[C::loadsPerThread], voffv[C::loadsPerThread];
+  // ---- per-lane constants ---------------------------------------------------------
+  // Direct load q of this thread covers 16-byte slot (q * kWaves + wave) * 64 + lane
+  // of a tile: row = slot / chunksPerRow, stored chunk = slot % chunksPerRow,
+  // which holds logical chunk (stored ^ swizzle(row)) of that key row.
 #pragma unroll
   for (int q = 0; q < C::loadsPerThread; ++q) {
-    const int slot = (q * kWaves + wave) * 64 + lane;
+    const int slot = (q * kWaves + L.wave) * 64 + lane;
     const int row = slot / C::chunksPerRow;
     const int stored = slot % C::chunksPerRow;
-    voffk[q] = (int)((row * ld + (stored ^ swz_k<D>(row)) * 8) * 2);
-    voffv[q] = (int)((row * ld + (stored ^ swz_v<D>(row)) * 8) * 2);
+    w.voffk[q] = (int)((row * a.ld + (stored ^ swz_k<D>(row)) * 8) * 2);
+    w.voffv[q] = (int)((row * a.ld + (stored ^ swz_v<D>(row)) * 8) * 2);
   }
-  auto gload = [&](int t, int buf) {
-    int64_t key0;
-    int nv;
-    tile_of(a.r, tb1, tb2, t, key0, nv);
-    stage_tile<D>(a, key0 * ld + hoff, nv, smem + buf * 2 * C::tileBytes, voffk, voffv, wave);
-  };
-
-  // per-lane LDS byte offsets of the MFMA operands (tile-relative)
-  int koff[C::kSlices];
 #pragma unroll
-  for (int kk = 0; kk < C::kSlices; ++kk) koff[kk] = chunk_off<D>(ql, 2 * kk + hh, swz_k<D>(ql));
-  const int g = lane >> 4;
-  const int sl = lane & 15;
-  int voffr[2][C::dBlocks];
+  for (int kk = 0; kk < C::kSlices; ++kk) w.koff[kk] = chunk_off<D>(ql, 2 * kk + L.hh, swz_k<D>(ql));
+  {
+    const uint32_t lds0 = lds_addr(smem);
+    const int g = lane >> 4, sl = lane & 15;
 #pragma unroll
-  for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-    for (int db = 0; db < C::dBlocks; ++db) {
-      const int row = 8 * h2 + 4 * (g >> 1) + (sl >> 2);
-      const int chunk = 4 * db + 2 * (g & 1) + ((sl & 3) >> 1);
-      voffr[h2][db] = chunk_off<D>(row, chunk, swz_v<D>(row)) + ((sl & 1) << 3);
-    }
-
-  auto finish = [&](float* out, float* lse) {
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
-    const float inv = 1.0f / l_tot;
-    if (q_ok) {
-      float* op = out + (int64_t)qrow * ld + hoff + 4 * hh;
+    for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
       for (int db = 0; db < C::dBlocks; ++db) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          f32x4 o;
-          o[0] = acc[db][4 * i + 0] * inv;
-          o[1] = acc[db][4 * i + 1] * inv;
-          o[2] = acc[db][4 * i + 2] * inv;
-          o[3] = acc[db][4 * i + 3] * inv;
-          *(f32x4*)(op + 32 * db + 8 * i) = o;
-        }
+        const int row = 8 * h2 + 4 * (g >> 1) + (sl >> 2);
+        const int chunk = 4 * db + 2 * (g & 1) + ((sl & 3) >> 1);
+        w.vaddr[h2][db] = lds0 + chunk_off<D>(row, chunk, swz_v<D>(row)) + ((sl & 1) << 3);
       }
-      if (lse != nullptr && hh == 0) lse[(int64_t)head * a.n_q + qrow] = m_run * a.scale + logf(l_tot);
-    }
-  };
+  }
 
-  if (n_tiles > 0) gload(0, 0);
+  // ---- online softmax state ------------------------------------------------------
+#pragma unroll
+  for (int i = 0; i < C::dBlocks; ++i) w.acc[i] = f32x16{};
+  w.m_run = -INFINITY;
+  w.l_run = 0.f;
+
+  if (L.n_tiles > 0) {
+    int64_t k0;
+    int n0;
+    tile_of(a.r, L.tb1, L.tb2, 0, k0, n0);
+    stage_tile<D>(a, k0 * a.ld + L.hoff, n0, smem, w.voffk, w.voffv, L.wave);
+  }
   __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (dual && t == n_tiles_local) finish(a.out_local, a.lse_local);
-    int64_t key0;
-    int nv;
-    tile_of(a.r, tb1, tb2, t, key0, nv);
-    if (t + 1 < n_tiles) gload(t + 1, buf ^ 1);
-
-    const char* ks = smem + buf * 2 * C::tileBytes;
-    const char* vs = ks + C::tileBytes;
-
-    // The tile is processed as two halves of 32 keys; each half is a complete
-    // online-softmax step (scores, max, lazy rescale, exp, P.V), which keeps
-    // only 16 score registers live.
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      // S^T = K . Q^T for keys 32b .. 32b+31 (rows 32b + ql share the swizzle of row ql)
-      f32x16 sc = f32x16{};
-      const char* kp = ks + 32 * b * C::rowBytes;
-#pragma unroll
-      for (int kk = 0; kk < C::kSlices; ++kk) {
-        const bf16x8 kf = *(const bf16x8*)(kp + koff[kk]);
-        sc = mfma32(kf, qf[kk], sc);
-      }
-      // mask keys beyond the end of a range (only the last tile of each range)
-      if (nv < 32 * (b + 1)) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 32 * b + 8 * (r >> 2) + 4 * hh + (r & 3);
-          if (key >= nv) sc[r] = -INFINITY;
-        }
-      }
-      float tmax = fmaxf(sc[0], sc[1]);
-#pragma unroll
-      for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, sc[r]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      // O and l are rescaled only when some row's running max grew: after the
-      // first few tiles most halves skip the 64 multiplies. The reference stays
-      // the exact running max, so the largest weight of a row is exactly 1 and
-      // carries no bf16 rounding error (a stale reference would put rounding
-      // error on the dominant terms).
-      if (__any(tmax > m_run)) {
-        const float m_new = fmaxf(m_run, tmax);
-        const float alpha = exp2_hw((m_run - m_new) * a.scale_log2);
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < C::dBlocks; ++db) acc[db] *= alpha;
-        m_run = m_new;
-      }
-      const float mc = m_run * a.scale_log2;
-      float psum = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2_hw(fmaf(sc[r], a.scale_log2, -mc));
-        sc[r] = p;
-        psum += p;
-      }
-      l_run += psum;
-      // O^T += V^T . P^T over the two 16-key slices of this half
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        bf16x8 pf;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sc[8 * t2 + e];
-        // rows 16 * slice + ...: both swizzles repeat every 16 rows
-        const char* vp = vs + 16 * (2 * b + t2) * C::rowBytes;
-        bf16x8 vf[C::dBlocks];
-        lds_read_tr_slice<C::dBlocks>(vp, voffr, vf);
-#pragma unroll
-        for (int db = 0; db < C::dBlocks; ++db) acc[db] = mfma32(vf[db], pf, acc[db]);
-      }
+  for (int t = 0; t < L.n_tiles; t += 2) {
+    if (L.dual && t == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
+    tile_step<D, 0>(a, w, L, smem, t);
+    if (t + 1 < L.n_tiles) {
+      if (L.dual && t + 1 == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
+      tile_step<D, 1>(a, w, L, smem, t + 1);
     }
-
-    __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct loads have landed
-    __syncthreads();
   }
-
-  if (dual && n_tiles_local == n_tiles) finish(a.out_local, a.lse_local);
-  finish(a.out, a.lse);
+  if (L.dual && L.n_tiles_local == L.n_tiles) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
+  finish<D>(a, w, L, qrow, head, a.out, a.lse);
 }
 
 }  // namespace
