@@ -13,14 +13,13 @@
 //   the device, wavefront shuffles then one fp64 atomic per workgroup.
 //
 // gram_kernel (bf16 MFMA 32x32x16, fp32 accumulation):
-//   G += X^T X on the lower block triangle of 128x128 tiles, C += X^T R.
-//   The contraction runs over rows, which are the slow (strided) dimension of
-//   both operands. Row-major tiles of 32 rows x 128 columns are staged in LDS
-//   and both MFMA operands are read with the LDS transpose read
-//   (ds_read_b64_tr_b16), which returns 4 consecutive rows of one column per
-//   lane. A workgroup (4 waves, 2x2 of 64x64) owns one output tile; the rows
-//   are split over several workgroups when there are too few tiles to fill the
-//   256 CUs, and partial sums are added with fp32 atomics.
+//   G += X^T X on the lower block triangle of 256x256 tiles, C += X^T R.
+//   The contraction runs over rows, the slow (strided) dimension of both
+//   operands: row-major stages of 32 rows go HBM -> LDS by buffer loads and both
+//   MFMA operands are read with the LDS transpose read (ds_read_b64_tr_b16), 4
+//   consecutive rows of one column per lane. Each wave owns a 128 x 128 quadrant
+//   of the tile. Rows are split over several workgroups when there are too few
+//   tiles to fill the 256 CUs, and partial sums are added with fp32 atomics.
 #include "ispa_internal.h"
 
 namespace ispa {
@@ -122,25 +121,45 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
 }
 
 // ---------------------------------------------------------------- Gram
-constexpr int kTile = 128;   // output tile (rows and columns)
-constexpr int kRows = 32;    // rows staged per step
-constexpr int kLds = kTile + 16;  // LDS row stride (elements) for the tr reads
+// Workgroup = 8 waves, tile 256 x 256 of G (lower block triangle of 256 x 256
+// blocks) or C. Wave w owns output rows 64 (w / 2) .. +63 (A side) and columns
+// 128 (w % 2) .. +127 (B side): 2 x 4 accumulator blocks of 32 x 32 (128
+// registers, two waves per SIMD). Rows are staged 32 at a time HBM -> LDS by
+// buffer loads (no register staging) into a ring of 4 stage buffers, 3 stages
+// ahead of the MFMAs. A stage holds the 32 rows of the tile's 256 X columns (A
+// side) and of its 256 X or R columns (B side), each as two 128-column halves
+// with 256-byte rows. Both MFMA operands need 8 consecutive rows of one column
+// per lane, which the LDS transpose read delivers; the 16-byte chunk index of
+// each row is XOR-swizzled with 4 (row mod 4) ^ 2 (row/4 mod 2) so that the 32
+// lanes of a transpose read hit 16 distinct chunk positions. The buffer
+// descriptor of a stage ends at the split's last row, so rows past it read as
+// zero; columns past d of a ragged last tile read neighbouring data that only
+// reaches output rows/columns >= d, which are never stored.
+constexpr int kGThreads = 512;
+constexpr int kGT = 256;                       // output tile (rows and columns)
+constexpr int kGK = 32;                        // rows per stage
+constexpr int kGRing = 4;                      // stage buffers
+constexpr int kHalfBytes = kGK * 256;          // one 32 x 128 half (bf16)
+constexpr int kSideBytes = 2 * kHalfBytes;     // 32 x 256
+constexpr int kStageBytes = 2 * kSideBytes;    // A side + B side
+constexpr int kLoadsPerStage = kStageBytes / (kGThreads * 16);  // direct loads per thread
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((ISPA_LDS i16x4*)(p));
+__device__ __forceinline__ int gswz(int row) { return (4 * (row & 3)) ^ (2 * ((row >> 2) & 1)); }
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, nbytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(ISPA_LDS const void*)p;
 }
 
-// Operand for rows [16*ks, 16*ks+16) and 32 columns starting at col0 of a
-// row-major LDS tile: lane l gets column col0 + l%32, rows 16ks + 8(l/32) + 0..7.
-__device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int ks, int col0, int lane) {
-  const int g = lane >> 4, sl = lane & 15;
-  const uint16_t* p = tile + (16 * ks + 8 * (g >> 1) + (sl >> 2)) * kLds + col0 + 16 * (g & 1) + 4 * (sl & 3);
-  const i16x4 v0 = lds_read_tr(p);
-  const i16x4 v1 = lds_read_tr(p + 4 * kLds);
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+// Wait until at most N vector memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
 }
 
 struct GramArgs {
@@ -154,98 +173,238 @@ struct GramArgs {
   int n_g_tiles;            // lower block triangle of G
   int n_tiles;              // G tiles + C tiles
   int splits;               // row splits
-  int64_t rows_per_split;   // multiple of kRows
+  int64_t rows_per_split;   // multiple of kGK
 };
 
-__global__ __launch_bounds__(kThreads) void gram_kernel(GramArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][kRows * kLds];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kRows * kLds];
-
-  const int tile = blockIdx.x % a.n_tiles;
-  const int split = blockIdx.x / a.n_tiles;
-  int ti, tj;
-  const uint16_t* bsrc;
-  int bld;
-  float* out;
-  int out_ld, out_cols;
-  if (tile < a.n_g_tiles) {
-    // lower block triangle: tile = ti (ti + 1) / 2 + tj, tj <= ti
-    ti = (int)((sqrtf(8.f * tile + 1.f) - 1.f) * 0.5f);
-    while ((ti + 1) * (ti + 2) / 2 <= tile) ++ti;
-    while (ti * (ti + 1) / 2 > tile) --ti;
-    tj = tile - ti * (ti + 1) / 2;
-    bsrc = a.x; bld = a.d_in; out = a.G; out_ld = a.d_in; out_cols = a.d_in;
-  } else {
-    const int c = tile - a.n_g_tiles;
-    ti = c / a.tiles_out;
-    tj = c % a.tiles_out;
-    bsrc = a.r; bld = a.d_out; out = a.C; out_ld = a.d_out; out_cols = a.d_out;
+// Direct loads of one stage side: 32 rows x 256 columns starting at (row0, col0)
+// of a row-major bf16 matrix with leading dimension ld, rows >= row_end zero.
+// Thread slots: load q of wave w covers 16-byte slot (q * 8 + w) * 64 + lane of
+// the side: half = slot / 512, row = (slot / 16) % 32, stored chunk = slot % 16.
+__device__ __forceinline__ void stage_side(const uint16_t* src, int64_t ld, int64_t row0, int64_t row_end, int col0,
+                                           char* dst, int wave, int lane) {
+  int64_t nrec = ((row_end - row0) * ld - col0) * 2;
+  if (nrec < 0) nrec = 0;
+  if (nrec > 0x7fffffff) nrec = 0x7fffffff;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(src + row0 * ld + col0, (int)nrec);
+#pragma unroll
+  for (int q = 0; q < kSideBytes / (kGThreads * 16); ++q) {
+    const int slot = (q * 8 + wave) * 64 + lane;
+    const int half = slot >> 9;
+    const int row = (slot >> 4) & 31;
+    const int c = (slot & 15) ^ gswz(row);
+    const int voff = (int)((row * ld + half * 128 + c * 8) * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * 8 + wave) * 1024), 16, voff, 0, 0, 0);
   }
-  const int row0 = ti * kTile;  // output rows = X columns
-  const int col0 = tj * kTile;  // output cols = X or R columns
-  const int64_t r_begin = (int64_t)split * a.rows_per_split;
-  int64_t r_end = r_begin + a.rows_per_split;
-  if (r_end > a.rows) r_end = a.rows;
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = (wave >> 1) * 64;  // wave's output sub-tile
-  const int wc = (wave & 1) * 64;
+// Transpose-read addresses of one side for this lane, stage buffer 0, k-slice
+// 0: [blk][h] for column block blk0 + blk (32 columns of a 128-column half) and
+// row half h (rows +4). The swizzle of a row depends only on (row mod 4,
+// row/4 mod 2), i.e. on the lane and h, so k-slices and stage buffers are pure
+// immediate offsets.
+template <int NB>
+struct SideAddr {
+  uint32_t a[NB][2];
+};
+template <int NB>
+__device__ __forceinline__ void side_addr(SideAddr<NB>& s, uint32_t half_base, int blk0, int lane) {
+  const int g = lane >> 4, sl = lane & 15;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int row = 8 * (g >> 1) + 4 * h + (sl >> 2);
+      const int chunk = 4 * (blk0 + b) + 2 * (g & 1) + ((sl & 3) >> 1);
+      s.a[b][h] = half_base + row * 256 + ((chunk ^ gswz(row)) << 4) + ((sl & 1) << 3);
+    }
+}
 
-  f32x16 acc[2][2];
+// The 12 transpose reads (A side: 2 blocks, B side: 4 blocks, 2 row halves each)
+// of one 16-row k-slice, as inline asm: through the builtin the compiler would
+// wait for the direct loads filling the other stage buffers before reading this
+// one. IMM is the compile-time offset of the stage buffer and k-slice.
+template <int IMM>
+__device__ __forceinline__ void gram_issue(const SideAddr<2>& A, const SideAddr<4>& B, u32x2 (&ra)[2][2],
+                                           u32x2 (&rb)[4][2]) {
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(ra[b][h]) : "v"(A.a[b][h]), "i"(IMM));
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(rb[b][h]) : "v"(B.a[b][h]), "i"(IMM));
+}
+
+// Wait until at most N LDS operations are outstanding (LDS operations complete
+// in order) and hand out the operands of that slice.
+template <int N>
+__device__ __forceinline__ void gram_wait(u32x2 (&ra)[2][2], u32x2 (&rb)[4][2], bf16x8* af, bf16x8* bf) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%12)"
+               : "+v"(ra[0][0]), "+v"(ra[0][1]), "+v"(ra[1][0]), "+v"(ra[1][1]), "+v"(rb[0][0]), "+v"(rb[0][1]),
+                 "+v"(rb[1][0]), "+v"(rb[1][1]), "+v"(rb[2][0]), "+v"(rb[2][1]), "+v"(rb[3][0]), "+v"(rb[3][1])
+               : "i"(N));
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+    af[b] = __builtin_bit_cast(bf16x8, u32x4{ra[b][0][0], ra[b][0][1], ra[b][1][0], ra[b][1][1]});
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+    bf[b] = __builtin_bit_cast(bf16x8, u32x4{rb[b][0][0], rb[b][0][1], rb[b][1][0], rb[b][1][1]});
+}
+
+struct GramTile {
+  const uint16_t* bsrc;
+  int64_t bld;
+  int64_t r_begin, r_end;
+  int row0, col0, steps, wave, lane;
+};
+
+__device__ __forceinline__ void stage_load(const GramArgs& a, const GramTile& t, char* smem, int s) {
+  const int64_t rr = t.r_begin + (int64_t)s * kGK;
+  char* d = smem + (s % kGRing) * kStageBytes;
+  stage_side(a.x, a.d_in, rr, t.r_end, t.row0, d, t.wave, t.lane);
+  stage_side(t.bsrc, t.bld, rr, t.r_end, t.col0, d + kSideBytes, t.wave, t.lane);
+}
+
+// Stage s from ring buffer BUF = s % 4: issue the loads of stage s + 3, run the
+// 16 MFMAs of this wave, then wait for stage s + 1 and synchronise.
+// A / B address the pair of stage buffers {BUF & ~1, BUF | 1} (LDS offsets are
+// 16-bit immediates, so buffers 2 and 3 use a second set of addresses).
+template <int BUF>
+__device__ __forceinline__ void gram_stage(const GramArgs& a, const GramTile& t, char* smem, const SideAddr<2>& A,
+                                           const SideAddr<4>& B, f32x16 (&acc)[2][4], int s) {
+  constexpr int kOff = (BUF & 1) * kStageBytes;
+  if (s + 3 < t.steps) stage_load(a, t, smem, s + 3);
+  // lgkmcnt counts at most 15 outstanding operations: the second slice's 12
+  // reads are issued once the first slice has landed, and overlap its MFMAs
+  u32x2 ra[2][2], rb[4][2];
+  bf16x8 af[2], bf[4];
+  gram_issue<kOff>(A, B, ra, rb);
+  gram_wait<0>(ra, rb, af, bf);
+  gram_issue<kOff + 16 * 256>(A, B, ra, rb);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-
-  // staging: 32 rows x 128 columns of each operand = 512 chunks of 8 bf16,
-  // two per thread per operand
-  u32x4 ra[2], rb[2];
-  auto gload = [&](int64_t r0) {
+    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+  gram_wait<0>(ra, rb, af, bf);
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int idx = tid + c * kThreads;
-      const int rr = idx >> 4;
-      const int cc = (idx & 15) * 8;
-      const int64_t row = r0 + rr;
-      const bool rok = row < r_end;
-      ra[c] = (rok && row0 + cc < a.d_in) ? *(const u32x4*)(a.x + row * a.d_in + row0 + cc) : u32x4{0, 0, 0, 0};
-      rb[c] = (rok && col0 + cc < out_cols) ? *(const u32x4*)(bsrc + row * bld + col0 + cc) : u32x4{0, 0, 0, 0};
-    }
-  };
-  auto sstore = [&](int buf) {
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int idx = tid + c * kThreads;
-      const int rr = idx >> 4;
-      const int cc = (idx & 15) * 8;
-      *(u32x4*)(&sA[buf][rr * kLds + cc]) = ra[c];
-      *(u32x4*)(&sB[buf][rr * kLds + cc]) = rb[c];
-    }
-  };
-
-  const int steps = r_end > r_begin ? (int)((r_end - r_begin + kRows - 1) / kRows) : 0;
-  if (steps > 0) {
-    gload(r_begin);
-    sstore(0);
+    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+  // stage s + 1 must have landed: younger stages still in flight are s + 2 and
+  // s + 3 when they exist (direct loads retire in order)
+  const int younger = t.steps - (s + 2);
+  if (younger >= 2) {
+    vm_wait<2 * kLoadsPerStage>();
+  } else if (younger == 1) {
+    vm_wait<kLoadsPerStage>();
+  } else {
+    vm_wait<0>();
   }
   __syncthreads();
-  for (int s = 0; s < steps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < steps) gload(r_begin + (int64_t)(s + 1) * kRows);
-#pragma unroll
-    for (int ks = 0; ks < kRows / 16; ++ks) {
-      bf16x8 af[2], bf[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = tr_operand(sA[buf], ks, wr + 32 * i, lane);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) bf[j] = tr_operand(sB[buf], ks, wc + 32 * j, lane);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+}
+
+// Output tile k of one split in panel-group order: row panels (X columns) are
+// taken kGroup at a time; within a group the G tiles of the lower block
+// triangle come column by column, then the C tiles column by column, each
+// column holding the group's rows. Returns true for a G tile (ti, tj: row and
+// column panel), false for a C tile.
+constexpr int kGroup = 4;
+__device__ __forceinline__ bool gram_tile_of(int k, int tiles_in, int tiles_out, int& ti, int& tj) {
+  int r0 = 0, gm = 0, n_g = 0;
+  for (;; r0 += kGroup) {
+    gm = min(kGroup, tiles_in - r0);
+    n_g = r0 * gm + gm * (gm + 1) / 2;
+    const int n = n_g + tiles_out * gm;
+    if (k < n || r0 + gm >= tiles_in) break;
+    k -= n;
+  }
+  if (k < r0 * gm) {  // full columns left of the group's diagonal block
+    tj = k / gm;
+    ti = r0 + k % gm;
+    return true;
+  }
+  if (k < n_g) {  // the diagonal block's lower triangle: column c holds rows c .. r0 + gm - 1
+    k -= r0 * gm;
+    tj = r0;
+    while (k >= r0 + gm - tj) {
+      k -= r0 + gm - tj;
+      ++tj;
     }
-    if (s + 1 < steps) sstore(buf ^ 1);
-    __syncthreads();
+    ti = tj + k;
+    return true;
+  }
+  k -= n_g;
+  tj = k / gm;
+  ti = r0 + k % gm;
+  return false;
+}
+
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) void gram_kernel(GramArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kGRing * kStageBytes];
+
+  // The work list (split-major, tiles in panel-group order within a split) is
+  // cut into 8 contiguous ranges, one per XCD (workgroups are dealt to the XCDs
+  // round robin), so that the workgroups resident on one XCD at a time work on
+  // few distinct X / R panels and share them through that XCD's L2.
+  const int n_items = a.n_tiles * a.splits;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+  if (item >= n_items) return;
+  const int split = item / a.n_tiles;
+  GramTile t;
+  int ti, tj;
+  const bool is_g = gram_tile_of(item % a.n_tiles, a.tiles_in, a.tiles_out, ti, tj);
+  float* out;
+  int out_ld, out_cols;
+  if (is_g) {
+    t.bsrc = a.x; t.bld = a.d_in; out = a.G; out_ld = a.d_in; out_cols = a.d_in;
+  } else {
+    t.bsrc = a.r; t.bld = a.d_out; out = a.C; out_ld = a.d_out; out_cols = a.d_out;
+  }
+  t.row0 = ti * kGT;  // output rows = X columns
+  t.col0 = tj * kGT;  // output cols = X or R columns
+  t.r_begin = (int64_t)split * a.rows_per_split;
+  t.r_end = t.r_begin + a.rows_per_split;
+  if (t.r_end > a.rows) t.r_end = a.rows;
+  t.lane = threadIdx.x & 63;
+  t.wave = threadIdx.x >> 6;
+  t.steps = t.r_end > t.r_begin ? (int)((t.r_end - t.r_begin + kGK - 1) / kGK) : 0;
+  const int wr = t.wave >> 1;  // output rows 64 wr .. +63: A half wr / 2, blocks 2 (wr % 2), +1
+  const int wc = t.wave & 1;   // output cols 128 wc .. +127: B half wc
+
+  const uint32_t lds0 = lds_addr(smem);
+  SideAddr<2> A, A2;
+  SideAddr<4> B, B2;
+  side_addr<2>(A, lds0 + (wr >> 1) * kHalfBytes, 2 * (wr & 1), t.lane);
+  side_addr<4>(B, lds0 + kSideBytes + wc * kHalfBytes, 0, t.lane);
+  side_addr<2>(A2, lds0 + 2 * kStageBytes + (wr >> 1) * kHalfBytes, 2 * (wr & 1), t.lane);
+  side_addr<4>(B2, lds0 + 2 * kStageBytes + kSideBytes + wc * kHalfBytes, 0, t.lane);
+
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+
+  // prologue: stages 0..2 in flight, wait for stage 0
+  for (int s = 0; s < 3 && s < t.steps; ++s) stage_load(a, t, smem, s);
+  if (t.steps >= 3) {
+    vm_wait<2 * kLoadsPerStage>();
+  } else if (t.steps == 2) {
+    vm_wait<kLoadsPerStage>();
+  } else {
+    vm_wait<0>();
+  }
+  __syncthreads();
+  for (int s = 0; s < t.steps; s += kGRing) {
+    gram_stage<0>(a, t, smem, A, B, acc, s);
+    if (s + 1 < t.steps) gram_stage<1>(a, t, smem, A, B, acc, s + 1);
+    if (s + 2 < t.steps) gram_stage<2>(a, t, smem, A2, B2, acc, s + 2);
+    if (s + 3 < t.steps) gram_stage<3>(a, t, smem, A2, B2, acc, s + 3);
   }
 
   // accumulate into G / C: lane holds column (lane%32) and rows 8(r/4)+4(lane/32)+r%4
@@ -253,11 +412,11 @@ __global__ __launch_bounds__(kThreads) void gram_kernel(GramArgs a) {
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int orow = row0 + wr + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int ocol = col0 + wc + 32 * j + (lane & 31);
+        const int orow = t.row0 + 64 * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
+        const int ocol = t.col0 + 128 * wc + 32 * j + (t.lane & 31);
         if (orow < a.d_in && ocol < out_cols) {
           float* p = out + (int64_t)orow * out_ld + ocol;
           if (atomic) {
@@ -315,21 +474,30 @@ hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d
   if (rows <= 0) return hipSuccess;
   GramArgs a;
   a.x = x; a.r = r; a.G = G; a.C = C; a.rows = rows; a.d_in = d_in; a.d_out = d_out;
-  a.tiles_in = (d_in + kTile - 1) / kTile;
-  a.tiles_out = (d_out + kTile - 1) / kTile;
+  a.tiles_in = (d_in + kGT - 1) / kGT;
+  a.tiles_out = (d_out + kGT - 1) / kGT;
   a.n_g_tiles = a.tiles_in * (a.tiles_in + 1) / 2;
   a.n_tiles = a.n_g_tiles + a.tiles_in * a.tiles_out;
-  // enough workgroups for 2 per CU, but at least 256 rows per split
-  int splits = (512 + a.n_tiles - 1) / a.n_tiles;
-  const int64_t max_splits = (rows + 255) / 256;
-  if (splits > max_splits) splits = (int)max_splits;
-  if (splits < 1) splits = 1;
+  // One workgroup per CU (128 KB of LDS). Rows are split so that the 256 CUs are
+  // used well: the split count s minimises rounds(n_tiles * s) / s, the smallest
+  // s winning ties (fewer atomics); every split keeps at least 8 stages of rows.
+  int splits = 1;
+  double best = 1e30;
+  for (int sc = 1; sc <= 4; ++sc) {
+    if (sc > 1 && rows < (int64_t)sc * 8 * kGK) break;
+    const int64_t wgs = (int64_t)a.n_tiles * sc;
+    const double cost = (double)((wgs + 255) / 256) / sc;
+    if (cost < best - 1e-12) {
+      best = cost;
+      splits = sc;
+    }
+  }
   int64_t per = (rows + splits - 1) / splits;
-  per = (per + kRows - 1) / kRows * kRows;
+  per = (per + kGK - 1) / kGK * kGK;
   splits = (int)((rows + per - 1) / per);
   a.splits = splits;
   a.rows_per_split = per;
-  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(a.n_tiles * splits)), dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(8 * ((a.n_tiles * splits + 7) / 8))), dim3(kGThreads), 0, stream, a);
   return hipGetLastError();
 }
 
