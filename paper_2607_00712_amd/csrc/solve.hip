@@ -21,13 +21,13 @@
 //   sub-blocks, each factored right-looking with a row per lane in registers
 //   and the column multipliers broadcast through LDS, then inverted
 //   column-wise; the off-diagonal pieces are 32 x 32 x 32 MFMA products.
-// Triangular solves, one launch per block row (right-looking, fused):
-//   forward  B_r -= L_{r,i} Z_i for r > i;  tile r = i+1 then forms
-//            Z_{i+1} = L_{i+1,i+1}^-1 B_{i+1}
-//   backward B_r -= L_{i,r}^T dW_i for r < i; tile r = i-1 then forms
-//            dW_{i-1} = L_{i-1,i-1}^-T B_{i-1}
-// Every GEMM is fp32 MFMA 32x32x2 (v_mfma_f32_32x32x2f32) on 64 x 64 LDS tiles,
-// one 32 x 32 quadrant per wave.
+// Triangular solves in block LDL^T form over 256-blocks (details below): the
+//   inverses X_I of the 256 x 256 diagonal blocks of L and P_I = X_I^T X_I,
+//   Lh = L diag(X_I) below the 256-block diagonal (its transpose mirrored into
+//   the upper part), then one right-looking rank-256 GEMM launch per block for
+//   the forward and for the backward sweep, with no diagonal work in them.
+// Every product is fp32 MFMA (v_mfma_f32_32x32x2f32); the sweeps' GEMM stages
+// its operands HBM -> LDS with direct buffer loads in a 4-deep ring.
 #include "ispa_internal.h"
 
 #include <math.h>
@@ -348,102 +348,253 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   store_tile(T, Lrt, n, rr, nd);
 }
 
-// Forward solve launch i (i = -1 .. nb-2): B_r -= L_{r,i} Z_i for r > i; tile
-// r = i+1 forms Z_{i+1} = Dinv_{i+1} B_{i+1}. Grid: (nb-1-i) x column tiles.
-__global__ __launch_bounds__(kThreads) void trsm_fwd_kernel(const float* L, const float* Dinv, float* Bw, float* Z,
-                                                           int n, int n_out, int i) {
-  __shared__ Tile A, X, Bt;
+// ---------------------------------------------------------------- 256-block
+// Triangular solves in block LDL^T form. With 256 x 256 diagonal blocks L_II of
+// L, X_I = L_II^-1, Lh_rI = L_rI X_I (unit block-lower Lh, L = Lh diag(L_II)) and
+// P_I = X_I^T X_I (the inverse of the I-th diagonal block of the Schur
+// complements):
+//   L Z = C      <=>  Lh Y = C,  Z_I = X_I Y_I
+//   L^T dW = Z   <=>  Lh^T dW = V,  V_I = P_I Y_I
+// Both unit-triangular sweeps are right-looking rank-256 GEMM updates with no
+// diagonal work, one launch per block: Y_r -= Lh_rI Y_I (r > I) and
+// dW_I -= Lh_JI^T dW_J (I < J). Lh overwrites the strictly-below-256-block part
+// of L and its transpose is mirrored into the (otherwise zero) upper part, so
+// that every GEMM operand is read as rows of a row-major matrix.
+constexpr int kBb = 256;  // block size of the triangular sweeps
+constexpr int kKc = 16;   // k rows per LDS chunk of the GEMM
+
+// quad() accumulated into acc
+template <bool TA, bool TB>
+__device__ __forceinline__ void quad_acc(f32x16& acc, const Tile& A, const Tile& B) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  mma<TA, TB>(acc, A, (wave >> 1) * 32, 0, B, (wave & 1) * 32, 0, kNb, lane);
+}
+__device__ __forceinline__ void quad_put(Tile& D, const f32x16& acc, float sign) {
+  quad_store(D, acc, sign, false);
+}
+
+// X_I = L_II^-1 for 256-block I = blockIdx.x, 64-column strip b = blockIdx.y:
+// X_bb = Dinv_b and, for a > b, X_ab = -Dinv_a sum_{c=b}^{a-1} L_ac X_cb (64-block
+// indices inside the 256-block). Writes the full 256 x 64 strip of X_I (zeros
+// above the diagonal and in 64-blocks past the end of the matrix).
+__global__ __launch_bounds__(kThreads) void inv256_kernel(const float* L, const float* Dinv, float* Xinv, int n) {
+  __shared__ Tile Xc[4];
+  __shared__ Tile U;
   const int nblk = (n + kNb - 1) / kNb;
-  const int ctiles = (n_out + kNb - 1) / kNb;
-  const int r = i + 1 + blockIdx.x / ctiles;
-  const int c = blockIdx.x % ctiles;
-  if (r >= nblk) return;
-  const int rr = min(kNb, n - r * kNb), cc = min(kNb, n_out - c * kNb);
-  float* Br = Bw + (int64_t)r * kNb * n_out + c * kNb;
-  const bool last = r == i + 1;
-  Frag fb, fa, fx, fd;
-  fetch(fb, Br, n_out, rr, cc);
-  if (i >= 0) {
-    const int ri = min(kNb, n - i * kNb);
-    fetch(fa, L + (int64_t)r * kNb * n + i * kNb, n, rr, ri);
-    fetch(fx, Z + (int64_t)i * kNb * n_out + c * kNb, n_out, ri, cc);
+  const int I = blockIdx.x, b = blockIdx.y;
+  const int g0 = I * 4;                       // first 64-block of the 256-block
+  const int n64 = min(4, nblk - g0);          // 64-blocks inside the matrix
+  float* X = Xinv + (int64_t)I * kBb * kBb;  // [256][256], row-major
+  if (b < n64) {
+    load_tile(Xc[b], Dinv + (int64_t)(g0 + b) * kNb * kNb, kNb, kNb, kNb);
+    __syncthreads();
+    for (int a = b + 1; a < n64; ++a) {
+      const int ra = min(kNb, n - (g0 + a) * kNb);
+      f32x16 t = {};
+      for (int c = b; c < a; ++c) {
+        load_tile(U, L + (int64_t)(g0 + a) * kNb * n + (int64_t)(g0 + c) * kNb, n, ra, kNb);
+        __syncthreads();
+        quad_acc<false, false>(t, U, Xc[c]);
+        __syncthreads();
+      }
+      // Xc[a] = -Dinv_a . T: T goes through Xc[a], Dinv_a through U
+      quad_put(Xc[a], t, 1.f);
+      load_tile(U, Dinv + (int64_t)(g0 + a) * kNb * kNb, kNb, kNb, kNb);
+      __syncthreads();
+      const f32x16 x = quad<false, false>(U, Xc[a]);
+      __syncthreads();
+      quad_put(Xc[a], x, -1.f);
+      __syncthreads();
+    }
   }
-  if (last) fetch(fd, Dinv + (int64_t)r * kNb * kNb, kNb, kNb, kNb);
-  put(Bt, fb);
-  if (i >= 0) {
-    put(A, fa);
-    put(X, fx);
-  }
-  __syncthreads();
-  if (i >= 0) {
-    quad_store(Bt, quad<false, false>(A, X), -1.f, true);
-    __syncthreads();
-  }
-  if (last) {
-    put(A, fd);
-    __syncthreads();
-    const f32x16 z = quad<false, false>(A, Bt);
-    __syncthreads();
-    quad_store(Bt, z, 1.f, false);
-    __syncthreads();
-    store_tile(Bt, Z + (int64_t)r * kNb * n_out + c * kNb, n_out, rr, cc);
-  } else {
-    store_tile(Bt, Br, n_out, rr, cc);
+  for (int a = 0; a < 4; ++a) {
+    float* dst = X + (int64_t)a * kNb * kBb + b * kNb;
+    if (b < n64 && a >= b && a < n64) {
+      store_tile(Xc[a], dst, kBb, kNb, kNb);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = threadIdx.x + q * kThreads;
+        const int r = e >> 4, c = (e & 15) * 4;
+        *(f32x4*)(dst + (int64_t)r * kBb + c) = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
   }
 }
 
-// Backward solve launch i (i = nb .. 1), in place on W (holds Z, becomes dW):
-// W_r -= L_{i,r}^T W_i for r < i; tile r = i-1 forms W_{i-1} = Dinv_{i-1}^T W_{i-1}.
-__global__ __launch_bounds__(kThreads) void trsm_bwd_kernel(const float* L, const float* Dinv, float* W, int n,
-                                                           int n_out, int i) {
-  __shared__ Tile A, X, Bt;
+// Upper part of L from Lh: U[c][r] = L[r][c] for every (r, c) whose 256-block
+// row is below its 256-block column. One 64 x 64 tile per workgroup.
+__global__ __launch_bounds__(kThreads) void mirror_kernel(float* L, int n) {
+  __shared__ Tile T;
   const int nblk = (n + kNb - 1) / kNb;
-  const int ctiles = (n_out + kNb - 1) / kNb;
-  const int r = i - 1 - blockIdx.x / ctiles;
-  const int c = blockIdx.x % ctiles;
-  if (r < 0) return;
-  const int rr = min(kNb, n - r * kNb), cc = min(kNb, n_out - c * kNb);
-  float* Wr = W + (int64_t)r * kNb * n_out + c * kNb;
-  const bool last = r == i - 1;
-  Frag fb, fa, fx, fd;
-  fetch(fb, Wr, n_out, rr, cc);
-  if (i < nblk) {
-    const int ri = min(kNb, n - i * kNb);
-    fetch(fa, L + (int64_t)i * kNb * n + r * kNb, n, ri, rr);  // L_{i,r}, used transposed
-    fetch(fx, W + (int64_t)i * kNb * n_out + c * kNb, n_out, ri, cc);
-  }
-  if (last) fetch(fd, Dinv + (int64_t)r * kNb * kNb, kNb, kNb, kNb);
-  put(Bt, fb);
-  if (i < nblk) {
-    put(A, fa);
-    put(X, fx);
-  }
+  const int tr = blockIdx.x / nblk, tc = blockIdx.x % nblk;
+  if (tr / 4 <= tc / 4) return;
+  const int rr = min(kNb, n - tr * kNb), rc = min(kNb, n - tc * kNb);
+  load_tile(T, L + (int64_t)tr * kNb * n + (int64_t)tc * kNb, n, rr, rc);
   __syncthreads();
-  if (i < nblk) {
-    quad_store(Bt, quad<true, false>(A, X), -1.f, true);
-    __syncthreads();
+  float* dst = L + (int64_t)tc * kNb * n + (int64_t)tr * kNb;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = threadIdx.x + q * kThreads;
+    const int r = e >> 4, c = (e & 15) * 4;
+    if (r < rc && c < rr) *(f32x4*)(dst + (int64_t)r * n + c) = f32x4{T[c][r], T[c + 1][r], T[c + 2][r], T[c + 3][r]};
   }
-  if (last) {
-    put(A, fd);
-    __syncthreads();
-    const f32x16 z = quad<true, false>(A, Bt);
-    __syncthreads();
-    quad_store(Bt, z, 1.f, false);
-    __syncthreads();
-  }
-  store_tile(Bt, Wr, n_out, rr, cc);
 }
 
-// scalars[0] = <dW, C>, scalars[1] = ||dW||^2 (zeroed by the first block, then
-// accumulated; launched as a single pass after zeroing)
-__global__ __launch_bounds__(kThreads) void eps_kernel(const float* dw, const float* C, int64_t n, double* scalars) {
-  __shared__ double red[2][kThreads / 64];
-  double a = 0, b = 0;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
-    const double w = dw[i];
-    a += w * (double)C[i];
-    b += w * w;
+// C(m, n) = [C(m, n) -] sum_k A(m, k) B(k, n) for m < M, n < N, in fp32 MFMA.
+// B(k, n) = B[k * ldb + n]. A(m, k) = A[k * lda + m] (k-major), or
+// A[m * lda + k] for the m-major instantiation. One launch runs up to two jobs
+// that share B, N and K (tiles of job 0 first), batched over blockIdx.y with
+// element strides per batch and M growing by batch_dm per batch. Dimensions
+// are multiples of 4 and rows 16-byte aligned. Operands are staged through
+// LDS k-major (a row of 16 k-rows per chunk, double buffered) so that the
+// 32 lanes of an MFMA operand read 32 consecutive floats.
+struct GemmJob {
+  const float* A;
+  float* C;
+  int M;
+  int64_t lda, ldc;
+  int sub;  // 1: C -= A B, 0: C = A B
+};
+struct GemmArgs {
+  GemmJob job[2];
+  int n_jobs;
+  const float* B;
+  int N, K;
+  int64_t ldb;
+  int64_t batch_a, batch_b, batch_c;
+  int batch_dm;
+};
+
+template <int WM, int WN, int QM, int QN, bool A_MK>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
+  constexpr int TM = WM * QM * 32, TN = WN * QN * 32;
+  constexpr int SA = TM + 32, SB = TN + 32;  // row strides: the two k rows of an operand read sit 32 banks apart
+  constexpr int NA = kKc * TM / 4 / kThreads, NB = kKc * TN / 4 / kThreads;
+  static_assert(WM * WN == kThreads / 64 && NA >= 1 && NB >= 1, "tile shape");
+  __shared__ __attribute__((aligned(16))) float As[2][kKc][SA];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kKc][SB];
+
+  const int tiles_n = (g.N + TN - 1) / TN;
+  const int dm = (int)blockIdx.y * g.batch_dm;
+  const int m_tiles0 = (g.job[0].M + dm + TM - 1) / TM;
+  int t = blockIdx.x;
+  const bool second = t >= m_tiles0 * tiles_n;
+  if (second) {
+    if (g.n_jobs < 2) return;
+    t -= m_tiles0 * tiles_n;
   }
+  const float* A = second ? g.job[1].A : g.job[0].A;
+  float* C = second ? g.job[1].C : g.job[0].C;
+  const int M = (second ? g.job[1].M : g.job[0].M) + dm;
+  const int64_t lda = second ? g.job[1].lda : g.job[0].lda;
+  const int64_t ldc = second ? g.job[1].ldc : g.job[0].ldc;
+  const int sub = second ? g.job[1].sub : g.job[0].sub;
+  const int m0 = (t / tiles_n) * TM, n0 = (t % tiles_n) * TN;
+  if (m0 >= M) return;
+  A += blockIdx.y * g.batch_a;
+  const float* B = g.B + blockIdx.y * g.batch_b;
+  C += blockIdx.y * g.batch_c;
+  const int N = g.N, K = g.K;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int wm0 = (wave / WN) * QM * 32, wn0 = (wave % WN) * QN * 32;
+
+  f32x4 ra[NA], rb[NB];
+  auto fetch_chunk = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < NA; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      if (A_MK) {
+        const int m = e / (kKc / 4), k = (e % (kKc / 4)) * 4;
+        ra[q] = (m0 + m < M && k0 + k < K) ? *(const f32x4*)(A + (int64_t)(m0 + m) * lda + k0 + k)
+                                             : f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+        const int k = e / (TM / 4), m = (e % (TM / 4)) * 4;
+        ra[q] = (k0 + k < K && m0 + m < M) ? *(const f32x4*)(A + (int64_t)(k0 + k) * lda + m0 + m)
+                                             : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int k = e / (TN / 4), nn = (e % (TN / 4)) * 4;
+      rb[q] = (k0 + k < K && n0 + nn < N) ? *(const f32x4*)(B + (int64_t)(k0 + k) * g.ldb + n0 + nn)
+                                            : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto put_chunk = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < NA; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      if (A_MK) {
+        const int m = e / (kKc / 4), k = (e % (kKc / 4)) * 4;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) As[buf][k + j][m] = ra[q][j];
+      } else {
+        const int k = e / (TM / 4), m = (e % (TM / 4)) * 4;
+        *(f32x4*)&As[buf][k][m] = ra[q];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int k = e / (TN / 4), nn = (e % (TN / 4)) * 4;
+      *(f32x4*)&Bs[buf][k][nn] = rb[q];
+    }
+  };
+
+  f32x16 acc[QM][QN];
+#pragma unroll
+  for (int i = 0; i < QM; ++i)
+#pragma unroll
+    for (int j = 0; j < QN; ++j) acc[i][j] = f32x16{};
+
+  const int nk = (K + kKc - 1) / kKc;
+  fetch_chunk(0);
+  put_chunk(0);
+  __syncthreads();
+  for (int c = 0; c < nk; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nk) fetch_chunk((c + 1) * kKc);
+#pragma unroll
+    for (int kk = 0; kk < kKc; kk += 2) {
+      float a[QM], b[QN];
+#pragma unroll
+      for (int i = 0; i < QM; ++i) a[i] = As[buf][kk + h][wm0 + 32 * i + l32];
+#pragma unroll
+      for (int j = 0; j < QN; ++j) b[j] = Bs[buf][kk + h][wn0 + 32 * j + l32];
+#pragma unroll
+      for (int i = 0; i < QM; ++i)
+#pragma unroll
+        for (int j = 0; j < QN; ++j) acc[i][j] = mfma_f32(a[i], b[j], acc[i][j]);
+    }
+    if (c + 1 < nk) put_chunk(buf ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int i = 0; i < QM; ++i)
+#pragma unroll
+    for (int j = 0; j < QN; ++j) {
+      const int col = n0 + wn0 + 32 * j + l32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm0 + 32 * i + acc_row(r, lane);
+        if (row < M && col < N) {
+          float* p = C + (int64_t)row * ldc + col;
+          *p = sub ? *p - acc[i][j][r] : acc[i][j][r];
+        }
+      }
+    }
+}
+
+// <dW, C> and ||dW||^2 in two passes: each of kEpsBlocks workgroups reduces a
+// grid-strided share (16-byte loads, n a multiple of 4) to one pair in
+// part[2 * block], then a single workgroup adds the pairs into scalars[0], [1].
+constexpr int kEpsBlocks = 512;
+__device__ __forceinline__ void block_sum2(double& a, double& b, double (*red)[kThreads / 64]) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     a += __shfl_xor(a, o);
@@ -454,59 +605,374 @@ __global__ __launch_bounds__(kThreads) void eps_kernel(const float* dw, const fl
     red[1][threadIdx.x >> 6] = b;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    double ta = 0, tb = 0;
-    for (int w = 0; w < kThreads / 64; ++w) {
-      ta += red[0][w];
-      tb += red[1][w];
-    }
-    atomicAdd(&scalars[0], ta);
-    atomicAdd(&scalars[1], tb);
+  a = 0;
+  b = 0;
+  for (int w = 0; w < kThreads / 64; ++w) {
+    a += red[0][w];
+    b += red[1][w];
   }
 }
-
-__global__ void zero_scalars_kernel(double* s) {
-  if (threadIdx.x < 2) s[threadIdx.x] = 0.0;
+__global__ __launch_bounds__(kThreads) void eps_partial_kernel(const float* dw, const float* C, int64_t n,
+                                                               double* part) {
+  __shared__ double red[2][kThreads / 64];
+  double a = 0, b = 0;
+  const int64_t n4 = n / 4;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n4; i += (int64_t)gridDim.x * kThreads) {
+    const f32x4 w = *(const f32x4*)(dw + 4 * i);
+    const f32x4 c = *(const f32x4*)(C + 4 * i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      a += (double)w[j] * (double)c[j];
+      b += (double)w[j] * (double)w[j];
+    }
+  }
+  block_sum2(a, b, red);
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = a;
+    part[2 * blockIdx.x + 1] = b;
+  }
+}
+__global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part, int n_part, double* scalars) {
+  __shared__ double red[2][kThreads / 64];
+  double a = 0, b = 0;
+  for (int i = threadIdx.x; i < n_part; i += kThreads) {
+    a += part[2 * i];
+    b += part[2 * i + 1];
+  }
+  block_sum2(a, b, red);
+  if (threadIdx.x == 0) {
+    scalars[0] = a;
+    scalars[1] = b;
+  }
 }
 
 }  // namespace
 
+namespace {
+
+// ---------------------------------------------------------------- ring GEMM
+// The sweeps' GEMM (both operands k-major: A(m, k) = A[k * lda + m]) with the
+// operands staged HBM -> LDS by buffer loads straight into LDS, in a ring of 4
+// stages of 16 k-rows, 3 stages ahead of the MFMAs. A stage side holds 16 rows
+// of the tile's TM (or TN) columns, 16-byte chunk c of row k stored at chunk
+// c ^ 8 (k & 1): the two k-rows read by one MFMA operand sit 32 banks apart.
+// The buffer descriptor of a side ends at the last valid element of the job,
+// so k-rows past K read as zero; columns past M or N read finite neighbouring
+// data that only reaches outputs that are not stored.
+constexpr int kRing = 4;
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
+
+template <int T>
+__device__ __forceinline__ void ring_side(const float* src, int64_t ld, int k0, int kend, int c0, int cend, char* dst,
+                                          int wave, int lane) {
+  int64_t nrec = ((int64_t)(kend - k0 - 1) * ld + (cend - c0)) * 4;
+  if (nrec < 0) nrec = 0;
+  if (nrec > 0x7fffffff) nrec = 0x7fffffff;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(src + (int64_t)k0 * ld + c0), 0, (int)nrec, 0x00020000);
+  constexpr int kChunks = T / 4;  // 16-byte chunks per row
+#pragma unroll
+  for (int q = 0; q < kKc * T * 4 / (kThreads * 16); ++q) {
+    const int slot = (q * 4 + wave) * 64 + lane;
+    const int row = slot / kChunks;
+    const int c = (slot % kChunks) ^ ((row & 1) << 3);
+    const int voff = (int)((row * ld + c * 4) * 4);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * 4 + wave) * 1024), 16, voff, 0, 0, 0);
+  }
+}
+
+template <int QM, int QN>
+struct RingRegs {
+  float a[2][QM], b[2][QN];
+};
+
+// LDS reads of k-row pair KK of stage buffer BUF into register set S
+template <int IMMA, int IMMB, int QM, int QN>
+__device__ __forceinline__ void ring_issue(const uint32_t (&oa)[QM], const uint32_t (&ob)[QN], float (&a)[QM],
+                                           float (&b)[QN]) {
+#pragma unroll
+  for (int i = 0; i < QM; ++i) asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(a[i]) : "v"(oa[i]), "i"(IMMA));
+#pragma unroll
+  for (int j = 0; j < QN; ++j) asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(b[j]) : "v"(ob[j]), "i"(IMMB));
+}
+
+// at most N LDS operations outstanding: the reads into a, b have landed
+template <int N, int QM, int QN>
+__device__ __forceinline__ void ring_wait(float (&a)[QM], float (&b)[QN]) {
+  static_assert(N >= 0 && N <= 15 && ((QM == 2 && QN == 2) || (QM == 1 && QN == 1)), "shape");
+  if constexpr (QM == 2) {
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]) : "i"(N));
+  } else {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a[0]), "+v"(b[0]) : "i"(N));
+  }
+}
+
+template <int BUF, int KK, int TM, int TN, int QM, int QN>
+__device__ __forceinline__ void ring_ksteps(const uint32_t (&oa)[QM], const uint32_t (&ob)[QN], RingRegs<QM, QN>& r,
+                                            f32x16 (&acc)[QM][QN]) {
+  constexpr int kStage = kKc * (TM + TN) * 4;
+  constexpr int cur = (KK / 2) & 1;
+  if constexpr (KK + 2 < kKc) {
+    ring_issue<BUF * kStage + (KK + 2) * TM * 4, BUF * kStage + (KK + 2) * TN * 4, QM, QN>(oa, ob, r.a[cur ^ 1],
+                                                                                           r.b[cur ^ 1]);
+    ring_wait<QM + QN, QM, QN>(r.a[cur], r.b[cur]);
+  } else {
+    ring_wait<0, QM, QN>(r.a[cur], r.b[cur]);
+  }
+#pragma unroll
+  for (int i = 0; i < QM; ++i)
+#pragma unroll
+    for (int j = 0; j < QN; ++j) acc[i][j] = mfma_f32(r.a[cur][i], r.b[cur][j], acc[i][j]);
+  if constexpr (KK + 2 < kKc) ring_ksteps<BUF, KK + 2, TM, TN, QM, QN>(oa, ob, r, acc);
+}
+
+struct RingTile {
+  const float* A;
+  const float* B;
+  int64_t lda, ldb;
+  int M, N, K, m0, n0, steps, wave, lane;
+};
+
+template <int TM, int TN>
+__device__ __forceinline__ void ring_load(const RingTile& t, char* smem, int s) {
+  constexpr int kStage = kKc * (TM + TN) * 4;
+  char* d = smem + (s % kRing) * kStage;
+  const int k0 = s * kKc;
+  ring_side<TM>(t.A, t.lda, k0, t.K, t.m0, t.M, d, t.wave, t.lane);
+  ring_side<TN>(t.B, t.ldb, k0, t.K, t.n0, t.N, d + kKc * TM * 4, t.wave, t.lane);
+}
+
+// stage s from ring buffer BUF = s % 4: loads of stage s + 3, the MFMAs of s,
+// then wait for stage s + 1 (direct loads retire in order) and synchronise
+template <int BUF, int TM, int TN, int QM, int QN>
+__device__ __forceinline__ void ring_stage(const RingTile& t, char* smem, const uint32_t (&oa)[QM],
+                                           const uint32_t (&ob)[QN], f32x16 (&acc)[QM][QN], int s) {
+  constexpr int kLoads = (TM + TN) / 64;  // direct loads per thread per stage
+  if (s + 3 < t.steps) ring_load<TM, TN>(t, smem, s + 3);
+  RingRegs<QM, QN> r;
+  ring_issue<BUF * kKc * (TM + TN) * 4, BUF * kKc * (TM + TN) * 4, QM, QN>(oa, ob, r.a[0], r.b[0]);
+  ring_ksteps<BUF, 0, TM, TN, QM, QN>(oa, ob, r, acc);
+  const int younger = t.steps - (s + 2);
+  if (younger >= 2) {
+    vm_wait<2 * kLoads>();
+  } else if (younger == 1) {
+    vm_wait<kLoads>();
+  } else {
+    vm_wait<0>();
+  }
+  // the direct loads of stage s + 1 have landed (vmcnt above) and every LDS
+  // read of this wave has completed (lgkmcnt(0) in the last k-step): a bare barrier
+  // suffices, where a fenced one would also wait for the younger stages
+  __builtin_amdgcn_s_barrier();
+}
+
+template <int WM, int WN, int QM, int QN>
+__global__ __launch_bounds__(kThreads) void gemm_ring_kernel(GemmArgs g) {
+  constexpr int TM = WM * QM * 32, TN = WN * QN * 32;
+  constexpr int kLoads = (TM + TN) / 64;
+  static_assert(WM * WN == kThreads / 64, "4 waves");
+  __shared__ __attribute__((aligned(1024))) char smem[kRing * kKc * (TM + TN) * 4];
+
+  const int tiles_n = (g.N + TN - 1) / TN;
+  const int m_tiles0 = (g.job[0].M + TM - 1) / TM;
+  int tt = blockIdx.x;
+  const bool second = tt >= m_tiles0 * tiles_n;
+  if (second) {
+    if (g.n_jobs < 2) return;
+    tt -= m_tiles0 * tiles_n;
+  }
+  RingTile t;
+  t.A = second ? g.job[1].A : g.job[0].A;
+  float* C = second ? g.job[1].C : g.job[0].C;
+  t.M = second ? g.job[1].M : g.job[0].M;
+  t.lda = second ? g.job[1].lda : g.job[0].lda;
+  const int64_t ldc = second ? g.job[1].ldc : g.job[0].ldc;
+  const int sub = second ? g.job[1].sub : g.job[0].sub;
+  t.m0 = (tt / tiles_n) * TM;
+  t.n0 = (tt % tiles_n) * TN;
+  if (t.m0 >= t.M) return;
+  t.B = g.B;
+  t.ldb = g.ldb;
+  t.N = g.N;
+  t.K = g.K;
+  t.steps = (g.K + kKc - 1) / kKc;
+  t.lane = threadIdx.x & 63;
+  t.wave = threadIdx.x >> 6;
+  const int h = t.lane >> 5, l32 = t.lane & 31;
+  const int wm0 = (t.wave / WN) * QM * 32, wn0 = (t.wave % WN) * QN * 32;
+
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(ISPA_LDS const void*)smem;
+  uint32_t oa[QM], ob[QN];
+#pragma unroll
+  for (int i = 0; i < QM; ++i) oa[i] = lds0 + h * TM * 4 + (((wm0 + 32 * i + l32) ^ (32 * h)) << 2);
+#pragma unroll
+  for (int j = 0; j < QN; ++j) ob[j] = lds0 + kKc * TM * 4 + h * TN * 4 + (((wn0 + 32 * j + l32) ^ (32 * h)) << 2);
+
+  f32x16 acc[QM][QN];
+#pragma unroll
+  for (int i = 0; i < QM; ++i)
+#pragma unroll
+    for (int j = 0; j < QN; ++j) acc[i][j] = f32x16{};
+
+  for (int s = 0; s < 3 && s < t.steps; ++s) ring_load<TM, TN>(t, smem, s);
+  if (t.steps >= 3) {
+    vm_wait<2 * kLoads>();
+  } else if (t.steps == 2) {
+    vm_wait<kLoads>();
+  } else {
+    vm_wait<0>();
+  }
+  __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
+  for (int s = 0; s < t.steps; s += kRing) {
+    ring_stage<0, TM, TN, QM, QN>(t, smem, oa, ob, acc, s);
+    if (s + 1 < t.steps) ring_stage<1, TM, TN, QM, QN>(t, smem, oa, ob, acc, s + 1);
+    if (s + 2 < t.steps) ring_stage<2, TM, TN, QM, QN>(t, smem, oa, ob, acc, s + 2);
+    if (s + 3 < t.steps) ring_stage<3, TM, TN, QM, QN>(t, smem, oa, ob, acc, s + 3);
+  }
+
+  const int lane = t.lane;
+#pragma unroll
+  for (int i = 0; i < QM; ++i)
+#pragma unroll
+    for (int j = 0; j < QN; ++j) {
+      const int col = t.n0 + wn0 + 32 * j + l32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = t.m0 + wm0 + 32 * i + acc_row(r, lane);
+        if (row < t.M && col < t.N) {
+          float* p = C + (int64_t)row * ldc + col;
+          *p = sub ? *p - acc[i][j][r] : acc[i][j][r];
+        }
+      }
+    }
+}
+
+}  // namespace
+
+// Dinv: 64 x 64 inverses of the diagonal blocks of L, then X_I and P_I of the
+// 256-blocks.
 size_t solve_dinv_bytes(int d) {
   const int nblk = (d + kNb - 1) / kNb;
-  return (size_t)nblk * kNb * kNb * sizeof(float);
+  const int nb = (d + kBb - 1) / kBb;
+  return (size_t)nblk * kNb * kNb * sizeof(float) + 2 * (size_t)nb * kBb * kBb * sizeof(float);
 }
+
+namespace {
+
+// Launches C (-)= A B over `tiles` output tiles of one of two shapes: 128 x 128
+// when there are enough of them to fill the chip, else 64 x 64.
+hipError_t launch_gemm(const GemmArgs& g, int batches, hipStream_t stream) {
+  auto tiles_of = [&](int tm, int tn) {
+    int t = 0;
+    for (int j = 0; j < g.n_jobs; ++j) t += ((g.job[j].M + tm - 1) / tm) * ((g.N + tn - 1) / tn);
+    return t;
+  };
+  const int t128 = tiles_of(128, 128), t64 = tiles_of(64, 64);
+  // rounds of one workgroup per CU; a 64-tile costs a bit more than a quarter
+  const double c128 = (double)((t128 * batches + 255) / 256);
+  const double c64 = 0.3 * (double)((t64 * batches + 255) / 256);
+  if (c128 <= c64) {
+    hipLaunchKernelGGL((gemm_ring_kernel<2, 2, 2, 2>), dim3(t128, batches), dim3(kThreads), 0, stream, g);
+  } else {
+    hipLaunchKernelGGL((gemm_ring_kernel<2, 2, 1, 1>), dim3(t64, batches), dim3(kThreads), 0, stream, g);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
 
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda, float* delta_w,
                         const SolveWork& w, hipStream_t stream) {
   const int nblk = (d + kNb - 1) / kNb;
-  const int ctiles = (d_out + kNb - 1) / kNb;
+  const int nb = (d + kBb - 1) / kBb;
+  float* xinv = w.dinv + (size_t)nblk * kNb * kNb;  // [nb][256][256]
+  float* pinv = xinv + (size_t)nb * kBb * kBb;       // [nb][256][256]
+  float* L = w.L;
+  float* Y = w.work;
   {
     const int64_t total = (int64_t)d * d + (int64_t)d * d_out;
     int grid = (int)((total + 255) / 256);
     if (grid > 8192) grid = 8192;
-    hipLaunchKernelGGL(solve_init_kernel, dim3(grid), dim3(256), 0, stream, G, w.L, C, w.work, d, d_out, lambda,
+    hipLaunchKernelGGL(solve_init_kernel, dim3(grid), dim3(256), 0, stream, G, L, C, Y, d, d_out, lambda,
                        w.status);
   }
   for (int k = -1; k <= nblk - 2; ++k) {
     const int m = nblk - 1 - k;  // blocks in the trailing triangle
     const int grid = k < 0 ? nblk : m * (m + 1) / 2;
-    hipLaunchKernelGGL(chol_step_kernel, dim3(grid), dim3(kThreads), 0, stream, w.L, w.dinv, d, k, w.status);
+    hipLaunchKernelGGL(chol_step_kernel, dim3(grid), dim3(kThreads), 0, stream, L, w.dinv, d, k, w.status);
   }
-  for (int i = -1; i <= nblk - 2; ++i) {
-    const int rows = i < 0 ? 1 : nblk - 1 - i;
-    hipLaunchKernelGGL(trsm_fwd_kernel, dim3(rows * ctiles), dim3(kThreads), 0, stream, w.L, w.dinv, w.work,
-                       delta_w, d, d_out, i);
+  // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above
+  hipLaunchKernelGGL(inv256_kernel, dim3(nb, 4), dim3(kThreads), 0, stream, L, w.dinv, xinv, d);
+  {
+    GemmArgs g = {};
+    g.job[0] = GemmJob{xinv, pinv, kBb, kBb, kBb, 0};
+    g.n_jobs = 1;
+    g.B = xinv;
+    g.N = kBb;
+    g.K = kBb;
+    g.ldb = kBb;
+    g.batch_a = g.batch_b = g.batch_c = (int64_t)kBb * kBb;
+    hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 1, false>), dim3(16, nb), dim3(kThreads), 0, stream, g);
   }
-  for (int i = nblk; i >= 1; --i) {
-    const int rows = i == nblk ? 1 : i;
-    hipLaunchKernelGGL(trsm_bwd_kernel, dim3(rows * ctiles), dim3(kThreads), 0, stream, w.L, w.dinv, delta_w, d,
-                       d_out, i);
+  if (nb > 1) {
+    // Lh_rI = L_rI X_I in place: a workgroup owns 64 rows x the whole 256-block
+    GemmArgs g = {};
+    float* first = L + (int64_t)kBb * d;  // rows of block 1, columns of block 0
+    g.job[0] = GemmJob{first, first, d - kBb, d, d, 0};
+    g.n_jobs = 1;
+    g.B = xinv;
+    g.N = kBb;
+    g.K = kBb;
+    g.ldb = kBb;
+    g.batch_a = g.batch_c = (int64_t)kBb * d + kBb;
+    g.batch_b = (int64_t)kBb * kBb;
+    g.batch_dm = -kBb;
+    hipLaunchKernelGGL((gemm_kernel<1, 4, 2, 2, true>), dim3((d - kBb + 63) / 64, nb - 1), dim3(kThreads), 0,
+                       stream, g);
+    hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk), dim3(kThreads), 0, stream, L, d);
   }
-  hipLaunchKernelGGL(zero_scalars_kernel, dim3(1), dim3(64), 0, stream, w.scalars);
+  // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I
+  for (int I = 0; I < nb; ++I) {
+    const int kI = min(kBb, d - I * kBb);
+    GemmArgs g = {};
+    const int below = d - (I + 1) * kBb;
+    int j = 0;
+    if (below > 0) {
+      g.job[j++] = GemmJob{L + (int64_t)I * kBb * d + (int64_t)(I + 1) * kBb, Y + (int64_t)(I + 1) * kBb * d_out,
+                           below, d, d_out, 1};
+    }
+    g.job[j++] = GemmJob{pinv + (int64_t)I * kBb * kBb, delta_w + (int64_t)I * kBb * d_out, kI, kBb, d_out, 0};
+    g.n_jobs = j;
+    g.B = Y + (int64_t)I * kBb * d_out;
+    g.N = d_out;
+    g.K = kI;
+    g.ldb = d_out;
+    const hipError_t e = launch_gemm(g, 1, stream);
+    if (e != hipSuccess) return e;
+  }
+  // backward sweep: dW_I -= Lh_JI^T dW_J (I < J)
+  for (int J = nb - 1; J >= 1; --J) {
+    const int kJ = min(kBb, d - J * kBb);
+    GemmArgs g = {};
+    g.job[0] = GemmJob{L + (int64_t)J * kBb * d, delta_w, J * kBb, d, d_out, 1};
+    g.n_jobs = 1;
+    g.B = delta_w + (int64_t)J * kBb * d_out;
+    g.N = d_out;
+    g.K = kJ;
+    g.ldb = d_out;
+    const hipError_t e = launch_gemm(g, 1, stream);
+    if (e != hipSuccess) return e;
+  }
+  // the P_I area is free once the forward sweep has run: it holds the partial sums
   const int64_t n = (int64_t)d * d_out;
-  int eg = (int)((n + kThreads - 1) / kThreads);
-  if (eg > 256) eg = 256;  // one fp64 atomic pair per block
-  hipLaunchKernelGGL(eps_kernel, dim3(eg), dim3(kThreads), 0, stream, delta_w, C, n, w.scalars);
+  hipLaunchKernelGGL(eps_partial_kernel, dim3(kEpsBlocks), dim3(kThreads), 0, stream, delta_w, C, n, (double*)pinv);
+  hipLaunchKernelGGL(eps_final_kernel, dim3(1), dim3(kThreads), 0, stream, (const double*)pinv, kEpsBlocks,
+                     w.scalars);
   return hipGetLastError();
 }
 

@@ -304,7 +304,10 @@ __device__ __forceinline__ void gram_stage(const GramArgs& a, const GramTile& t,
   } else {
     vm_wait<0>();
   }
-  __syncthreads();
+  // the direct loads of stage s + 1 have landed (vmcnt above) and every LDS
+  // read of this wave has completed (lgkmcnt(0) before the last MFMAs): a bare barrier
+  // suffices, where a fenced one would also wait for the younger stages
+  __builtin_amdgcn_s_barrier();
 }
 
 // Output tile k of one split in panel-group order: row panels (X columns) are
@@ -399,7 +402,7 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   } else {
     vm_wait<0>();
   }
-  __syncthreads();
+  __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
   for (int s = 0; s < t.steps; s += kGRing) {
     gram_stage<0>(a, t, smem, A, B, acc, s);
     if (s + 1 < t.steps) gram_stage<1>(a, t, smem, A, B, acc, s + 1);

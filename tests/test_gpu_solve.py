@@ -19,9 +19,11 @@ def rows(wid, i, n, d, dtype=torch.bfloat16):
     return synth.normal((n, d), synth.seed_of(wid, i, synth.X), DEV, dtype=dtype)
 
 
-def test_solve_matches_oracle_ragged():
-    # d not a multiple of the 64-wide panel; rows > d so G is well conditioned
-    d_in, d_out, n, lam = 200, 72, 700, 0.5
+@pytest.mark.parametrize("d_in,d_out,n", [(200, 72, 700), (776, 328, 1600)])
+def test_solve_matches_oracle_ragged(d_in, d_out, n):
+    # d not a multiple of the 64-wide panel (776: three 256-blocks and a ragged
+    # fourth of 8 rows); rows > d so G is well conditioned
+    lam = 0.5
     x = rows(30, 0, n, d_in)
     yf = synth.normal((n, d_out), synth.seed_of(30, 0, synth.Y_FULL), DEV, dtype=torch.float32)
     yl = synth.normal((n, d_out), synth.seed_of(30, 0, synth.Y_LOCAL), DEV, dtype=torch.float32)
