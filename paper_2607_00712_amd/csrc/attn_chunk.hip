@@ -38,7 +38,8 @@
 //   online softmax is a per-lane scalar.
 //
 // Softmax uses exp2 with the logit scale folded into one FMA:
-//   p = 2^(s * c - m * c), c = scale * log2(e); LSE = m * scale + ln(l).
+//   p = 2^(s * c - m * c), c = scale * log2(e); LSE = m * scale + ln(l),
+// where the reference m trails the running max by at most 8 (log2 units).
 //
 // Workgroups are remapped so that the 8 XCDs (dispatched round-robin) each own
 // a contiguous run of (head, query tile) work items: tiles of one head share
@@ -56,6 +57,7 @@ constexpr int kBqWave = 32;
 constexpr int kBq = kWaves * kBqWave;  // queries per workgroup
 constexpr int kBk = 64;                // keys per tile
 constexpr int kXcds = 8;
+constexpr float kLazyLog2 = 8.f;       // rescale threshold of the softmax reference
 
 template <int D>
 struct Cfg {
@@ -140,6 +142,29 @@ __device__ __forceinline__ void tr_wait(u32x2 (&r)[2][NB], bf16x8* out) {
   }
 }
 
+// The kSlices K operands (A of S^T = K Q^T) of one half; IMM is the
+// compile-time byte offset of the half (buffer, half rows). `dep` is a value
+// computed from the previous half's scores: taking it as an input orders the
+// reads after the MFMAs that consumed the previous contents of r.
+template <int NS, int IMM>
+__device__ __forceinline__ void k_issue(const uint32_t (&addr)[NS], u32x4 (&r)[NS], float dep) {
+#pragma unroll
+  for (int kk = 0; kk < NS; ++kk)
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r[kk]) : "v"(addr[kk]), "i"(IMM), "v"(dep));
+}
+template <int N>
+__device__ __forceinline__ void k_wait(u32x4 (&r)[8]) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%8)"
+               : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
+               : "i"(N));
+}
+template <int N>
+__device__ __forceinline__ void k_wait(u32x4 (&r)[4]) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]) : "i"(N));
+}
+
 // Lane-pair (l, l ^ 32) exchange with v_permlane32_swap: it swaps the upper 32
 // lanes of its first operand with the lower 32 lanes of its second, so with
 // A = B = x in two registers it leaves A = [x_lo, x_lo] and B = [x_hi, x_hi].
@@ -155,10 +180,23 @@ __device__ __forceinline__ float l_run_total(float x) {
   pair_halves(x, lo, hi);
   return lo + hi;
 }
+// Maxima of finite-or-minus-infinity scores as plain v_max3 / v_max (fmaxf
+// would first quiet possible signalling NaNs with an extra instruction per
+// operand; scores are never NaN).
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max2(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 __device__ __forceinline__ float pair_max(float x) {
   float lo, hi;
   pair_halves(x, lo, hi);
-  return fmaxf(lo, hi);
+  return max2(lo, hi);
 }
 
 // Tile t of the flattened range list: first key and number of valid keys.
@@ -181,17 +219,20 @@ __device__ __forceinline__ void tile_of(const AttnRanges& r, int tb1, int tb2, i
 // use the LDS-load builtin.)
 template <int D>
 __device__ __forceinline__ void stage_tile(const AttnArgs& a, int64_t base, int nv, char* dst,
-                                           const int* voffk, const int* voffv, int wave) {
+                                           int voffk, int voffv, int wave) {
   using C = Cfg<D>;
   const int nbytes = (int)(((int64_t)(nv - 1) * a.ld + D) * 2);
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(a.k + base, nbytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(a.v + base, nbytes);
+  // load q covers the rows of load 0 plus q * (kThreads / chunksPerRow), with
+  // the same swizzles (they depend on the row mod 16)
+  const int qstride = (int)((kThreads / C::chunksPerRow) * a.ld * 2);
 #pragma unroll
   for (int q = 0; q < C::loadsPerThread; ++q) {
     const int wslot = (q * kWaves + wave) * 64 * 16;  // wave-uniform LDS destination
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (ISPA_LDS void*)(dst + wslot), 16, voffk[q], 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (ISPA_LDS void*)(dst + C::tileBytes + wslot), 16, voffv[q], 0,
-                                             0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (ISPA_LDS void*)(dst + wslot), 16, voffk + q * qstride, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (ISPA_LDS void*)(dst + C::tileBytes + wslot), 16,
+                                             voffv + q * qstride, 0, 0, 0);
   }
 }
 
@@ -200,12 +241,14 @@ template <int D>
 struct Wave {
   using C = Cfg<D>;
   f32x16 acc[C::dBlocks];      // O^T, one 32 x 32 block per 32 head dims
-  float m_run;                 // running max (raw score units) of this lane's query
+  float m_run;                 // softmax reference (raw score units) of this lane's query
+  float lazy;                  // kLazyLog2 in raw score units
   float l_run;                 // running sum of p (this lane's half of the keys)
   bf16x8 qf[C::kSlices];       // Q^T operand
-  int koff[C::kSlices];        // K operand byte offsets inside a tile
+  u32x4 kr[C::kSlices];        // K operands of the current half
+  uint32_t koff[C::kSlices];   // K operand LDS addresses (buffer 0, half 0)
   uint32_t vaddr[2][C::dBlocks];  // V transpose-read LDS addresses (buffer 0, slice 0)
-  int voffk[C::loadsPerThread], voffv[C::loadsPerThread];  // direct-load offsets
+  int voffk, voffv;            // direct-load offsets of a thread's first load
 };
 
 struct Loop {
@@ -241,15 +284,12 @@ __device__ __forceinline__ void finish(const AttnArgs& a, Wave<D>& w, const Loop
 template <int D, int BUF, int B>
 __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const Loop& L, const char* smem, int nv) {
   using C = Cfg<D>;
-  constexpr int kBase = BUF * 2 * C::tileBytes + 32 * B * C::rowBytes;
   constexpr int vBase = BUF * 2 * C::tileBytes + C::tileBytes;
-  // S^T = K . Q^T (rows 32B + ql share the swizzle of row ql)
+  // S^T = K . Q^T (rows 32B + ql share the swizzle of row ql); the K operands
+  // of this half are in registers
   f32x16 sc = f32x16{};
 #pragma unroll
-  for (int kk = 0; kk < C::kSlices; ++kk) {
-    const bf16x8 kf = *(const bf16x8*)(smem + kBase + w.koff[kk]);
-    sc = mfma32(kf, w.qf[kk], sc);
-  }
+  for (int kk = 0; kk < C::kSlices; ++kk) sc = mfma32(__builtin_bit_cast(bf16x8, w.kr[kk]), w.qf[kk], sc);
   // V^T operands of this half's two 16-key slices, in flight during the softmax
   u32x2 v0[2][C::dBlocks], v1[2][C::dBlocks];
   tr_issue<C::dBlocks, vBase + 16 * (2 * B) * C::rowBytes>(w.vaddr, v0);
@@ -262,16 +302,16 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
       if (key >= nv) sc[r] = -INFINITY;
     }
   }
-  float tmax = fmaxf(sc[0], sc[1]);
+  float tmax = max3(sc[0], sc[1], sc[2]);
 #pragma unroll
-  for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, sc[r]);
-  tmax = pair_max(tmax);
-  // O and l are rescaled only when some row's running max grew: after the
-  // first few tiles most steps skip the multiplies. The reference stays the
-  // exact running max, so the largest weight of a row is exactly 1 and carries
-  // no bf16 rounding error (a stale reference would put rounding error on the
-  // dominant terms).
-  if (__any(tmax > w.m_run)) {
+  for (int r = 3; r < 15; r += 2) tmax = max3(tmax, sc[r], sc[r + 1]);
+  tmax = pair_max(max2(tmax, sc[15]));
+  // O and l are rescaled only when some row's max exceeds its reference by
+  // more than kLazyLog2 (log2 units): the weights then stay below 2^kLazyLog2
+  // and after the first tiles almost every step skips the multiplies. l sums
+  // the unrounded weights in fp32, so the LSE is unaffected by the bf16
+  // rounding of the weights.
+  if (__any(tmax > w.m_run + w.lazy)) {
     const float m_new = fmaxf(w.m_run, tmax);
     const float alpha = exp2_hw((w.m_run - m_new) * a.scale_log2);
     w.l_run *= alpha;
@@ -280,14 +320,15 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
     w.m_run = m_new;
   }
   const float mc = w.m_run * a.scale_log2;
-  float psum = 0.f;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float p = exp2_hw(fmaf(sc[r], a.scale_log2, -mc));
-    sc[r] = p;
-    psum += p;
+  for (int r = 0; r < 16; ++r) sc[r] = exp2_hw(fmaf(sc[r], a.scale_log2, -mc));
+  float s0 = sc[0] + sc[1], s1 = sc[2] + sc[3];
+#pragma unroll
+  for (int r = 4; r < 16; r += 4) {
+    s0 += sc[r] + sc[r + 1];
+    s1 += sc[r + 2] + sc[r + 3];
   }
-  w.l_run += psum;
+  w.l_run += s0 + s1;
   bf16x8 pf0, pf1;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -299,7 +340,14 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
   tr_wait<2 * C::dBlocks, C::dBlocks>(v0, vf);
 #pragma unroll
   for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf0, w.acc[db]);
-  tr_wait<0, C::dBlocks>(v1, vf);
+  if constexpr (B == 0) {
+    // the second half's K operands, in flight during the last MFMAs (tmax
+    // depends on this half's S^T MFMAs, which have read the old ones)
+    k_issue<C::kSlices, BUF * 2 * C::tileBytes + 32 * C::rowBytes>(w.koff, w.kr, tmax);
+    tr_wait<C::kSlices, C::dBlocks>(v1, vf);
+  } else {
+    tr_wait<0, C::dBlocks>(v1, vf);
+  }
 #pragma unroll
   for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf1, w.acc[db]);
 }
@@ -318,7 +366,11 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, Wave<D>& w, const L
     tile_of(a.r, L.tb1, L.tb2, t + 1, k1, n1);
     stage_tile<D>(a, k1 * a.ld + L.hoff, n1, smem + (BUF ^ 1) * 2 * C::tileBytes, w.voffk, w.voffv, L.wave);
   }
+  // half 0's K operands: the tile became visible at the last barrier
+  k_issue<C::kSlices, BUF * 2 * C::tileBytes>(w.koff, w.kr, 0.f);
+  k_wait<0>(w.kr);
   half_step<D, BUF, 0>(a, w, L, smem, nv);
+  k_wait<0>(w.kr);
   half_step<D, BUF, 1>(a, w, L, smem, nv);
   __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct loads have landed
   __syncthreads();
@@ -370,18 +422,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // Direct load q of this thread covers 16-byte slot (q * kWaves + wave) * 64 + lane
   // of a tile: row = slot / chunksPerRow, stored chunk = slot % chunksPerRow,
   // which holds logical chunk (stored ^ swizzle(row)) of that key row.
-#pragma unroll
-  for (int q = 0; q < C::loadsPerThread; ++q) {
-    const int slot = (q * kWaves + L.wave) * 64 + lane;
+  {
+    const int slot = L.wave * 64 + lane;
     const int row = slot / C::chunksPerRow;
     const int stored = slot % C::chunksPerRow;
-    w.voffk[q] = (int)((row * a.ld + (stored ^ swz_k<D>(row)) * 8) * 2);
-    w.voffv[q] = (int)((row * a.ld + (stored ^ swz_v<D>(row)) * 8) * 2);
+    w.voffk = (int)((row * a.ld + (stored ^ swz_k<D>(row)) * 8) * 2);
+    w.voffv = (int)((row * a.ld + (stored ^ swz_v<D>(row)) * 8) * 2);
   }
-#pragma unroll
-  for (int kk = 0; kk < C::kSlices; ++kk) w.koff[kk] = chunk_off<D>(ql, 2 * kk + L.hh, swz_k<D>(ql));
   {
     const uint32_t lds0 = lds_addr(smem);
+#pragma unroll
+    for (int kk = 0; kk < C::kSlices; ++kk) w.koff[kk] = lds0 + chunk_off<D>(ql, 2 * kk + L.hh, swz_k<D>(ql));
     const int g = lane >> 4, sl = lane & 15;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2)
@@ -398,6 +449,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   for (int i = 0; i < C::dBlocks; ++i) w.acc[i] = f32x16{};
   w.m_run = -INFINITY;
   w.l_run = 0.f;
+  w.lazy = kLazyLog2 / a.scale_log2;
 
   if (L.n_tiles > 0) {
     int64_t k0;
