@@ -48,7 +48,7 @@ PEAK_HBM_GBS = 8000.0
 # (profiles/attn_chunk_wan13b_dual.md, profiles/hbm_copy_calibration.md). Valid
 # only for the kernel source they were taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "52f017a08660b581", "bytes_per_launch": 521.3e6},
+    "1.3b": {"attn_chunk_sha256_16": "710087735d980b64", "bytes_per_launch": 400.1e6},
 }
 
 

@@ -9,7 +9,8 @@
 // history keys gives the LSE fusion of Eq. 11-12 without a second pass.
 //
 // Work decomposition
-//   workgroup = 4 waves = 128 queries of one head; each wave owns 32 queries.
+//   workgroup = 8 waves (two per SIMD) = 256 queries of one head; each wave
+//   owns 32 queries, and every K / V tile is staged once for all 256.
 //   Keys are visited in tiles of 64 rows. Only tiles that intersect the key set
 //   are visited; the tile at the end of each contiguous range is masked
 //   element-wise.
@@ -51,7 +52,7 @@
 namespace ispa {
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBqWave = 32;
 constexpr int kBq = kWaves * kBqWave;  // queries per workgroup
@@ -180,19 +181,15 @@ __device__ __forceinline__ float l_run_total(float x) {
   pair_halves(x, lo, hi);
   return lo + hi;
 }
-// Maxima of finite-or-minus-infinity scores as plain v_max3 / v_max (fmaxf
+// Maxima of finite-or-minus-infinity scores as v_maximum3 / v_maximum (fmaxf
 // would first quiet possible signalling NaNs with an extra instruction per
-// operand; scores are never NaN).
+// operand; scores are never NaN). They stay compiler-visible instructions:
+// the scores are MFMA results, and only the compiler inserts the wait states
+// that a VALU read of an MFMA destination needs.
 __device__ __forceinline__ float max3(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
 }
-__device__ __forceinline__ float max2(float a, float b) {
-  float r;
-  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
-}
+__device__ __forceinline__ float max2(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float pair_max(float x) {
   float lo, hi;
   pair_halves(x, lo, hi);

@@ -94,13 +94,19 @@ def test_without_lse_outputs():
     assert torch.equal(out, out2)
 
 
-def test_deterministic():
-    q, k, v = synth.chunk_qkv(6, 0, 0, 200, 900, 256, DEV)
-    a = ispa.attn_chunk(q, k, v, 900, 300, 2, sink_len=10, dual=True)
-    b = ispa.attn_chunk(q, k, v, 900, 300, 2, sink_len=10, dual=True)
-    torch.cuda.synchronize()
-    for x, y in zip(a, b):
-        assert torch.equal(x, y)
+@pytest.mark.parametrize("shape", [(64, 300, 100, 0), (200, 900, 300, 10), (700, 1100, 400, 0)])
+def test_deterministic(shape):
+    # repeated launches are bit-identical (the two waves sharing a SIMD make
+    # any missing wait on an MFMA result show up as run-to-run differences)
+    n_q, N, w, s = shape
+    q, k, v = synth.chunk_qkv(6, 0, 0, n_q, N, 256, DEV)
+    first = ispa.attn_chunk(q, k, v, N, w, 2, sink_len=s, dual=True)
+    for i in range(8):
+        again = ispa.attn_chunk(q, k, v, N, w, 2, sink_len=s, dual=True, need_lse=(i % 2 == 0))
+        torch.cuda.synchronize()
+        for x, y in zip(first, again):
+            if y is not None:
+                assert torch.equal(x, y), f"launch {i + 1} differs"
 
 
 def test_binding_rejects_bad_tensors():
