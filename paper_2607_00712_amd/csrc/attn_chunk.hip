@@ -47,6 +47,7 @@
 // the K/V stream through one XCD's L2.
 #include "ispa_internal.h"
 
+#include <limits.h>
 #include <math.h>
 
 namespace ispa {
@@ -153,6 +154,23 @@ __device__ __forceinline__ void k_issue(const uint32_t (&addr)[NS], u32x4 (&r)[N
   for (int kk = 0; kk < NS; ++kk)
     asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r[kk]) : "v"(addr[kk]), "i"(IMM), "v"(dep));
 }
+// Wait until K operand `r` (issued N reads before the last one) has arrived.
+template <int N>
+__device__ __forceinline__ void k_wait_one(u32x4& r) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(r) : "i"(N));
+}
+// S^T += K . Q^T over the slices KK.. of a half, each MFMA after its own wait.
+template <int NS, int KK = 0>
+__device__ __forceinline__ void qk_chain(u32x4 (&kr)[NS], const bf16x8 (&qf)[NS], f32x16& sc) {
+  if constexpr (KK < NS) {
+    k_wait_one<NS - 1 - KK>(kr[KK]);
+    sc = mfma32(__builtin_bit_cast(bf16x8, kr[KK]), qf[KK], sc);
+    // keep the next wait behind this MFMA (only VALU / SALU work may move across)
+    __builtin_amdgcn_sched_barrier(0x6);
+    qk_chain<NS, KK + 1>(kr, qf, sc);
+  }
+}
 template <int N>
 __device__ __forceinline__ void k_wait(u32x4 (&r)[8]) {
   static_assert(N >= 0 && N <= 15, "lgkmcnt range");
@@ -196,14 +214,24 @@ __device__ __forceinline__ float pair_max(float x) {
   return max2(lo, hi);
 }
 
-// Tile t of the flattened range list: first key and number of valid keys.
-// tb1/tb2 are the tile indices where ranges 1 and 2 start.
-__device__ __forceinline__ void tile_of(const AttnRanges& r, int tb1, int tb2, int t,
-                                        int64_t& key0, int& nvalid) {
-  const bool in2 = r.n_total > 2 && t >= tb2;
-  const bool in1 = !in2 && r.n_total > 1 && t >= tb1;
-  const int64_t begin = in2 ? r.begin[2] : (in1 ? r.begin[1] : r.begin[0]);
-  const int64_t end = in2 ? r.end[2] : (in1 ? r.end[1] : r.end[0]);
+// The flattened range list, held in registers for the key loop: range i
+// covers keys [b_i, e_i) and starts at tile tb_i (tb_i = INT_MAX for an absent
+// range). A scalar load inside the loop would also count in lgkmcnt and, unlike
+// LDS reads, complete out of order, which the counted LDS waits cannot allow.
+struct TileMap {
+  int64_t b0, b1, b2, e0, e1, e2;
+  int tb1, tb2;
+};
+// Tile t: first key and number of valid keys.
+__device__ __forceinline__ void tile_of(const TileMap& m, int t, int64_t& key0, int& nvalid) {
+  // selects of values, not of member lvalues (those would select addresses
+  // and keep the map in memory)
+  const int64_t b0 = m.b0, b1 = m.b1, b2 = m.b2, e0 = m.e0, e1 = m.e1, e2 = m.e2;
+  const int tb1 = m.tb1, tb2 = m.tb2;
+  const bool in2 = t >= tb2;
+  const bool in1 = !in2 && t >= tb1;
+  const int64_t begin = in2 ? b2 : (in1 ? b1 : b0);
+  const int64_t end = in2 ? e2 : (in1 ? e1 : e0);
   const int first = in2 ? tb2 : (in1 ? tb1 : 0);
   key0 = begin + (int64_t)(t - first) * kBk;
   const int64_t left = end - key0;
@@ -249,7 +277,8 @@ struct Wave {
 };
 
 struct Loop {
-  int tb1, tb2, n_tiles, n_tiles_local, hoff, wave, hh;
+  TileMap map;
+  int n_tiles, n_tiles_local, hoff, wave, hh;
   bool dual;
 };
 
@@ -284,9 +313,10 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
   constexpr int vBase = BUF * 2 * C::tileBytes + C::tileBytes;
   // S^T = K . Q^T (rows 32B + ql share the swizzle of row ql); the K operands
   // of this half are in registers
+  // (each MFMA waits only for its own K operand: the reads of this half are
+  // the only LDS operations in flight and complete in issue order)
   f32x16 sc = f32x16{};
-#pragma unroll
-  for (int kk = 0; kk < C::kSlices; ++kk) sc = mfma32(__builtin_bit_cast(bf16x8, w.kr[kk]), w.qf[kk], sc);
+  qk_chain<C::kSlices>(w.kr, w.qf, sc);
   // V^T operands of this half's two 16-key slices, in flight during the softmax
   u32x2 v0[2][C::dBlocks], v1[2][C::dBlocks];
   tr_issue<C::dBlocks, vBase + 16 * (2 * B) * C::rowBytes>(w.vaddr, v0);
@@ -349,28 +379,27 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
   for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf1, w.acc[db]);
 }
 
-// One 64-key tile from LDS buffer BUF; the next tile's direct loads into the
-// other buffer are issued first.
+// One 64-key tile (nv valid keys) from LDS buffer BUF; the next tile's direct
+// loads into the other buffer are issued while the first K operands are in
+// flight. Returns the next tile's number of valid keys.
 template <int D, int BUF>
-__device__ __forceinline__ void tile_step(const AttnArgs& a, Wave<D>& w, const Loop& L, char* smem, int t) {
+__device__ __forceinline__ int tile_step(const AttnArgs& a, Wave<D>& w, const Loop& L, char* smem, int t, int nv) {
   using C = Cfg<D>;
-  int64_t key0;
-  int nv;
-  tile_of(a.r, L.tb1, L.tb2, t, key0, nv);
-  if (t + 1 < L.n_tiles) {
-    int64_t k1;
-    int n1;
-    tile_of(a.r, L.tb1, L.tb2, t + 1, k1, n1);
-    stage_tile<D>(a, k1 * a.ld + L.hoff, n1, smem + (BUF ^ 1) * 2 * C::tileBytes, w.voffk, w.voffv, L.wave);
-  }
   // half 0's K operands: the tile became visible at the last barrier
   k_issue<C::kSlices, BUF * 2 * C::tileBytes>(w.koff, w.kr, 0.f);
-  k_wait<0>(w.kr);
+  int n1 = 0;
+  if (t + 1 < L.n_tiles) {
+    int64_t k1;
+    tile_of(L.map, t + 1, k1, n1);
+    stage_tile<D>(a, k1 * a.ld + L.hoff, n1, smem + (BUF ^ 1) * 2 * C::tileBytes, w.voffk, w.voffv, L.wave);
+  }
   half_step<D, BUF, 0>(a, w, L, smem, nv);
-  k_wait<0>(w.kr);
+  // the last P V MFMAs of half 0 are issued before half 1 waits for its K
+  __builtin_amdgcn_sched_barrier(0);
   half_step<D, BUF, 1>(a, w, L, smem, nv);
   __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct loads have landed
   __syncthreads();
+  return n1;
 }
 
 template <int D>
@@ -409,8 +438,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int nt0 = (int)((a.r.end[0] - a.r.begin[0] + kBk - 1) / kBk);
   const int nt1 = a.r.n_total > 1 ? (int)((a.r.end[1] - a.r.begin[1] + kBk - 1) / kBk) : 0;
   const int nt2 = a.r.n_total > 2 ? (int)((a.r.end[2] - a.r.begin[2] + kBk - 1) / kBk) : 0;
-  L.tb1 = nt0;
-  L.tb2 = nt0 + nt1;
+  L.map.b0 = a.r.begin[0];
+  L.map.e0 = a.r.end[0];
+  L.map.b1 = a.r.n_total > 1 ? a.r.begin[1] : 0;
+  L.map.e1 = a.r.n_total > 1 ? a.r.end[1] : 0;
+  L.map.b2 = a.r.n_total > 2 ? a.r.begin[2] : 0;
+  L.map.e2 = a.r.n_total > 2 ? a.r.end[2] : 0;
+  L.map.tb1 = a.r.n_total > 1 ? nt0 : INT_MAX;
+  L.map.tb2 = a.r.n_total > 2 ? nt0 + nt1 : INT_MAX;
   L.n_tiles = nt0 + nt1 + nt2;
   L.n_tiles_local = a.r.n_local == 1 ? nt0 : nt0 + nt1;
   L.dual = a.out_local != nullptr;
@@ -448,21 +483,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   w.l_run = 0.f;
   w.lazy = kLazyLog2 / a.scale_log2;
 
+  int nv = 0;  // valid keys of the tile in the current buffer
   if (L.n_tiles > 0) {
     int64_t k0;
-    int n0;
-    tile_of(a.r, L.tb1, L.tb2, 0, k0, n0);
-    stage_tile<D>(a, k0 * a.ld + L.hoff, n0, smem, w.voffk, w.voffv, L.wave);
+    tile_of(L.map, 0, k0, nv);
+    stage_tile<D>(a, k0 * a.ld + L.hoff, nv, smem, w.voffk, w.voffv, L.wave);
   }
   __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
   __syncthreads();
 
   for (int t = 0; t < L.n_tiles; t += 2) {
     if (L.dual && t == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
-    tile_step<D, 0>(a, w, L, smem, t);
+    nv = tile_step<D, 0>(a, w, L, smem, t, nv);
     if (t + 1 < L.n_tiles) {
       if (L.dual && t + 1 == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
-      tile_step<D, 1>(a, w, L, smem, t + 1);
+      nv = tile_step<D, 1>(a, w, L, smem, t + 1, nv);
     }
   }
   if (L.dual && L.n_tiles_local == L.n_tiles) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
