@@ -15,8 +15,8 @@ Inputs are seeded synthetic N(0, 1) bf16 tensors already resident in HBM.
 `value` is the algorithmic TFLOP/s of the whole step (visible keys only for
 attention, the symmetric half of X^T X, D^3/3 + 2 D^2 D_out for the solve)
 divided by the measured step time. The roofline object covers the dominant
-kernel (the dual-stream attention), timed with HIP events on the stream it
-runs on. `cpu_baseline` times the CPU oracle on a bounded sample of the same
+call (the dual-stream attention: its kernel and, when the work is split over
+the chip, the merge kernel), timed with HIP events on the stream it runs on. `cpu_baseline` times the CPU oracle on a bounded sample of the same
 step. `--workload 14b` runs the 14B-like shape instead (40 heads, 98280 keys).
 """
 
@@ -43,12 +43,13 @@ WORKLOADS = {
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0
 
-# HBM bytes per launch of the dual-stream attention kernel, from rocprofv3
-# FETCH_SIZE and WRITE_SIZE scaled by the plain-copy calibration
-# (profiles/attn_chunk_wan13b_dual.md, profiles/hbm_copy_calibration.md). Valid
-# only for the kernel source they were taken on; reported as null otherwise.
+# HBM bytes of one dual-stream attention call (the attention kernel plus the
+# merge of its split work items), from rocprofv3 FETCH_SIZE and WRITE_SIZE
+# scaled by the plain-copy calibration (profiles/attn_chunk_wan13b_dual.md,
+# profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
+# taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "710087735d980b64", "bytes_per_launch": 400.1e6},
+    "1.3b": {"attn_chunk_sha256_16": "56ebf55894cb74a1", "bytes_per_launch": 767.4e6},
 }
 
 
@@ -251,14 +252,14 @@ def main():
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
-            "kernel": "attn_chunk_kernel<128> (F-Layer, dual stream)",
+            "kernel": "attn_chunk_kernel<128> + attn_merge_split_kernel<128> (F-Layer, dual stream; one call)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+            "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE of both kernels, copy-calibrated)",
         },
         "breakdown": {
             "attn_dual_ms": round(avg["attn_dual"], 4),

@@ -100,6 +100,71 @@ int ispa_attn_chunk(const void* q, const void* k_cache, const void* v_cache,
                     float* out, float* lse, float* out_local, float* lse_local,
                     hipStream_t stream);
 
+/*
+ * ispa_attn_chunk with the work split over the whole chip. Whole work items
+ * (256 queries of one head over all their keys) per workgroup can leave a
+ * large part of the last round of workgroups idle (e.g. 12 heads x 19 query
+ * blocks = 228 work items on 256 compute units). Split, every workgroup takes
+ * an equal run of (work item, 64-key tile) units; runs that end inside a work
+ * item leave a normalised partial output and LSE in the workspace, and a merge
+ * kernel combines them with Eq. 11-12. The results agree with ispa_attn_chunk
+ * within rounding (the merge reassociates the softmax sums).
+ *
+ *   segments   < 0: never split (exactly ispa_attn_chunk)
+ *              0:   split when whole work items would fill the device poorly
+ *              > 0: split into exactly this many runs (at most the number of
+ *                   units)
+ *   workspace  device, 256-byte aligned, at least ispa_attn_workspace_bytes
+ *              bytes for the same arguments on the same device; may be NULL
+ *              when that is 0. Used only during the call's device work.
+ * Other arguments and outputs as for ispa_attn_chunk.
+ */
+int ispa_attn_chunk_ws(const void* q, const void* k_cache, const void* v_cache,
+                       int64_t cache_len, int64_t window, int64_t sink_len,
+                       int32_t n_q, int32_t n_heads, int32_t head_dim, float scale,
+                       float* out, float* lse, float* out_local, float* lse_local,
+                       int32_t segments, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/* Workspace bytes ispa_attn_chunk_ws needs for these arguments on the current
+ * device (dual != 0: the dual-stream form); 0 when it does not split or the
+ * arguments are invalid. */
+size_t ispa_attn_workspace_bytes(int64_t cache_len, int64_t window, int64_t sink_len,
+                                 int32_t n_q, int32_t n_heads, int32_t head_dim,
+                                 int32_t dual, int32_t segments);
+
+/*
+ * Attention over an explicit key set: one branch of the decomposable form of
+ * Sec. 3.4 (Eq. 9-10), e.g. the history alone.
+ *
+ *   ranges     host array of n_ranges [begin, end) pairs of cache rows, each
+ *              0 <= begin < end <= 2^31; the rows must exist in k_cache and
+ *              v_cache. The set is their union (ranges should not overlap).
+ *   n_ranges   0..3; 0 is the empty set: out = 0 and lse = -inf, the values
+ *              that make ispa_attn_merge return the other branch unchanged.
+ * q, k_cache, v_cache, n_q, n_heads, head_dim, scale, out, lse as for
+ * ispa_attn_chunk (single-stream form).
+ */
+int ispa_attn_ranges(const void* q, const void* k_cache, const void* v_cache,
+                     const int64_t* ranges, int32_t n_ranges,
+                     int32_t n_q, int32_t n_heads, int32_t head_dim, float scale,
+                     float* out, float* lse, hipStream_t stream);
+
+/*
+ * LSE fusion of two attention results over disjoint key sets (Sec. 3.4,
+ * Eq. 11-12):
+ *   lse = ln(e^lse_a + e^lse_b)  (evaluated as m + ln(e^(lse_a-m) + e^(lse_b-m)))
+ *   out = e^(lse_a - lse) out_a + e^(lse_b - lse) out_b
+ * Two empty branches (lse -inf) give out = 0, lse = -inf.
+ *   out_a, out_b, out   fp32 [n_q, n_heads * head_dim]; out may be out_a or out_b
+ *   lse_a, lse_b        fp32 [n_heads, n_q] (natural log)
+ *   lse                 fp32 [n_heads, n_q] or NULL; must not overlap lse_a/lse_b
+ *   head_dim            a positive multiple of 4
+ */
+int ispa_attn_merge(const float* out_a, const float* lse_a, const float* out_b, const float* lse_b,
+                    int32_t n_q, int32_t n_heads, int32_t head_dim,
+                    float* out, float* lse, hipStream_t stream);
+
 /* ---------------------------------------------------------- statistics */
 /*
  * Sufficient statistics of one layer's absorption problem (Sec. 3.2): the

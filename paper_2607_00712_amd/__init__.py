@@ -6,7 +6,9 @@ pointers plus the current HIP stream. There is no CPU fallback: importing
 works without the library, but every call raises if it is not built.
 
     attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0,
-               dual=False) -> (out, lse) or (out, lse, out_local, lse_local)
+               dual=False, segments=0) -> (out, lse) or (out, lse, out_local, lse_local)
+    attn_ranges(q, k_cache, v_cache, ranges, n_heads) -> (out, lse)
+    attn_merge(out_a, lse_a, out_b, lse_b) -> (out, lse)
     Stats(d_in, d_out, max_rows).accum(x, y_full, y_local)
     Stats.solve(lam) -> (delta_w, eps)
 """
@@ -16,7 +18,7 @@ import os
 
 import torch
 
-__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "Stats", "status_string",
+__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "status_string",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
            "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
 
@@ -39,6 +41,12 @@ _SIGNATURES = {
     "ispa_abi_version": (ctypes.c_int, []),
     "ispa_attn_chunk": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
                                        _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "ispa_attn_chunk_ws": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
+                                          _c_f32, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p, _c_sz, _c_p]),
+    "ispa_attn_workspace_bytes": (_c_sz, [_c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "ispa_attn_ranges": (ctypes.c_int, [_c_p, _c_p, _c_p, ctypes.POINTER(_c_i64), _c_i32, _c_i32, _c_i32, _c_i32,
+                                        _c_f32, _c_p, _c_p, _c_p]),
+    "ispa_attn_merge": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
     "ispa_stats_workspace_bytes": (_c_sz, [_c_i32, _c_i32, _c_i64]),
     "ispa_stats_create": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_p, _c_sz, _c_i32, _c_i32, _c_i64, _c_p]),
     "ispa_stats_reset": (ctypes.c_int, [_c_p]),
@@ -109,15 +117,19 @@ def _require(t, name, dtype, device=None, ndim=2):
         raise ValueError(f"{name} must be a contiguous {ndim}-d tensor")
 
 
-def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scale=0.0,
-               dual=False, out=None, lse=None, out_local=None, lse_local=None, need_lse=True):
-    """Chunk attention (see ispa_attn_chunk in include/ispa.h).
+_workspaces = {}
 
-    q [n_q, H*d] bf16; k_cache, v_cache [>= cache_len, H*d] bf16 on one device.
-    Returns (out, lse), or (out, lse, out_local, lse_local) when dual: out is then
-    the full-cache result and out_local the sink + window result.
-    """
-    L = lib()
+
+def _workspace(device, nbytes):
+    """A cached device workspace of at least nbytes (grown on demand)."""
+    ws = _workspaces.get(device)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(((nbytes + 255) // 256) * 256, dtype=torch.uint8, device=device)
+        _workspaces[device] = ws
+    return ws
+
+
+def _qkv(q, k_cache, v_cache, n_heads):
     _require(q, "q", torch.bfloat16)
     dev = q.device
     _require(k_cache, "k_cache", torch.bfloat16, dev)
@@ -125,9 +137,31 @@ def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scal
     n_q, hidden = q.shape
     if hidden % n_heads:
         raise ValueError("hidden size is not a multiple of n_heads")
-    head_dim = hidden // n_heads
     if k_cache.shape[1] != hidden or v_cache.shape[1] != hidden:
         raise ValueError("k/v hidden size differs from q")
+    return dev, n_q, hidden, hidden // n_heads
+
+
+def _outputs(dev, n_q, hidden, n_heads, pairs):
+    for name, t, shape in pairs:
+        if t is not None:
+            _require(t, name, torch.float32, dev)
+            if tuple(t.shape) != shape:
+                raise ValueError(f"{name} must have shape {shape}")
+
+
+def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scale=0.0,
+               dual=False, out=None, lse=None, out_local=None, lse_local=None, need_lse=True, segments=0):
+    """Chunk attention (see ispa_attn_chunk / ispa_attn_chunk_ws in include/ispa.h).
+
+    q [n_q, H*d] bf16; k_cache, v_cache [>= cache_len, H*d] bf16 on one device.
+    Returns (out, lse), or (out, lse, out_local, lse_local) when dual: out is then
+    the full-cache result and out_local the sink + window result. ``segments``:
+    0 splits the work over the chip when whole work items fill it poorly, < 0
+    never splits, > 0 forces that many runs (the workspace is cached per device).
+    """
+    L = lib()
+    dev, n_q, hidden, head_dim = _qkv(q, k_cache, v_cache, n_heads)
     if k_cache.shape[0] < cache_len or v_cache.shape[0] < cache_len:
         raise ValueError("cache tensors hold fewer than cache_len rows")
     if out is None:
@@ -139,17 +173,68 @@ def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scal
             out_local = torch.empty((n_q, hidden), dtype=torch.float32, device=dev)
         if lse_local is None and need_lse:
             lse_local = torch.empty((n_heads, n_q), dtype=torch.float32, device=dev)
-    for name, t, shape in (("out", out, (n_q, hidden)), ("out_local", out_local, (n_q, hidden)),
-                           ("lse", lse, (n_heads, n_q)), ("lse_local", lse_local, (n_heads, n_q))):
-        if t is not None:
-            _require(t, name, torch.float32, dev)
-            if tuple(t.shape) != shape:
-                raise ValueError(f"{name} must have shape {shape}")
-    st = L.ispa_attn_chunk(_ptr(q), _ptr(k_cache), _ptr(v_cache), int(cache_len), int(window), int(sink_len),
-                           int(n_q), int(n_heads), int(head_dim), float(scale), _ptr(out), _ptr(lse),
-                           _ptr(out_local if dual else None), _ptr(lse_local if dual else None), _stream(dev))
-    _check(st, "ispa_attn_chunk")
+    _outputs(dev, n_q, hidden, n_heads,
+             (("out", out, (n_q, hidden)), ("out_local", out_local, (n_q, hidden)),
+              ("lse", lse, (n_heads, n_q)), ("lse_local", lse_local, (n_heads, n_q))))
+    with torch.cuda.device(dev):
+        nbytes = L.ispa_attn_workspace_bytes(int(cache_len), int(window), int(sink_len), int(n_q), int(n_heads),
+                                             int(head_dim), int(bool(dual)), int(segments))
+    ws = _workspace(dev, nbytes) if nbytes > 0 else None
+    st = L.ispa_attn_chunk_ws(_ptr(q), _ptr(k_cache), _ptr(v_cache), int(cache_len), int(window), int(sink_len),
+                              int(n_q), int(n_heads), int(head_dim), float(scale), _ptr(out), _ptr(lse),
+                              _ptr(out_local if dual else None), _ptr(lse_local if dual else None),
+                              int(segments), _ptr(ws), int(ws.numel() if ws is not None else 0), _stream(dev))
+    _check(st, "ispa_attn_chunk_ws")
     return (out, lse, out_local, lse_local) if dual else (out, lse)
+
+
+def attn_ranges(q, k_cache, v_cache, ranges, n_heads, scale=0.0, out=None, lse=None):
+    """Attention over the union of key ranges [(begin, end), ...] (ispa_attn_ranges):
+    one branch of the decomposable form (an empty list gives out = 0, lse = -inf)."""
+    L = lib()
+    dev, n_q, hidden, head_dim = _qkv(q, k_cache, v_cache, n_heads)
+    ranges = [(int(b), int(e)) for b, e in ranges]
+    if len(ranges) > 3:
+        raise ValueError("at most 3 key ranges")
+    for b, e in ranges:
+        if not (0 <= b < e) or e > k_cache.shape[0] or e > v_cache.shape[0]:
+            raise ValueError(f"key range {(b, e)} is empty or outside the cache tensors")
+    if out is None:
+        out = torch.empty((n_q, hidden), dtype=torch.float32, device=dev)
+    if lse is None:
+        lse = torch.empty((n_heads, n_q), dtype=torch.float32, device=dev)
+    _outputs(dev, n_q, hidden, n_heads, (("out", out, (n_q, hidden)), ("lse", lse, (n_heads, n_q))))
+    arr = (_c_i64 * max(1, 2 * len(ranges)))(*[v for r in ranges for v in r])
+    st = L.ispa_attn_ranges(_ptr(q), _ptr(k_cache), _ptr(v_cache), arr, len(ranges), int(n_q), int(n_heads),
+                            int(head_dim), float(scale), _ptr(out), _ptr(lse), _stream(dev))
+    _check(st, "ispa_attn_ranges")
+    return out, lse
+
+
+def attn_merge(out_a, lse_a, out_b, lse_b, out=None, lse=None):
+    """Eq. 11-12 LSE fusion of two branches over disjoint key sets (ispa_attn_merge)."""
+    L = lib()
+    _require(out_a, "out_a", torch.float32)
+    dev = out_a.device
+    n_q, hidden = out_a.shape
+    _require(lse_a, "lse_a", torch.float32, dev)
+    n_heads = lse_a.shape[0]
+    if hidden % n_heads:
+        raise ValueError("hidden size is not a multiple of n_heads")
+    for name, t, shape in (("out_b", out_b, (n_q, hidden)), ("lse_a", lse_a, (n_heads, n_q)),
+                           ("lse_b", lse_b, (n_heads, n_q))):
+        _require(t, name, torch.float32, dev)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must have shape {shape}")
+    if out is None:
+        out = torch.empty((n_q, hidden), dtype=torch.float32, device=dev)
+    if lse is None:
+        lse = torch.empty((n_heads, n_q), dtype=torch.float32, device=dev)
+    _outputs(dev, n_q, hidden, n_heads, (("out", out, (n_q, hidden)), ("lse", lse, (n_heads, n_q))))
+    st = L.ispa_attn_merge(_ptr(out_a), _ptr(lse_a), _ptr(out_b), _ptr(lse_b), int(n_q), int(n_heads),
+                           int(hidden // n_heads), _ptr(out), _ptr(lse), _stream(dev))
+    _check(st, "ispa_attn_merge")
+    return out, lse
 
 
 _DT = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}

@@ -57,9 +57,11 @@ constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBqWave = 32;
 constexpr int kBq = kWaves * kBqWave;  // queries per workgroup
+static_assert(kBq == kAttnBq, "work item size");
 constexpr int kBk = 64;                // keys per tile
 constexpr int kXcds = 8;
 constexpr float kLazyLog2 = 8.f;       // rescale threshold of the softmax reference
+constexpr int kSplitMinTiles = 384;    // automatic split only from this many key tiles per item
 
 template <int D>
 struct Cfg {
@@ -268,7 +270,8 @@ struct Wave {
   f32x16 acc[C::dBlocks];      // O^T, one 32 x 32 block per 32 head dims
   float m_run;                 // softmax reference (raw score units) of this lane's query
   float lazy;                  // kLazyLog2 in raw score units
-  float l_run;                 // running sum of p (this lane's half of the keys)
+  float l_run;                 // running sum of p (this lane's half of the keys), for the LSE
+  float lr_run;                // running sum of the bf16-rounded p, the normaliser of O
   bf16x8 qf[C::kSlices];       // Q^T operand
   u32x4 kr[C::kSlices];        // K operands of the current half
   uint32_t koff[C::kSlices];   // K operand LDS addresses (buffer 0, half 0)
@@ -282,28 +285,39 @@ struct Loop {
   bool dual;
 };
 
+// Writes the normalised output and LSE of this lane's query, either to the
+// launch's output rows (slot < 0) or to partial slot `slot` (part `which`:
+// 0 end state, 1 local set) of the split.
 template <int D>
-__device__ __forceinline__ void finish(const AttnArgs& a, Wave<D>& w, const Loop& L, int qrow, int head,
-                                       float* out, float* lse) {
+__device__ __forceinline__ void write_state(const AttnArgs& a, Wave<D>& w, const Loop& L, int qloc, int qrow,
+                                            int head, float* out, float* lse, int slot, int which) {
   using C = Cfg<D>;
   const float l_tot = l_run_total(w.l_run);
-  const float inv = 1.0f / l_tot;
-  if (qrow < a.n_q) {
-    float* op = out + (int64_t)qrow * a.ld + L.hoff + 4 * L.hh;
-#pragma unroll
-    for (int db = 0; db < C::dBlocks; ++db) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 o;
-        o[0] = w.acc[db][4 * i + 0] * inv;
-        o[1] = w.acc[db][4 * i + 1] * inv;
-        o[2] = w.acc[db][4 * i + 2] * inv;
-        o[3] = w.acc[db][4 * i + 3] * inv;
-        *(f32x4*)(op + 32 * db + 8 * i) = o;
-      }
-    }
-    if (lse != nullptr && L.hh == 0) lse[(int64_t)head * a.n_q + qrow] = w.m_run * a.scale + logf(l_tot);
+  const float inv = 1.0f / l_run_total(w.lr_run);
+  if (qrow >= a.n_q) return;
+  float* op;
+  float* lp;
+  if (slot < 0) {
+    op = out + (int64_t)qrow * a.ld + L.hoff + 4 * L.hh;
+    lp = lse != nullptr ? lse + (int64_t)head * a.n_q + qrow : nullptr;
+  } else {
+    const int64_t base = ((int64_t)slot * 2 + which) * kBq;
+    op = a.split.part_o + (base + qloc) * D + 4 * L.hh;
+    lp = a.split.part_lse + base + qloc;
   }
+#pragma unroll
+  for (int db = 0; db < C::dBlocks; ++db) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f32x4 o;
+      o[0] = w.acc[db][4 * i + 0] * inv;
+      o[1] = w.acc[db][4 * i + 1] * inv;
+      o[2] = w.acc[db][4 * i + 2] * inv;
+      o[3] = w.acc[db][4 * i + 3] * inv;
+      *(f32x4*)(op + 32 * db + 8 * i) = o;
+    }
+  }
+  if (lp != nullptr && L.hh == 0) *lp = w.m_run * a.scale + logf(l_tot);
 }
 
 // One 32-key online-softmax step: keys 32B .. 32B+31 of the tile in LDS buffer BUF.
@@ -323,11 +337,13 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
   tr_issue<C::dBlocks, vBase + 16 * (2 * B + 1) * C::rowBytes>(w.vaddr, v1);
   // keys past the end of a range (only in the last tile of each range)
   if (nv < 32 * (B + 1)) {
+    // register r holds key 32B + 4 hh + 8 (r / 4) + r % 4 of the tile (compared
+    // as a compile-time offset against one limit, so that no per-register key
+    // indices stay live across the loop)
+    const int lim = nv - 32 * B - 4 * L.hh;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = 32 * B + 8 * (r >> 2) + 4 * L.hh + (r & 3);
-      if (key >= nv) sc[r] = -INFINITY;
-    }
+    for (int r = 0; r < 16; ++r)
+      if (8 * (r >> 2) + (r & 3) >= lim) sc[r] = -INFINITY;
   }
   float tmax = max3(sc[0], sc[1], sc[2]);
 #pragma unroll
@@ -342,6 +358,7 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
     const float m_new = fmaxf(w.m_run, tmax);
     const float alpha = exp2_hw((w.m_run - m_new) * a.scale_log2);
     w.l_run *= alpha;
+    w.lr_run *= alpha;
 #pragma unroll
     for (int db = 0; db < C::dBlocks; ++db) w.acc[db] *= alpha;
     w.m_run = m_new;
@@ -362,6 +379,20 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
     pf0[e] = (__bf16)sc[e];
     pf1[e] = (__bf16)sc[8 + e];
   }
+  // O is normalised by the sum of the weights the P V MFMAs actually apply, so
+  // the bf16 rounding of a dominant weight cancels in the quotient
+  {
+    const bf16x2 one2 = {(__bf16)1.f, (__bf16)1.f};
+    float r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf0, pf0, 0, 1), one2, w.lr_run, false);
+    float r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf0, pf0, 2, 3), one2, 0.f, false);
+    r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf0, pf0, 4, 5), one2, r0, false);
+    r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf0, pf0, 6, 7), one2, r1, false);
+    r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf1, pf1, 0, 1), one2, r0, false);
+    r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf1, pf1, 2, 3), one2, r1, false);
+    r0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf1, pf1, 4, 5), one2, r0, false);
+    r1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf1, pf1, 6, 7), one2, r1, false);
+    w.lr_run = r0 + r1;
+  }
   // O^T += V^T . P^T over the two slices
   bf16x8 vf[C::dBlocks];
   tr_wait<2 * C::dBlocks, C::dBlocks>(v0, vf);
@@ -379,16 +410,17 @@ __device__ __forceinline__ void half_step(const AttnArgs& a, Wave<D>& w, const L
   for (int db = 0; db < C::dBlocks; ++db) w.acc[db] = mfma32(vf[db], pf1, w.acc[db]);
 }
 
-// One 64-key tile (nv valid keys) from LDS buffer BUF; the next tile's direct
-// loads into the other buffer are issued while the first K operands are in
-// flight. Returns the next tile's number of valid keys.
+// One 64-key tile (nv valid keys) from LDS buffer BUF; the next tile of the
+// piece (ending at t_end) is loaded into the other buffer while the first K
+// operands are in flight. Returns the next tile's number of valid keys.
 template <int D, int BUF>
-__device__ __forceinline__ int tile_step(const AttnArgs& a, Wave<D>& w, const Loop& L, char* smem, int t, int nv) {
+__device__ __forceinline__ int tile_step(const AttnArgs& a, Wave<D>& w, const Loop& L, char* smem, int t, int nv,
+                                         int t_end) {
   using C = Cfg<D>;
   // half 0's K operands: the tile became visible at the last barrier
   k_issue<C::kSlices, BUF * 2 * C::tileBytes>(w.koff, w.kr, 0.f);
   int n1 = 0;
-  if (t + 1 < L.n_tiles) {
+  if (t + 1 < t_end) {
     int64_t k1;
     tile_of(L.map, t + 1, k1, n1);
     stage_tile<D>(a, k1 * a.ld + L.hoff, n1, smem + (BUF ^ 1) * 2 * C::tileBytes, w.voffk, w.voffv, L.wave);
@@ -402,39 +434,80 @@ __device__ __forceinline__ int tile_step(const AttnArgs& a, Wave<D>& w, const Lo
   return n1;
 }
 
+// Segment arithmetic of the split (shared by the attention and merge kernels).
+__device__ __forceinline__ int64_t seg_begin(const AttnSplit& s, int g) { return (int64_t)g * s.units / s.n_seg; }
+// segment that holds unit u: the largest g with seg_begin(g) <= u
+__device__ __forceinline__ int seg_of(const AttnSplit& s, int64_t u) {
+  return (int)(((u + 1) * s.n_seg - 1) / s.units);
+}
+
+// One piece: tiles [ta, tb) of work item `item` with a fresh softmax state.
+// Whatever the piece completes (all tiles, or all local tiles from tile 0) is
+// written to the outputs; the rest goes to partial slot `slot`.
+template <int D>
+__device__ __forceinline__ void run_piece(const AttnArgs& a, Wave<D>& w, Loop& L, char* smem, int q_tiles, int item,
+                                          int ta, int tb, int slot, int ql) {
+  using C = Cfg<D>;
+  const int head = item / q_tiles;
+  const int qtile = item - head * q_tiles;
+  L.hoff = head * D;
+  const int qloc = L.wave * kBqWave + ql;
+  const int qrow = qtile * kBq + qloc;
+  // ---- Q^T operand, resident for the piece -----------------------------------
+  {
+    const uint16_t* qp = a.q + (int64_t)qrow * a.ld + L.hoff + 8 * L.hh;
+#pragma unroll
+    for (int kk = 0; kk < C::kSlices; ++kk) w.qf[kk] = qrow < a.n_q ? *(const bf16x8*)(qp + 16 * kk) : bf16x8{};
+  }
+#pragma unroll
+  for (int i = 0; i < C::dBlocks; ++i) w.acc[i] = f32x16{};
+  w.m_run = -INFINITY;
+  w.l_run = 0.f;
+  w.lr_run = 0.f;
+
+  int nv;  // valid keys of the tile in the current buffer
+  {
+    int64_t k0;
+    tile_of(L.map, ta, k0, nv);
+    stage_tile<D>(a, k0 * a.ld + L.hoff, nv, smem, w.voffk, w.voffv, L.wave);
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
+  __syncthreads();
+
+  const int Lt = L.n_tiles_local;
+  for (int t = ta; t < tb; t += 2) {
+    // local set complete after tile Lt - 1 (a piece that started at tile 0 owns it)
+    if (L.dual && t == Lt && t > ta)
+      write_state<D>(a, w, L, qloc, qrow, head, a.out_local, a.lse_local, ta == 0 ? -1 : slot, 1);
+    nv = tile_step<D, 0>(a, w, L, smem, t, nv, tb);
+    if (t + 1 < tb) {
+      if (L.dual && t + 1 == Lt)
+        write_state<D>(a, w, L, qloc, qrow, head, a.out_local, a.lse_local, ta == 0 ? -1 : slot, 1);
+      nv = tile_step<D, 1>(a, w, L, smem, t + 1, nv, tb);
+    }
+  }
+  const bool whole = ta == 0 && tb == L.n_tiles;
+  write_state<D>(a, w, L, qloc, qrow, head, a.out, a.lse, whole ? -1 : slot, 0);
+  // a piece ending inside (or at the end of) the local set also holds its
+  // local contribution
+  if (L.dual && tb <= Lt)
+    write_state<D>(a, w, L, qloc, qrow, head, a.out_local, a.lse_local, (ta == 0 && tb == Lt) ? -1 : slot, 1);
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_kernel(AttnArgs a,
                                                                                                   int q_tiles) {
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * C::tileBytes];  // [buf][K|V]
 
-  // ---- XCD-aware work mapping ------------------------------------------
-  const int n_work = q_tiles * a.n_heads;
-  const int per_xcd = (n_work + kXcds - 1) / kXcds;
-  const int bid = blockIdx.x;
-  const int work = (bid % kXcds) * per_xcd + bid / kXcds;
-  if (work >= n_work) return;  // padding blocks (uniform exit, before any barrier)
-  const int head = work / q_tiles;
-  const int qtile = work % q_tiles;
-
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   Loop L;
   L.wave = tid >> 6;
   L.hh = lane >> 5;  // lane half
-  L.hoff = head * D;
   const int ql = lane & 31;  // this lane's query within the wave
-  const int qrow = qtile * kBq + L.wave * kBqWave + ql;
 
-  Wave<D> w;
-  // ---- Q^T operand, resident for the whole key loop ------------------------
-  {
-    const uint16_t* qp = a.q + (int64_t)qrow * a.ld + L.hoff + 8 * L.hh;
-#pragma unroll
-    for (int kk = 0; kk < C::kSlices; ++kk) w.qf[kk] = qrow < a.n_q ? *(const bf16x8*)(qp + 16 * kk) : bf16x8{};
-  }
-
-  // ---- tile enumeration -------------------------------------------------------
+  // ---- tile enumeration (the same for every work item) --------------------------
   const int nt0 = (int)((a.r.end[0] - a.r.begin[0] + kBk - 1) / kBk);
   const int nt1 = a.r.n_total > 1 ? (int)((a.r.end[1] - a.r.begin[1] + kBk - 1) / kBk) : 0;
   const int nt2 = a.r.n_total > 2 ? (int)((a.r.end[2] - a.r.begin[2] + kBk - 1) / kBk) : 0;
@@ -449,7 +522,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   L.n_tiles = nt0 + nt1 + nt2;
   L.n_tiles_local = a.r.n_local == 1 ? nt0 : nt0 + nt1;
   L.dual = a.out_local != nullptr;
+  const int T = L.n_tiles;
+  if (T <= 0) return;  // (an empty key set is handled on the host)
 
+  // ---- XCD-aware mapping of workgroups to work items or segments ------------------
+  // The 8 XCDs take workgroups round-robin; consecutive logical indices (the
+  // tiles of one head) stay on one XCD and share its L2.
+  const int n_work = q_tiles * a.n_heads;
+  const int n_log = a.split.n_seg > 0 ? a.split.n_seg : n_work;
+  const int per_xcd = (int)(gridDim.x / kXcds);
+  const int bid = blockIdx.x;
+  const int g = (bid % kXcds) * per_xcd + bid / kXcds;
+  if (g >= n_log) return;  // padding blocks (uniform exit, before any barrier)
+  int64_t u0, u1;
+  if (a.split.n_seg > 0) {
+    u0 = seg_begin(a.split, g);
+    u1 = seg_begin(a.split, g + 1);
+  } else {
+    u0 = (int64_t)g * T;
+    u1 = u0 + T;
+  }
+
+  Wave<D> w;
   // ---- per-lane constants ---------------------------------------------------------
   // Direct load q of this thread covers 16-byte slot (q * kWaves + wave) * 64 + lane
   // of a tile: row = slot / chunksPerRow, stored chunk = slot % chunksPerRow,
@@ -465,57 +559,210 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const uint32_t lds0 = lds_addr(smem);
 #pragma unroll
     for (int kk = 0; kk < C::kSlices; ++kk) w.koff[kk] = lds0 + chunk_off<D>(ql, 2 * kk + L.hh, swz_k<D>(ql));
-    const int g = lane >> 4, sl = lane & 15;
+    const int gq = lane >> 4, sl = lane & 15;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
       for (int db = 0; db < C::dBlocks; ++db) {
-        const int row = 8 * h2 + 4 * (g >> 1) + (sl >> 2);
-        const int chunk = 4 * db + 2 * (g & 1) + ((sl & 3) >> 1);
+        const int row = 8 * h2 + 4 * (gq >> 1) + (sl >> 2);
+        const int chunk = 4 * db + 2 * (gq & 1) + ((sl & 3) >> 1);
         w.vaddr[h2][db] = lds0 + chunk_off<D>(row, chunk, swz_v<D>(row)) + ((sl & 1) << 3);
       }
   }
-
-  // ---- online softmax state ------------------------------------------------------
-#pragma unroll
-  for (int i = 0; i < C::dBlocks; ++i) w.acc[i] = f32x16{};
-  w.m_run = -INFINITY;
-  w.l_run = 0.f;
   w.lazy = kLazyLog2 / a.scale_log2;
 
-  int nv = 0;  // valid keys of the tile in the current buffer
-  if (L.n_tiles > 0) {
-    int64_t k0;
-    tile_of(L.map, 0, k0, nv);
-    stage_tile<D>(a, k0 * a.ld + L.hoff, nv, smem, w.voffk, w.voffv, L.wave);
+  // ---- the pieces of this workgroup's unit range, last one first -------------------
+  // The last piece starts at tile 0 of its item and the first one ends at the
+  // item's last tile, so with this order every segment of a head visits the
+  // same tile offset at the same time (from the start, then from the end of
+  // the item): the workgroups of one head keep sharing K/V through L2.
+  const int i_first = (int)(u0 / T), i_last = (int)((u1 - 1) / T);
+  for (int item = i_last; item >= i_first; --item) {
+    const int64_t ibase = (int64_t)item * T;
+    const int ta = (int)((u0 > ibase ? u0 : ibase) - ibase);
+    const int tb = (int)((u1 < ibase + T ? u1 : ibase + T) - ibase);
+    run_piece<D>(a, w, L, smem, q_tiles, item, ta, tb,
+                 a.split.n_seg > 0 ? g * a.split.max_pieces + (item - i_first) : -1, ql);
   }
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
-  __syncthreads();
+}
 
-  for (int t = 0; t < L.n_tiles; t += 2) {
-    if (L.dual && t == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
-    nv = tile_step<D, 0>(a, w, L, smem, t, nv);
-    if (t + 1 < L.n_tiles) {
-      if (L.dual && t + 1 == L.n_tiles_local) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
-      nv = tile_step<D, 1>(a, w, L, smem, t + 1, nv);
+// Eq. 11-12 over the pieces of each split work item: for every query row,
+// LSE = m + ln sum_p e^(LSE_p - m) and O = sum_p e^(LSE_p - LSE) O_p, for the
+// full result (all pieces) and the local result (pieces that start in the local
+// set). Items or sets covered by one piece were written by that piece.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_split_kernel(AttnArgs a, int q_tiles, int n_tiles,
+                                                               int n_tiles_local) {
+  constexpr int kVec = D / 4;            // float4 per row
+  constexpr int kRows = 256 / kVec;      // rows per block
+  const AttnSplit& s = a.split;
+  const int item = blockIdx.x;
+  const int r = threadIdx.x / kVec, c = threadIdx.x % kVec;
+  const int qloc = blockIdx.y * kRows + r;
+  const int head = item / q_tiles;
+  const int qrow = (item - head * q_tiles) * kBq + qloc;
+  if (qrow >= a.n_q) return;
+  const int64_t i0 = (int64_t)item * n_tiles;
+  const int g_lo = seg_of(s, i0);
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    if (which == 1 && a.out_local == nullptr) break;
+    const int g_hi = seg_of(s, i0 + (which == 0 ? n_tiles : n_tiles_local) - 1);
+    if (g_hi == g_lo) continue;
+    float m = -INFINITY;
+    for (int gg = g_lo; gg <= g_hi; ++gg) {
+      const int slot = gg * s.max_pieces + (item - (int)(seg_begin(s, gg) / n_tiles));
+      m = fmaxf(m, s.part_lse[((int64_t)slot * 2 + which) * kBq + qloc]);
     }
+    float sum = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    for (int gg = g_lo; gg <= g_hi; ++gg) {
+      const int slot = gg * s.max_pieces + (item - (int)(seg_begin(s, gg) / n_tiles));
+      const int64_t base = ((int64_t)slot * 2 + which) * kBq + qloc;
+      const float e = expf(s.part_lse[base] - m);
+      const f32x4 v = *(const f32x4*)(s.part_o + base * D + 4 * c);
+      sum += e;
+      o += e * v;
+    }
+    const float inv = 1.f / sum;
+    float* out = which == 0 ? a.out : a.out_local;
+    float* lse = which == 0 ? a.lse : a.lse_local;
+    *(f32x4*)(out + (int64_t)qrow * a.ld + (int64_t)head * D + 4 * c) = o * inv;
+    if (lse != nullptr && c == 0) lse[(int64_t)head * a.n_q + qrow] = m + logf(sum);
   }
-  if (L.dual && L.n_tiles_local == L.n_tiles) finish<D>(a, w, L, qrow, head, a.out_local, a.lse_local);
-  finish<D>(a, w, L, qrow, head, a.out, a.lse);
+}
+
+// Attention over an empty key set: O = 0, LSE = -inf (the convention that
+// makes Eq. 11-12 return the other branch unchanged).
+__global__ void attn_empty_kernel(float* out, float* lse, int64_t n_out, int64_t n_lse) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_out; i += (int64_t)gridDim.x * blockDim.x) {
+    out[i] = 0.f;
+    if (lse != nullptr && i < n_lse) lse[i] = -INFINITY;
+  }
+}
+
+// Eq. 11-12 for two results over disjoint key sets, evaluated as
+// m + ln(e^(a - m) + e^(b - m)); both empty gives O = 0, LSE = -inf.
+__global__ void attn_merge2_kernel(const float* o_a, const float* lse_a, const float* o_b, const float* lse_b,
+                                   int64_t n_q, int64_t n_heads, int head_dim, float* out, float* lse) {
+  const int64_t hidden = n_heads * head_dim;
+  const int64_t n4 = n_q * hidden / 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t e = 4 * i;
+    const int64_t row = e / hidden;
+    const int64_t h = (e - row * hidden) / head_dim;
+    const float la = lse_a[h * n_q + row], lb = lse_b[h * n_q + row];
+    const float m = fmaxf(la, lb);
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    float l = -INFINITY;
+    if (m != -INFINITY) {
+      const float ea = expf(la - m), eb = expf(lb - m);
+      l = m + logf(ea + eb);
+      const float wa = expf(la - l), wb = expf(lb - l);
+      const f32x4 va = *(const f32x4*)(o_a + e), vb = *(const f32x4*)(o_b + e);
+      o = wa * va + wb * vb;
+    }
+    *(f32x4*)(out + e) = o;
+    if (lse != nullptr && e % head_dim == 0) lse[h * n_q + row] = l;
+  }
 }
 
 }  // namespace
 
+int attn_tiles(const AttnRanges& r, int* n_tiles_local) {
+  int nt[3] = {0, 0, 0};
+  for (int i = 0; i < r.n_total; ++i) nt[i] = (int)((r.end[i] - r.begin[i] + kBk - 1) / kBk);
+  if (n_tiles_local) *n_tiles_local = r.n_local == 1 ? nt[0] : nt[0] + nt[1];
+  return nt[0] + nt[1] + nt[2];
+}
+
+int attn_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  static int cache[64];
+  if (dev >= 0 && dev < 64 && cache[dev] > 0) return cache[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (dev >= 0 && dev < 64) cache[dev] = n;
+  return n;
+}
+
+size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit* s) {
+  s->units = 0;
+  s->n_seg = 0;
+  s->max_pieces = 0;
+  s->part_o = nullptr;
+  s->part_lse = nullptr;
+  const int T = attn_tiles(a.r, nullptr);
+  const int64_t n_work = (int64_t)((a.n_q + kBq - 1) / kBq) * a.n_heads;
+  if (segments < 0 || T <= 0) return 0;
+  const int64_t U = n_work * T;
+  int64_t G;
+  if (segments > 0) {
+    G = segments;
+  } else {
+    // whole work items per workgroup leave a fraction of the last round of
+    // workgroups idle; split only when that fraction is large and the launch
+    // is long enough to repay the partial results' traffic and the merge
+    // (measured at about 40-60 us per launch on 256 CUs)
+    const int n_cu = attn_cu_count();
+    if (n_cu <= 0 || T < kSplitMinTiles) return 0;
+    const int64_t rounds = (n_work + n_cu - 1) / n_cu;
+    if (n_work * 100 >= rounds * n_cu * 92) return 0;
+    G = n_cu;
+    if (U / G < 16) G = U / 16;
+    if (G < 2) return 0;
+  }
+  if (G > U) G = U;
+  if (G > (1 << 20)) G = 1 << 20;
+  const int64_t seg_max = (U + G - 1) / G;
+  s->units = U;
+  s->n_seg = (int32_t)G;
+  s->max_pieces = (int32_t)((seg_max + T - 1) / T + 1);
+  const size_t slots = (size_t)G * s->max_pieces * 2 * kBq;
+  const size_t o_bytes = (slots * head_dim * 4 + 255) / 256 * 256;
+  return o_bytes + slots * 4;
+}
+
 hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream) {
   const int q_tiles = (a.n_q + kBq - 1) / kBq;
   const int n_work = q_tiles * a.n_heads;
-  const int per_xcd = (n_work + kXcds - 1) / kXcds;
+  const int n_log = a.split.n_seg > 0 ? a.split.n_seg : n_work;
+  const int per_xcd = (n_log + kXcds - 1) / kXcds;
   const int grid = per_xcd * kXcds;
   if (head_dim == 128) {
     hipLaunchKernelGGL(attn_chunk_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
   } else {
     hipLaunchKernelGGL(attn_chunk_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.split.n_seg == 0) return e;
+  int n_local = 0;
+  const int T = attn_tiles(a.r, &n_local);
+  const dim3 mgrid(n_work, head_dim == 128 ? kBq / 8 : kBq / 16);
+  if (head_dim == 128) {
+    hipLaunchKernelGGL(attn_merge_split_kernel<128>, mgrid, dim3(256), 0, stream, a, q_tiles, T, n_local);
+  } else {
+    hipLaunchKernelGGL(attn_merge_split_kernel<64>, mgrid, dim3(256), 0, stream, a, q_tiles, T, n_local);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_empty(float* out, float* lse, int64_t n_q, int64_t n_heads, int head_dim,
+                             hipStream_t stream) {
+  const int64_t n_out = n_q * n_heads * head_dim;
+  const int blocks = (int)((n_out + 255) / 256 < 4096 ? (n_out + 255) / 256 : 4096);
+  hipLaunchKernelGGL(attn_empty_kernel, dim3(blocks), dim3(256), 0, stream, out, lse, n_out, n_q * n_heads);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_merge2(const float* o_a, const float* lse_a, const float* o_b, const float* lse_b,
+                              int64_t n_q, int64_t n_heads, int head_dim, float* out, float* lse,
+                              hipStream_t stream) {
+  const int64_t n4 = n_q * n_heads * head_dim / 4;
+  const int blocks = (int)((n4 + 255) / 256 < 8192 ? (n4 + 255) / 256 : 8192);
+  hipLaunchKernelGGL(attn_merge2_kernel, dim3(blocks), dim3(256), 0, stream, o_a, lse_a, o_b, lse_b, n_q, n_heads,
+                     head_dim, out, lse);
   return hipGetLastError();
 }
 

@@ -76,58 +76,148 @@ const char* ispa_status_string(int status) {
   }
 }
 
-int ispa_abi_version(void) { return 100; }
+int ispa_abi_version(void) { return 101; }
+
+}  // extern "C"
+
+namespace {
+
+// Validates the arguments shared by the attention calls and fills the
+// launch-independent part of AttnArgs.
+int attn_common(const void* q, const void* k_cache, const void* v_cache, int32_t n_q, int32_t n_heads,
+                int32_t head_dim, float scale, float* out, float* lse, ispa::AttnArgs* a) {
+  if (head_dim != 64 && head_dim != 128) return ISPA_ERR_UNSUPPORTED;
+  if (!q || !k_cache || !v_cache || !out) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return ISPA_ERR_INVALID_ARG;
+  if ((uintptr_t)lse & 3u) return ISPA_ERR_INVALID_ARG;
+  if (n_q < 1 || n_heads < 1 || n_heads > 65535) return ISPA_ERR_INVALID_ARG;
+  if (!(scale == scale) || isinf(scale)) return ISPA_ERR_INVALID_ARG;
+  if ((int64_t)n_heads * head_dim > ((int64_t)1 << 20)) return ISPA_ERR_INVALID_ARG;
+  const float s = scale > 0.f ? scale : 1.0f / sqrtf((float)head_dim);
+  memset(a, 0, sizeof(*a));
+  a->q = (const uint16_t*)q;
+  a->k = (const uint16_t*)k_cache;
+  a->v = (const uint16_t*)v_cache;
+  a->out = out;
+  a->lse = lse;
+  a->ld = (int64_t)n_heads * head_dim;
+  a->n_q = n_q;
+  a->n_heads = n_heads;
+  a->scale = s;
+  a->scale_log2 = s * 1.4426950408889634f;
+  return ISPA_OK;
+}
+
+// Key sets of Sec. 3.4, Eq. 7-8: local = [0, s') U [lo, N), hist = [s', lo).
+int chunk_ranges(int64_t cache_len, int64_t window, int64_t sink_len, int32_t n_q, bool dual, ispa::AttnRanges* r) {
+  if (cache_len < n_q || cache_len > ((int64_t)1 << 31)) return ISPA_ERR_INVALID_ARG;
+  if (window < 1 || sink_len < 0) return ISPA_ERR_INVALID_ARG;
+  const int64_t N = cache_len;
+  const int64_t s1 = sink_len < N ? sink_len : N;
+  const int64_t lo = N - window > 0 ? N - window : 0;
+  if (lo <= s1) {
+    r->begin[0] = 0; r->end[0] = N;
+    r->n_local = 1;
+    r->n_total = 1;
+  } else {
+    int i = 0;
+    if (s1 > 0) { r->begin[i] = 0; r->end[i] = s1; ++i; }
+    r->begin[i] = lo; r->end[i] = N; ++i;
+    r->n_local = i;
+    r->n_total = i;
+    if (dual) { r->begin[i] = s1; r->end[i] = lo; ++i; r->n_total = i; }
+  }
+  for (int i = r->n_total; i < 3; ++i) { r->begin[i] = 0; r->end[i] = 0; }
+  return ISPA_OK;
+}
+
+}  // namespace
+
+extern "C" {
 
 int ispa_attn_chunk(const void* q, const void* k_cache, const void* v_cache, int64_t cache_len,
                     int64_t window, int64_t sink_len, int32_t n_q, int32_t n_heads, int32_t head_dim,
                     float scale, float* out, float* lse, float* out_local, float* lse_local,
                     hipStream_t stream) {
-  if (head_dim != 64 && head_dim != 128) return ISPA_ERR_UNSUPPORTED;
-  if (!q || !k_cache || !v_cache || !out) return ISPA_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return ISPA_ERR_INVALID_ARG;
-  if (out_local && !aligned16(out_local)) return ISPA_ERR_INVALID_ARG;
-  if (((uintptr_t)lse & 3u) || ((uintptr_t)lse_local & 3u)) return ISPA_ERR_INVALID_ARG;
-  if (lse_local && !out_local) return ISPA_ERR_INVALID_ARG;
-  if (n_q < 1 || n_heads < 1 || n_heads > 65535) return ISPA_ERR_INVALID_ARG;
-  if (cache_len < n_q || cache_len > ((int64_t)1 << 31)) return ISPA_ERR_INVALID_ARG;
-  if (window < 1 || sink_len < 0) return ISPA_ERR_INVALID_ARG;
-  if (!(scale == scale) || isinf(scale)) return ISPA_ERR_INVALID_ARG;
-  if ((int64_t)n_heads * head_dim > ((int64_t)1 << 20)) return ISPA_ERR_INVALID_ARG;
+  return ispa_attn_chunk_ws(q, k_cache, v_cache, cache_len, window, sink_len, n_q, n_heads, head_dim, scale,
+                            out, lse, out_local, lse_local, -1, nullptr, 0, stream);
+}
 
-  const float s = scale > 0.f ? scale : 1.0f / sqrtf((float)head_dim);
+size_t ispa_attn_workspace_bytes(int64_t cache_len, int64_t window, int64_t sink_len, int32_t n_q,
+                                 int32_t n_heads, int32_t head_dim, int32_t dual, int32_t segments) {
+  if (head_dim != 64 && head_dim != 128) return 0;
+  if (n_q < 1 || n_heads < 1 || n_heads > 65535) return 0;
   ispa::AttnArgs a;
-  a.q = (const uint16_t*)q;
-  a.k = (const uint16_t*)k_cache;
-  a.v = (const uint16_t*)v_cache;
-  a.out = out;
-  a.lse = lse;
-  a.out_local = out_local;
-  a.lse_local = lse_local;
-  a.ld = (int64_t)n_heads * head_dim;
+  memset(&a, 0, sizeof(a));
   a.n_q = n_q;
   a.n_heads = n_heads;
-  a.scale = s;
-  a.scale_log2 = s * 1.4426950408889634f;
+  if (chunk_ranges(cache_len, window, sink_len, n_q, dual != 0, &a.r) != ISPA_OK) return 0;
+  ispa::AttnSplit sp;
+  return ispa::attn_plan_split(a, head_dim, segments, &sp);
+}
 
-  // Key sets of Sec. 3.4, Eq. 7-8: local = [0, s') U [lo, N), hist = [s', lo).
-  const int64_t N = cache_len;
-  const int64_t s1 = sink_len < N ? sink_len : N;
-  const int64_t lo = N - window > 0 ? N - window : 0;
-  ispa::AttnRanges& r = a.r;
-  if (lo <= s1) {
-    r.begin[0] = 0; r.end[0] = N;
-    r.n_local = 1;
-    r.n_total = 1;
-  } else {
-    int i = 0;
-    if (s1 > 0) { r.begin[i] = 0; r.end[i] = s1; ++i; }
-    r.begin[i] = lo; r.end[i] = N; ++i;
-    r.n_local = i;
-    r.n_total = i;
-    if (out_local) { r.begin[i] = s1; r.end[i] = lo; ++i; r.n_total = i; }
+int ispa_attn_chunk_ws(const void* q, const void* k_cache, const void* v_cache, int64_t cache_len,
+                       int64_t window, int64_t sink_len, int32_t n_q, int32_t n_heads, int32_t head_dim,
+                       float scale, float* out, float* lse, float* out_local, float* lse_local,
+                       int32_t segments, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  ispa::AttnArgs a;
+  int st = attn_common(q, k_cache, v_cache, n_q, n_heads, head_dim, scale, out, lse, &a);
+  if (st != ISPA_OK) return st;
+  if (out_local && !aligned16(out_local)) return ISPA_ERR_INVALID_ARG;
+  if ((uintptr_t)lse_local & 3u) return ISPA_ERR_INVALID_ARG;
+  if (lse_local && !out_local) return ISPA_ERR_INVALID_ARG;
+  st = chunk_ranges(cache_len, window, sink_len, n_q, out_local != nullptr, &a.r);
+  if (st != ISPA_OK) return st;
+  a.out_local = out_local;
+  a.lse_local = lse_local;
+  const size_t need = ispa::attn_plan_split(a, head_dim, segments, &a.split);
+  if (a.split.n_seg > 0) {
+    if (!workspace || ((uintptr_t)workspace & 255u) || workspace_bytes < need) return ISPA_ERR_INVALID_ARG;
+    const size_t slots = (size_t)a.split.n_seg * a.split.max_pieces * 2 * ispa::kAttnBq;
+    a.split.part_o = (float*)workspace;
+    a.split.part_lse = (float*)((char*)workspace + round_up(slots * head_dim * 4, 256));
   }
-  for (int i = r.n_total; i < 3; ++i) { r.begin[i] = 0; r.end[i] = 0; }
   return ispa::launch_attn_chunk(a, head_dim, stream) == hipSuccess ? ISPA_OK : ISPA_ERR_HIP;
+}
+
+int ispa_attn_ranges(const void* q, const void* k_cache, const void* v_cache, const int64_t* ranges,
+                     int32_t n_ranges, int32_t n_q, int32_t n_heads, int32_t head_dim, float scale, float* out,
+                     float* lse, hipStream_t stream) {
+  ispa::AttnArgs a;
+  int st = attn_common(q, k_cache, v_cache, n_q, n_heads, head_dim, scale, out, lse, &a);
+  if (st != ISPA_OK) return st;
+  if (n_ranges < 0 || n_ranges > 3 || (n_ranges > 0 && !ranges)) return ISPA_ERR_INVALID_ARG;
+  for (int i = 0; i < n_ranges; ++i) {
+    const int64_t b = ranges[2 * i], e = ranges[2 * i + 1];
+    if (b < 0 || e <= b || e > ((int64_t)1 << 31)) return ISPA_ERR_INVALID_ARG;
+    a.r.begin[i] = b;
+    a.r.end[i] = e;
+  }
+  if (n_ranges == 0)
+    return ispa::launch_attn_empty(out, lse, n_q, n_heads, head_dim, stream) == hipSuccess ? ISPA_OK
+                                                                                           : ISPA_ERR_HIP;
+  a.r.n_local = n_ranges;
+  a.r.n_total = n_ranges;
+  return ispa::launch_attn_chunk(a, head_dim, stream) == hipSuccess ? ISPA_OK : ISPA_ERR_HIP;
+}
+
+int ispa_attn_merge(const float* out_a, const float* lse_a, const float* out_b, const float* lse_b, int32_t n_q,
+                    int32_t n_heads, int32_t head_dim, float* out, float* lse, hipStream_t stream) {
+  if (!out_a || !lse_a || !out_b || !lse_b || !out) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(out_a) || !aligned16(out_b) || !aligned16(out)) return ISPA_ERR_INVALID_ARG;
+  if (((uintptr_t)lse_a & 3u) || ((uintptr_t)lse_b & 3u) || ((uintptr_t)lse & 3u)) return ISPA_ERR_INVALID_ARG;
+  if (n_q < 1 || n_heads < 1 || head_dim < 4 || head_dim % 4 != 0) return ISPA_ERR_INVALID_ARG;
+  if ((int64_t)n_heads * head_dim > ((int64_t)1 << 20)) return ISPA_ERR_INVALID_ARG;
+  // the merged LSE is written while other rows still read the inputs' LSE
+  const size_t lse_bytes = (size_t)n_q * n_heads * 4;
+  auto overlap = [](const void* x, const void* y, size_t n) {
+    return (const char*)x < (const char*)y + n && (const char*)y < (const char*)x + n;
+  };
+  if (lse && (overlap(lse, lse_a, lse_bytes) || overlap(lse, lse_b, lse_bytes))) return ISPA_ERR_INVALID_ARG;
+  return ispa::launch_attn_merge2(out_a, lse_a, out_b, lse_b, n_q, n_heads, head_dim, out, lse, stream) ==
+                 hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
 }
 
 size_t ispa_stats_workspace_bytes(int32_t d_in, int32_t d_out, int64_t max_rows) {

@@ -31,6 +31,22 @@ struct AttnRanges {
   int n_total;   // n_local or n_local + 1
 };
 
+// Split of the work over workgroups (used when whole work items would leave
+// part of the chip idle). The units are (work item, key tile) pairs in
+// item-major order, U = work items x tiles per item; segment g of G covers
+// units [g U / G, (g + 1) U / G). A piece is the part of one work item inside
+// one segment; a piece that does not cover all tiles of its item (or all its
+// local tiles) leaves its normalised output and LSE in a partial slot for
+// attn_merge_split.
+struct AttnSplit {
+  int64_t units;       // U
+  int32_t n_seg;       // G; 0: one whole work item per workgroup, no partials
+  int32_t max_pieces;  // partial slots per segment
+  float* part_o;       // [G * max_pieces][2][kAttnBq][head_dim]: [.][0] end state, [.][1] local set
+  float* part_lse;     // [G * max_pieces][2][kAttnBq]
+};
+constexpr int kAttnBq = 256;  // queries per work item
+
 struct AttnArgs {
   const uint16_t* q;
   const uint16_t* k;
@@ -45,9 +61,25 @@ struct AttnArgs {
   float scale_log2;   // logit scale * log2(e)
   float scale;        // logit scale (for the natural-log LSE)
   AttnRanges r;
+  AttnSplit split;
 };
 
+// Tiles of 64 keys visited for each work item, and those of the local set.
+int attn_tiles(const AttnRanges& r, int* n_tiles_local);
+// Compute units of the current device.
+int attn_cu_count();
+// Split plan for a launch: segments < 0 never splits, 0 splits when whole work
+// items would fill the chip poorly, > 0 forces that many segments. Fills
+// units/n_seg/max_pieces (n_seg = 0: no split) and returns the workspace bytes.
+size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit* s);
 hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream);
+// out = 0, lse = -inf (attention over an empty key set)
+hipError_t launch_attn_empty(float* out, float* lse, int64_t n_q, int64_t n_heads, int head_dim,
+                             hipStream_t stream);
+// Eq. 11-12 merge of two results over disjoint key sets (out may alias a or b).
+hipError_t launch_attn_merge2(const float* o_a, const float* lse_a, const float* o_b, const float* lse_b,
+                              int64_t n_q, int64_t n_heads, int head_dim, float* out, float* lse,
+                              hipStream_t stream);
 
 // ---- statistics (stats.hip) ----
 hipError_t launch_discrepancy(const void* x, int x_dtype, const void* y_full, const void* y_local,

@@ -38,7 +38,7 @@ def test_status_strings(L):
     for code in (0, -1, -2, -3, -4, -5):
         assert ispa.status_string(code).startswith("ISPA")
     assert "unknown" in ispa.status_string(7)
-    assert L.ispa_abi_version() == 100
+    assert L.ispa_abi_version() == 101
 
 
 def _attn(L, **kw):

@@ -16,12 +16,12 @@ DEV = "cuda"
 
 
 def run_and_check(n_q, cache_len, window, sink, heads, hd, dual, wid, capacity=None, q_scale=1.0,
-                  rows=None):
+                  rows=None, segments=0):
     print(f"[attn] n_q={n_q} N={cache_len} w={window} s={sink} H={heads} d={hd} dual={dual} "
-          f"wid={wid}", flush=True)
+          f"wid={wid} segments={segments}", flush=True)
     q, k, v = synth.chunk_qkv(wid, 0, 0, n_q, cache_len, heads * hd, DEV, q_scale=q_scale,
                               capacity=capacity)
-    res = ispa.attn_chunk(q, k, v, cache_len, window, heads, sink_len=sink, dual=dual)
+    res = ispa.attn_chunk(q, k, v, cache_len, window, heads, sink_len=sink, dual=dual, segments=segments)
     torch.cuda.synchronize()
     if rows is None:
         qn, sel = f64(q), None
@@ -107,6 +107,98 @@ def test_deterministic(shape):
         for x, y in zip(first, again):
             if y is not None:
                 assert torch.equal(x, y), f"launch {i + 1} differs"
+
+
+# the work split over the chip: runs of (work item, key tile) units that end
+# inside a work item leave partial results merged with Eq. 11-12
+@pytest.mark.parametrize("case", [
+    # n_q, N, w, s, H, d, dual, segments
+    (300, 1000, 200, 0, 2, 128, True, 3),      # pieces across items and the local boundary
+    (100, 333, 97, 13, 3, 128, True, 5),       # sink + window + history, ragged
+    (257, 1500, 1500, 0, 2, 128, False, 7),    # F-Layer, single stream
+    (600, 3000, 1000, 64, 2, 64, True, 11),    # d = 64
+    (64, 640, 64, 0, 2, 64, True, 20),         # one tile per run
+    (520, 2000, 300, 1, 1, 128, True, 2),      # fewer runs than work items
+])
+def test_split_parity(case):
+    n_q, N, w, s, H, d, dual, seg = case
+    run_and_check(n_q, N, w, s, H, d, dual, wid=12, segments=seg)
+
+
+def test_split_matches_unsplit_and_is_deterministic():
+    q, k, v = synth.chunk_qkv(13, 0, 0, 500, 2200, 256, DEV)
+    ref = ispa.attn_chunk(q, k, v, 2200, 700, 2, sink_len=5, dual=True, segments=-1)
+    a = ispa.attn_chunk(q, k, v, 2200, 700, 2, sink_len=5, dual=True, segments=9)
+    b = ispa.attn_chunk(q, k, v, 2200, 700, 2, sink_len=5, dual=True, segments=9)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    # the runs restart the softmax reference, so the bf16 rounding of the
+    # weights differs from the unsplit pass: agreement is within the parity
+    # tolerances, not bitwise
+    for x, y in zip(a[::2], ref[::2]):
+        assert_attn(f64(x), f64(y), "split vs unsplit")
+    for x, y in zip(a[1::2], ref[1::2]):
+        assert_lse(f64(x), f64(y), "split vs unsplit lse")
+
+
+def test_split_is_used_for_the_12_head_chunk():
+    # 12 heads x 19 query blocks = 228 work items: whole items would leave 28 of
+    # 256 compute units idle, so the automatic choice splits
+    L = ispa.lib()
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    nbytes = L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 12, 128, 1, 0)
+    if n_cu >= 240:
+        assert nbytes > 0
+    assert L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 12, 128, 1, -1) == 0
+
+
+# the paper's literal decomposable form (Eq. 9-12): local and history branches
+# as separate calls, fused by the LSE merge
+@pytest.mark.parametrize("case", [(300, 1000, 200, 0, 2, 128), (130, 900, 64, 7, 3, 64), (96, 700, 5000, 0, 2, 128)])
+def test_decomposable_branches_and_merge(case):
+    n_q, N, w, s, H, d = case
+    q, k, v = synth.chunk_qkv(14, 0, 0, n_q, N, H * d, DEV)
+    s1, lo = min(s, N), max(N - w, 0)
+    o_loc, l_loc = ispa.attn_chunk(q, k, v, N, w, H, sink_len=s)
+    hist = [(s1, lo)] if lo > s1 else []
+    o_hist, l_hist = ispa.attn_ranges(q, k, v, hist, H)
+    o_full, l_full = ispa.attn_merge(o_loc, l_loc, o_hist, l_hist)
+    torch.cuda.synchronize()
+    ref = oracle.chunk_attention(f64(q), f64(k[:N]), f64(v[:N]), N, w, H, sink_len=s,
+                                 branches=("full", "hist"))
+    assert_attn(f64(o_full), ref["full"][0], "merged full")
+    assert_lse(f64(l_full), ref["full"][1], "merged full lse")
+    if hist:
+        assert_attn(f64(o_hist), ref["hist"][0], "hist")
+        assert_lse(f64(l_hist), ref["hist"][1], "hist lse")
+    else:
+        assert torch.all(o_hist == 0) and torch.all(torch.isneginf(l_hist))
+        assert torch.equal(o_full, o_loc) and torch.equal(l_full, l_loc)
+
+
+def test_merge_kernel_against_oracle():
+    g = torch.Generator().manual_seed(15)
+    n_q, H, d = 77, 3, 64
+    oa = torch.randn(n_q, H * d, generator=g)
+    ob = torch.randn(n_q, H * d, generator=g)
+    la = torch.randn(H, n_q, generator=g) * 20
+    lb = torch.randn(H, n_q, generator=g) * 20
+    la[0, :5] = -float("inf")                 # one branch empty
+    lb[1, 3:9] = -float("inf")
+    la[2, 10:12] = -float("inf")              # both empty
+    lb[2, 10:12] = -float("inf")
+    out, lse = ispa.attn_merge(oa.to(DEV), la.to(DEV), ob.to(DEV), lb.to(DEV))
+    torch.cuda.synchronize()
+    o_ref = np.zeros((n_q, H * d))
+    l_ref = np.zeros((H, n_q))
+    for h in range(H):
+        cols = slice(h * d, (h + 1) * d)
+        o_ref[:, cols], l_ref[h] = oracle.lse_merge(f64(oa)[:, cols], f64(la)[h], f64(ob)[:, cols], f64(lb)[h])
+    np.testing.assert_allclose(f64(out), o_ref, rtol=2e-6, atol=2e-6)
+    fin = np.isfinite(l_ref)
+    np.testing.assert_allclose(f64(lse)[fin], l_ref[fin], rtol=0, atol=1e-5)
+    assert np.all(np.isneginf(f64(lse)[~fin]))
 
 
 def test_binding_rejects_bad_tensors():
