@@ -14,7 +14,10 @@ follows:
 * ``attention``  -- chunk attention over an explicit key set (Sec. 2, Eq. 3;
   Sec. 3.4, Eq. 7-10) and the log-sum-exp fusion (Eq. 11-12).
 * ``absorb``     -- residual, sufficient statistics, closed-form ridge solve,
-  feasibility score and layer ranking (Sec. 3.2, Eq. 4-6; Sec. 3.3).
+  feasibility score, layer ranking and the weight update (Sec. 3.2, Eq. 4-6;
+  Sec. 3.3).
+* ``kvcache``    -- what an L-Layer's cache holds after the permanent
+  eviction (Sec. 3.3; the local set of Eq. 7 as chunks keep arriving).
 * ``budget``     -- KV-cache accounting for a given L-Layer budget
   (Sec. 4, Table 1/2 "KVCache" column; K = xN).
 
@@ -39,7 +42,9 @@ from .absorb import (
     feasibility,
     feasibility_direct,
     select_layers,
+    inject,
 )
+from .kvcache import evict_local, LocalHistory
 from .budget import kv_retained_fraction, n_local_layers
 
 __all__ = [
@@ -56,6 +61,9 @@ __all__ = [
     "feasibility",
     "feasibility_direct",
     "select_layers",
+    "inject",
+    "evict_local",
+    "LocalHistory",
     "kv_retained_fraction",
     "n_local_layers",
 ]

@@ -10,7 +10,7 @@ Definitions followed (arXiv 2607.00712):
 * Sec. 3.2, last paragraph: the method only sums A_loc^T A_loc and A_loc^T R
   over the warmup rows and solves one D x D system at the end of warmup.
 * Sec. 3.3: layers are ranked by eps ascending and the K lowest become
-  L-Layers.
+  L-Layers; each of them takes W_new = W + dW in place.
 
 Readings where the paper is silent (each listed in the design doc):
 
@@ -26,6 +26,10 @@ Readings where the paper is silent (each listed in the design doc):
 * "Matrix inversion" is carried out as a Cholesky solve of the SPD system;
   a non-positive pivot (possible only when lam = 0) is reported as NotSPD.
 * Ties in the ranking are broken by layer index (stable ascending sort).
+* W is stored either as in Eq. 4 ([D_in, D_out], rows are input features) or
+  transposed ([D_out, D_in], the usual linear-layer weight); a bf16 weight is
+  updated as bf16_rne(fp32(W) + dW), an fp32 weight as fp32(W) + dW (one IEEE
+  float32 addition per element).
 """
 
 import numpy as np
@@ -145,3 +149,20 @@ def select_layers(eps, k):
     eps = np.asarray(eps, dtype=np.float64)
     order = sorted(range(eps.size), key=lambda i: (eps[i], i))
     return np.asarray(order[: int(k)], dtype=np.int64)
+
+
+def inject(W, dW, transposed=False):
+    """W_new = W + dW for an L-Layer's output projection (Sec. 3.3).
+
+    ``W`` is float32 holding the weight's values (bf16 values for a bf16
+    weight); ``dW`` is [D_in, D_out] as solved by Eq. 5. With ``transposed``
+    the weight is [D_out, D_in] and receives dW^T. Returns the float32 sum
+    (the caller rounds to bf16 with bf16_round for a bf16 weight).
+    """
+    W = np.asarray(W, dtype=np.float32)
+    d = np.asarray(dW, dtype=np.float32)
+    if transposed:
+        d = d.T
+    if W.shape != d.shape:
+        raise ValueError("weight and dW shapes differ")
+    return (W + d).astype(np.float32)

@@ -386,6 +386,55 @@ def pin_select_layers(select_layers):
     assert list(select_layers(eps, 6)) == [4, 1, 3, 2, 0, 5]
 
 
+def pin_inject(inject, bf16_round):
+    # hand example: W_new = W + dW (Sec. 3.3), in both storage orders
+    W = np.array([[1.0, 2.0], [3.0, 4.0]], dtype=np.float32)
+    dW = np.array([[0.5, -1.0], [0.25, 0.0]], dtype=np.float32)
+    want = np.array([[1.5, 1.0], [3.25, 4.0]], dtype=np.float32)
+    assert np.array_equal(inject(W, dW), want)
+    assert np.array_equal(inject(W.T.copy(), dW, transposed=True), want.T)
+    # a non-square weight: [D_in, D_out] = [2, 3], transposed [3, 2]
+    W2 = np.arange(6, dtype=np.float32).reshape(2, 3)
+    d2 = np.full((2, 3), 0.5, dtype=np.float32)
+    d2[1, 2] = -2.0
+    assert np.array_equal(inject(W2, d2), W2 + d2)
+    assert np.array_equal(inject(W2.T.copy(), d2, transposed=True), (W2 + d2).T)
+    try:
+        inject(W2, d2, transposed=True)
+        raise AssertionError("shape mismatch not rejected")
+    except ValueError:
+        pass
+    # bf16 weight: the fp32 sum rounded to nearest even bf16 (spacing 2^-7 at 1)
+    one = np.ones((1, 1), dtype=np.float32)
+    assert bf16_round(inject(one, np.full((1, 1), 2.0 ** -9, np.float32)))[0, 0] == 1.0
+    assert bf16_round(inject(one, np.full((1, 1), 3 * 2.0 ** -9, np.float32)))[0, 0] == 1.0 + 2.0 ** -7
+
+
+def pin_evict_local(evict_local):
+    rows = np.arange(10, dtype=np.float32)[:, None] * np.ones((1, 4), np.float32)
+    k, v = evict_local(rows, -rows, 10, 3, 2)
+    assert list(k[:, 0]) == [0, 1, 7, 8, 9] and list(v[:, 0]) == [0, -1, -7, -8, -9]
+    k, v = evict_local(rows, -rows, 5, 3, 4)       # sink and window meet: all rows
+    assert list(k[:, 0]) == [0, 1, 2, 3, 4]
+    k, v = evict_local(rows, -rows, 8, 100, 0)     # window beyond the cache
+    assert list(k[:, 0]) == list(range(8))
+    k, v = evict_local(rows, -rows, 10, 1, 0)      # the last key only
+    assert list(k[:, 0]) == [9]
+
+
+def pin_local_history(LocalHistory):
+    lab = lambda a, b: np.arange(a, b, dtype=np.float32)[:, None] * np.ones((1, 2), np.float32)
+    h = LocalHistory(lab(0, 6), -lab(0, 6), 6, 4, 1)
+    k, v = h.rows()
+    assert list(k[:, 0]) == [0, 2, 3, 4, 5]
+    h.append(lab(6, 9), -lab(6, 9))                # rows 6..8 arrive
+    k, v = h.rows()
+    assert list(k[:, 0]) == [0, 5, 6, 7, 8] and list(v[:, 0]) == [0, -5, -6, -7, -8]
+    h.append(lab(9, 15), -lab(9, 15))              # more than the window at once
+    k, _ = h.rows()
+    assert list(k[:, 0]) == [0, 11, 12, 13, 14]
+
+
 # ---------------------------------------------------------------- budget
 
 def _frac(s):

@@ -88,6 +88,18 @@ def test_select_layers():
     P.pin_select_layers(oracle.select_layers)
 
 
+def test_inject():
+    P.pin_inject(oracle.inject, oracle.bf16_round)
+
+
+def test_evict_local():
+    P.pin_evict_local(oracle.evict_local)
+
+
+def test_local_history():
+    P.pin_local_history(oracle.LocalHistory)
+
+
 def test_kv_table():
     P.pin_kv_table(oracle.kv_retained_fraction)
 

@@ -46,7 +46,13 @@ def absorb_pins(m):
         lambda: P.pin_not_spd(m.solve_modulation, m.NotSPD),
         lambda: P.pin_feasibility(m.Stats, m.solve_modulation, m.feasibility, m.feasibility_direct, m.residual),
         lambda: P.pin_select_layers(m.select_layers),
+        lambda: P.pin_inject(m.inject, m.bf16_round),
     ]
+
+
+def kvcache_pins(m):
+    return [lambda: P.pin_evict_local(m.evict_local),
+            lambda: P.pin_local_history(m.LocalHistory)]
 
 
 def budget_pins(m):
@@ -81,6 +87,13 @@ MUTATIONS = [
      "return float(s) + float(np.sum(dW * C)) - float(lam) * float(np.sum(dW * dW))", absorb_pins),
     ("oracle.absorb", "key=lambda i: (eps[i], i)", "key=lambda i: (-eps[i], i)", absorb_pins),
     ("oracle.absorb", "self.s += float(np.sum(r * r))", "self.s += float(np.sum(np.abs(r)))", absorb_pins),
+    ("oracle.absorb", "        d = d.T", "        pass", absorb_pins),
+    ("oracle.absorb", "return (W + d).astype(np.float32)", "return (W - d).astype(np.float32)", absorb_pins),
+    # kvcache
+    ("oracle.kvcache", "return k[local], v[local]", "return k[local], k[local]", kvcache_pins),
+    ("oracle.kvcache", "k = np.concatenate(self.k, axis=0)", "k = self.k[-1]", kvcache_pins),
+    ("oracle.kvcache", "return evict_local(k, v, k.shape[0], self.window, self.sink)",
+     "return evict_local(k, v, k.shape[0], self.window + 1, self.sink)", kvcache_pins),
     # budget
     ("oracle.budget", "return (1.0 - x) * 1.0 + x * r", "return 1.0 - x * r", budget_pins),
     ("oracle.budget", "return int(round(float(x) * int(n_layers)))",
@@ -103,7 +116,7 @@ def test_planted_mistake_is_caught(module_name, old, new, pins):
 
 def test_unmutated_copies_pass():
     for name, pins in (("oracle.attention", attention_pins), ("oracle.absorb", absorb_pins),
-                       ("oracle.budget", budget_pins)):
+                       ("oracle.kvcache", kvcache_pins), ("oracle.budget", budget_pins)):
         m = mutant(name, "\"\"\"", "\"\"\"")
         for pin in pins(m):
             pin()
