@@ -133,7 +133,39 @@ def gpu_run(w, steps, warmup, only="all"):
         parts["solve"].append(ev[3].elapsed_time(ev[4]))
     avg = {k2: sum(v2) / len(v2) for k2, v2 in parts.items()}
     ms_step = (t1 - t0) * 1e3 / steps
+    if only == "all":
+        avg["absorb"] = absorb_run(ispa, w, k, v, dw, dev)
     return ms_step, avg
+
+
+def absorb_run(ispa, w, k, v, dw, dev, reps=10):
+    """The one-off absorption at the end of warmup (Sec. 3.3), outside the step:
+    the in-place update of a bf16 linear-layer weight with dW^T, and the
+    eviction of the layer's cache to its local set. Returns ms and HBM GB/s."""
+    D = w["heads"] * w["head_dim"]
+    weight = torch.zeros((D, D), dtype=torch.bfloat16, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    inj = timed(lambda: ispa.inject_modulation(weight, dw, transposed=True))
+    ring = (torch.empty((w["sink"] + w["window"], D), dtype=torch.bfloat16, device=dev),
+            torch.empty((w["sink"] + w["window"], D), dtype=torch.bfloat16, device=dev))
+    ev = timed(lambda: ispa.LocalKV(k, v, w["cache_len"], w["window"], w["sink"], ring=ring))
+    rows = ispa.LocalKV(k, v, w["cache_len"], w["window"], w["sink"], ring=ring).rows
+    inj_bytes = D * D * (2 + 4 + 2)
+    ev_bytes = rows * D * 2 * 2 * 2
+    return {"inject_ms": round(inj, 4), "inject_gbs": round(inj_bytes / inj / 1e6, 1),
+            "evict_ms": round(ev, 4), "evict_gbs": round(ev_bytes / ev / 1e6, 1),
+            "hbm_peak_gbs": PEAK_HBM_GBS}
 
 
 def hbm_copy(steps, warmup, nbytes=1 << 30):
@@ -271,6 +303,7 @@ def main():
             "solve_ms": round(avg["solve"], 4),
             "solve_tflops": round(f["solve"] / avg["solve"] / 1e9, 2),
             "flop": {k2: v2 for k2, v2 in f.items()},
+            "absorb": avg.get("absorb"),
         },
     }
     if args.only != "all":

@@ -12,6 +12,9 @@
  *                          and the last paragraph of Sec. 3.2)
  *   ispa_solve_modulation  dW = (G + lambda I)^-1 C and the feasibility score
  *                          eps (Sec. 3.2, Eq. 5-6)
+ * and the layer absorption that follows warmup (Sec. 3.3): ranking by eps,
+ * the in-place weight update W + dW, and the L-Layer cache after the
+ * permanent eviction of the history.
  *
  * Conventions shared by every call
  *   - Matrices are row-major with the last dimension contiguous.
@@ -234,6 +237,63 @@ int ispa_accum_stats(ispa_stats* handle, const void* x, int32_t x_dtype,
  * ISPA_ERR_NOT_SPD (delta_w then unspecified) if a pivot is not positive.
  */
 int ispa_solve_modulation(ispa_stats* handle, float lambda, float* delta_w, double* eps_out);
+
+/* ---------------------------------------------------------- absorption */
+/*
+ * Instance-specific layer selection (Sec. 3.3): the k layers with the lowest
+ * feasibility score eps become L-Layers. Host-only (no device work).
+ *   eps        host double [n_layers]
+ *   k          0 <= k <= n_layers
+ *   selected   host int32 [k]: layer indices in ascending eps order; ties by
+ *              layer index, NaN after every number
+ */
+int ispa_select_layers(const double* eps, int32_t n_layers, int32_t k, int32_t* selected);
+
+/*
+ * In-place weight update of an L-Layer's output projection (Sec. 3.3):
+ * W_new = W + dW, one fp32 addition per element, rounded to nearest even for a
+ * bf16 weight.
+ *   weight        device [d_in, d_out] (transposed == 0: the row-vector form of
+ *                 Eq. 4, Y = A W) or [d_out, d_in] (transposed != 0: a linear
+ *                 layer's weight, Y = A W^T, which receives dW^T); of
+ *                 weight_dtype ISPA_DTYPE_BF16 or ISPA_DTYPE_F32
+ *   delta_w       device fp32 [d_in, d_out], as written by ispa_solve_modulation;
+ *                 must not overlap weight
+ * Asynchronous on `stream`.
+ */
+int ispa_inject_modulation(void* weight, int32_t weight_dtype, int32_t transposed, const float* delta_w,
+                           int32_t d_in, int32_t d_out, hipStream_t stream);
+
+/*
+ * The permanent eviction of an L-Layer's history (Sec. 3.3): copies the local
+ * set of Eq. 7 of a cache of cache_len keys into a compact ring buffer:
+ *   ring rows [0, s')            = cache rows [0, s'),  s' = min(sink_len, N)
+ *   ring rows [s', s' + w')      = the last w' = min(window, N - s') cache rows
+ * The ring buffers hold at least s' + window rows of `hidden` bf16 values (the
+ * window part keeps growing to `window` rows as keys arrive); `*ring_rows`
+ * (host, may be NULL) receives s' + w'. The window rows then form a ring whose
+ * head (window keys written so far) is w'; see ispa_kv_ring_append.
+ *   k_cache, v_cache, k_ring, v_ring   device bf16, rows of `hidden` elements
+ *                                       (hidden a multiple of 8), 16-byte aligned;
+ *                                       the ring must not overlap the cache
+ * Attention over the L-Layer is then ispa_attn_chunk on the ring with
+ * cache_len = the filled ring rows and window >= cache_len (key order does not
+ * matter to softmax attention). Asynchronous on `stream`.
+ */
+int ispa_kv_evict(const void* k_cache, const void* v_cache, int64_t cache_len, int64_t window, int64_t sink_len,
+                  int32_t hidden, void* k_ring, void* v_ring, int64_t* ring_rows, hipStream_t stream);
+
+/*
+ * Appends n_new keys (k_new/v_new [n_new, hidden] bf16) to an L-Layer ring:
+ * window key number head + r goes to ring row sink_rows + (head + r) mod window,
+ * so the ring keeps the sink rows and the most recent `window` keys (the local
+ * set of Eq. 7 of the whole sequence). head = window keys written so far (w'
+ * after ispa_kv_evict); afterwards the caller's head is head + n_new and the
+ * filled ring rows are sink_rows + min(head + n_new, window). Only the last
+ * min(n_new, window) new keys are copied. Asynchronous on `stream`.
+ */
+int ispa_kv_ring_append(void* k_ring, void* v_ring, int64_t sink_rows, int64_t window, int64_t head,
+                        const void* k_new, const void* v_new, int64_t n_new, int32_t hidden, hipStream_t stream);
 
 #ifdef __cplusplus
 }

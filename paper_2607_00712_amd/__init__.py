@@ -9,6 +9,8 @@ works without the library, but every call raises if it is not built.
                dual=False, segments=0) -> (out, lse) or (out, lse, out_local, lse_local)
     attn_ranges(q, k_cache, v_cache, ranges, n_heads) -> (out, lse)
     attn_merge(out_a, lse_a, out_b, lse_b) -> (out, lse)
+    select_layers(eps, k) -> indices;  inject_modulation(weight, delta_w, transposed)
+    LocalKV(k_cache, v_cache, cache_len, window, sink_len): evict, append, attend
     Stats(d_in, d_out, max_rows).accum(x, y_full, y_local)
     Stats.solve(lam) -> (delta_w, eps)
 """
@@ -19,6 +21,7 @@ import os
 import torch
 
 __all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "status_string",
+           "select_layers", "inject_modulation", "LocalKV",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
            "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
 
@@ -47,6 +50,11 @@ _SIGNATURES = {
     "ispa_attn_ranges": (ctypes.c_int, [_c_p, _c_p, _c_p, ctypes.POINTER(_c_i64), _c_i32, _c_i32, _c_i32, _c_i32,
                                         _c_f32, _c_p, _c_p, _c_p]),
     "ispa_attn_merge": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
+    "ispa_select_layers": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), _c_i32, _c_i32, ctypes.POINTER(_c_i32)]),
+    "ispa_inject_modulation": (ctypes.c_int, [_c_p, _c_i32, _c_i32, _c_p, _c_i32, _c_i32, _c_p]),
+    "ispa_kv_evict": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_p, _c_p, ctypes.POINTER(_c_i64),
+                                     _c_p]),
+    "ispa_kv_ring_append": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i32, _c_p]),
     "ispa_stats_workspace_bytes": (_c_sz, [_c_i32, _c_i32, _c_i64]),
     "ispa_stats_create": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_p, _c_sz, _c_i32, _c_i32, _c_i64, _c_p]),
     "ispa_stats_reset": (ctypes.c_int, [_c_p]),
@@ -326,3 +334,86 @@ class Stats:
             self.close()
         except Exception:
             pass
+
+
+def select_layers(eps, k):
+    """Indices of the k layers with the lowest eps (ispa_select_layers, Sec. 3.3)."""
+    L = lib()
+    vals = [float(e) for e in eps]
+    arr = (ctypes.c_double * max(1, len(vals)))(*vals)
+    out = (_c_i32 * max(1, int(k)))()
+    _check(L.ispa_select_layers(arr, len(vals), int(k), out), "ispa_select_layers")
+    return [int(out[i]) for i in range(int(k))]
+
+
+def inject_modulation(weight, delta_w, transposed=False):
+    """In-place W += dW (or dW^T for a [d_out, d_in] linear weight); ispa_inject_modulation."""
+    L = lib()
+    if weight.dtype not in _DT:
+        raise TypeError("weight must be bf16 or fp32")
+    _require(weight, "weight", weight.dtype)
+    _require(delta_w, "delta_w", torch.float32, weight.device)
+    d_in, d_out = delta_w.shape
+    want = (d_out, d_in) if transposed else (d_in, d_out)
+    if tuple(weight.shape) != want:
+        raise ValueError(f"weight must have shape {want}")
+    st = L.ispa_inject_modulation(_ptr(weight), _DT[weight.dtype], int(bool(transposed)), _ptr(delta_w), int(d_in),
+                                  int(d_out), _stream(weight.device))
+    _check(st, "ispa_inject_modulation")
+    return weight
+
+
+class LocalKV:
+    """An L-Layer's KV cache after the permanent eviction (ispa_kv_evict /
+    ispa_kv_ring_append): the sink rows and a ring of the `window` most recent
+    keys, attended as one contiguous set of rows."""
+
+    def __init__(self, k_cache, v_cache, cache_len, window, sink_len=0, ring=None):
+        """``ring`` optionally supplies the (k, v) ring tensors, each at least
+        [min(sink_len, cache_len) + window, hidden] bf16 (reused instead of allocated)."""
+        L = lib()
+        _require(k_cache, "k_cache", torch.bfloat16)
+        dev = k_cache.device
+        _require(v_cache, "v_cache", torch.bfloat16, dev)
+        if k_cache.shape != v_cache.shape or k_cache.shape[0] < cache_len:
+            raise ValueError("k/v caches must have the same shape and hold cache_len rows")
+        self.hidden = int(k_cache.shape[1])
+        self.window = int(window)
+        self.sink = int(min(sink_len, cache_len))
+        shape = (self.sink + self.window, self.hidden)
+        if ring is None:
+            self.k = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+            self.v = torch.empty_like(self.k)
+        else:
+            self.k, self.v = ring
+            for name, t in (("ring k", self.k), ("ring v", self.v)):
+                _require(t, name, torch.bfloat16, dev)
+                if t.shape[0] < shape[0] or t.shape[1] != shape[1]:
+                    raise ValueError(f"{name} must be at least {shape}")
+        rows = _c_i64(0)
+        st = L.ispa_kv_evict(_ptr(k_cache), _ptr(v_cache), int(cache_len), self.window, int(sink_len), self.hidden,
+                             _ptr(self.k), _ptr(self.v), ctypes.byref(rows), _stream(dev))
+        _check(st, "ispa_kv_evict")
+        self.head = int(rows.value) - self.sink
+
+    @property
+    def rows(self):
+        """Filled ring rows (sink + window keys held)."""
+        return self.sink + min(self.head, self.window)
+
+    def append(self, k_new, v_new):
+        L = lib()
+        _require(k_new, "k_new", torch.bfloat16, self.k.device)
+        _require(v_new, "v_new", torch.bfloat16, self.k.device)
+        if k_new.shape != v_new.shape or k_new.shape[1] != self.hidden:
+            raise ValueError("new keys/values must be [n, hidden] of the cache's hidden size")
+        st = L.ispa_kv_ring_append(_ptr(self.k), _ptr(self.v), self.sink, self.window, self.head, _ptr(k_new),
+                                   _ptr(v_new), int(k_new.shape[0]), self.hidden, _stream(self.k.device))
+        _check(st, "ispa_kv_ring_append")
+        self.head += int(k_new.shape[0])
+
+    def attend(self, q, n_heads, **kw):
+        """Attention of q over every key the L-Layer holds (append the current
+        chunk first: the keys of the current chunk are part of its local set)."""
+        n = self.rows
+        return attn_chunk(q, self.k, self.v, n, n, n_heads, **kw)

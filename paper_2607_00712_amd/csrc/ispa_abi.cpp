@@ -3,6 +3,7 @@
 // Every argument error is reported before anything is enqueued.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <math.h>
 #include <new>
 #include <stdint.h>
@@ -336,6 +337,82 @@ int ispa_solve_modulation(ispa_stats* h, float lambda, float* delta_w, double* e
   if (status != 0) return ISPA_ERR_NOT_SPD;
   if (eps_out) *eps_out = sc[0] - sc[2] - (double)lambda * sc[3];
   return ISPA_OK;
+}
+
+
+int ispa_select_layers(const double* eps, int32_t n_layers, int32_t k, int32_t* selected) {
+  if (!eps || n_layers < 0 || n_layers > (1 << 20) || k < 0 || k > n_layers || (k > 0 && !selected))
+    return ISPA_ERR_INVALID_ARG;
+  int32_t* idx = new (std::nothrow) int32_t[n_layers > 0 ? n_layers : 1];
+  if (!idx) return ISPA_ERR_STATE;
+  for (int32_t i = 0; i < n_layers; ++i) idx[i] = i;
+  // ascending eps, NaN after every number, ties by layer index (stable sort)
+  std::stable_sort(idx, idx + n_layers, [eps](int32_t a, int32_t b) {
+    const double x = eps[a], y = eps[b];
+    if (isnan(x)) return false;
+    if (isnan(y)) return true;
+    return x < y;
+  });
+  for (int32_t i = 0; i < k; ++i) selected[i] = idx[i];
+  delete[] idx;
+  return ISPA_OK;
+}
+
+int ispa_inject_modulation(void* weight, int32_t weight_dtype, int32_t transposed, const float* delta_w,
+                           int32_t d_in, int32_t d_out, hipStream_t stream) {
+  if (weight_dtype != ISPA_DTYPE_BF16 && weight_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (!weight || !delta_w) return ISPA_ERR_INVALID_ARG;
+  if (d_in < 1 || d_out < 1 || d_in > 65536 || d_out > 65536) return ISPA_ERR_INVALID_ARG;
+  const size_t esz = weight_dtype == ISPA_DTYPE_BF16 ? 2 : 4;
+  if (((uintptr_t)weight % esz) || ((uintptr_t)delta_w & 3u)) return ISPA_ERR_INVALID_ARG;
+  const size_t n = (size_t)d_in * d_out;
+  const char* w0 = (const char*)weight;
+  const char* d0 = (const char*)delta_w;
+  if (w0 < d0 + n * 4 && d0 < w0 + n * esz) return ISPA_ERR_INVALID_ARG;
+  return ispa::launch_inject(weight, weight_dtype == ISPA_DTYPE_BF16 ? 0 : 1, transposed != 0, delta_w, d_in, d_out,
+                             stream) == hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
+}
+
+int ispa_kv_evict(const void* k_cache, const void* v_cache, int64_t cache_len, int64_t window, int64_t sink_len,
+                  int32_t hidden, void* k_ring, void* v_ring, int64_t* ring_rows, hipStream_t stream) {
+  if (!k_cache || !v_cache || !k_ring || !v_ring) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_ring) || !aligned16(v_ring))
+    return ISPA_ERR_INVALID_ARG;
+  if (hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20)) return ISPA_ERR_INVALID_ARG;
+  if (cache_len < 1 || cache_len > ((int64_t)1 << 31) || window < 1 || sink_len < 0) return ISPA_ERR_INVALID_ARG;
+  if (k_ring == k_cache || v_ring == v_cache || k_ring == v_ring) return ISPA_ERR_INVALID_ARG;
+  // local set of Eq. 7: sink rows [0, s'), window rows [max(N - w, s'), N)
+  const int64_t N = cache_len;
+  const int64_t s1 = sink_len < N ? sink_len : N;
+  const int64_t lo = N - window > s1 ? N - window : s1;
+  const int64_t src[2] = {0, lo}, dst[2] = {0, s1}, n[2] = {s1, N - lo};
+  if (ring_rows) *ring_rows = s1 + (N - lo);
+  return ispa::launch_kv_copy(k_cache, v_cache, k_ring, v_ring, (int64_t)hidden * 2, src, dst, n, 2, stream) ==
+                 hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
+}
+
+int ispa_kv_ring_append(void* k_ring, void* v_ring, int64_t sink_rows, int64_t window, int64_t head,
+                        const void* k_new, const void* v_new, int64_t n_new, int32_t hidden, hipStream_t stream) {
+  if (!k_ring || !v_ring || !k_new || !v_new) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(k_ring) || !aligned16(v_ring) || !aligned16(k_new) || !aligned16(v_new)) return ISPA_ERR_INVALID_ARG;
+  if (hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20)) return ISPA_ERR_INVALID_ARG;
+  if (sink_rows < 0 || window < 1 || head < 0 || n_new < 0 || window > ((int64_t)1 << 31)) return ISPA_ERR_INVALID_ARG;
+  if (n_new == 0) return ISPA_OK;
+  // new key r is window key number head + r, at ring row sink + (head + r) mod window;
+  // only the last min(n_new, window) of them survive
+  const int64_t m = n_new < window ? n_new : window;
+  const int64_t p = (head + n_new - m) % window;
+  const int64_t first = m < window - p ? m : window - p;
+  const int64_t src[2] = {n_new - m, n_new - m + first}, dst[2] = {sink_rows + p, sink_rows};
+  const int64_t n[2] = {first, m - first};
+  return ispa::launch_kv_copy(k_new, v_new, k_ring, v_ring, (int64_t)hidden * 2, src, dst, n, 2, stream) ==
+                 hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
 }
 
 }  // extern "C"

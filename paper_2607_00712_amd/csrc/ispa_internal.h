@@ -90,6 +90,14 @@ hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d
                        float* G, float* C, hipStream_t stream);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
 
+// ---- absorption (absorb.hip) ----
+// W += dW (transposed: W[j][i] += dW[i][j]); dtype 0 bf16, 1 fp32
+hipError_t launch_inject(void* W, int dtype, bool transposed, const float* dW, int d_in, int d_out,
+                         hipStream_t stream);
+// up to 3 row copies of K and V (rows of row_bytes, a multiple of 16)
+hipError_t launch_kv_copy(const void* k_src, const void* v_src, void* k_dst, void* v_dst, int64_t row_bytes,
+                          const int64_t* src, const int64_t* dst, const int64_t* n, int n_seg, hipStream_t stream);
+
 // ---- solve (solve.hip) ----
 struct SolveWork {
   float* L;          // [d, d] factor (lower triangle)

@@ -111,3 +111,36 @@ def test_product_never_imports_oracle():
             if f.endswith((".py", ".cpp", ".hip", ".h")):
                 src = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in src.replace("the oracle", ""), f"{f} mentions the oracle"
+
+
+def test_select_layers_against_oracle(L):
+    # host-only entry point: compared with the oracle's stable ranking
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(7)
+    for n in (1, 5, 30, 40):
+        eps = rng.integers(0, 6, size=n).astype(np.float64) * 0.25   # many ties
+        for k in (0, 1, n // 2, n):
+            assert ispa.select_layers(eps, k) == list(oracle.select_layers(eps, k))
+    # NaN sorts after every number
+    assert ispa.select_layers([float("nan"), 2.0, -1.0, float("inf")], 4) == [2, 1, 3, 0]
+    E = ispa.ISPA_ERR_INVALID_ARG
+    arr = (ctypes.c_double * 3)(1.0, 2.0, 3.0)
+    out = (ctypes.c_int32 * 4)()
+    assert L.ispa_select_layers(arr, 3, 4, out) == E
+    assert L.ispa_select_layers(arr, 3, -1, out) == E
+    assert L.ispa_select_layers(None, 3, 1, out) == E
+
+
+def test_absorption_argument_errors(L):
+    E, U = ispa.ISPA_ERR_INVALID_ARG, ispa.ISPA_ERR_UNSUPPORTED
+    p = lambda v: ctypes.c_void_p(v)
+    assert L.ispa_inject_modulation(p(256), 7, 0, p(4096), 4, 4, p(0)) == U
+    assert L.ispa_inject_modulation(p(0), 0, 0, p(4096), 4, 4, p(0)) == E
+    assert L.ispa_inject_modulation(p(256), 0, 0, p(4096), 0, 4, p(0)) == E
+    assert L.ispa_inject_modulation(p(4096), 0, 0, p(4096), 4, 4, p(0)) == E      # overlap
+    assert L.ispa_kv_evict(p(16), p(32), 10, 3, 0, 12, p(64), p(128), None, p(0)) == E   # hidden % 8
+    assert L.ispa_kv_evict(p(16), p(32), 0, 3, 0, 16, p(64), p(128), None, p(0)) == E
+    assert L.ispa_kv_evict(p(16), p(32), 10, 3, 0, 16, p(16), p(128), None, p(0)) == E  # ring == cache
+    assert L.ispa_kv_ring_append(p(16), p(32), 0, 0, 0, p(64), p(128), 4, 16, p(0)) == E  # window 0
+    assert L.ispa_kv_ring_append(p(16), p(32), 0, 4, -1, p(64), p(128), 4, 16, p(0)) == E

@@ -1,0 +1,103 @@
+"""GPU parity of the absorption calls (Sec. 3.3) against the oracle on
+identical seeded inputs, through the C ABI via the ctypes binding: the
+in-place weight update W + dW, the permanent eviction of an L-Layer's history
+and its ring of recent keys, and attention over that ring."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2607_00712_amd as ispa
+from parity_util import assert_attn, assert_lse, f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def bits(t):
+    """Exact bit patterns of a bf16 tensor (for bitwise comparisons)."""
+    return t.detach().cpu().view(torch.int16).numpy()
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("transposed", [False, True])
+@pytest.mark.parametrize("shape", [(128, 128), (200, 72), (64, 1000)])
+def test_inject_bitwise(dtype, transposed, shape):
+    d_in, d_out = shape
+    g = torch.Generator().manual_seed(d_in * 7 + d_out)
+    w = torch.randn((d_out, d_in) if transposed else (d_in, d_out), generator=g).to(dtype)
+    dw = torch.randn((d_in, d_out), generator=g) * 0.05
+    w_dev = w.to(DEV)
+    ispa.inject_modulation(w_dev, dw.to(DEV), transposed=transposed)
+    torch.cuda.synchronize()
+    want = oracle.inject(w.float().numpy(), dw.numpy(), transposed=transposed)
+    if dtype == torch.bfloat16:
+        want_t = torch.from_numpy(oracle.bf16_round(want)).to(torch.bfloat16)
+        assert np.array_equal(bits(w_dev), bits(want_t))
+    else:
+        assert np.array_equal(w_dev.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("case", [(640, 192, 64), (640, 192, 0), (300, 1000, 0), (300, 64, 500), (257, 100, 13)])
+def test_evict_bitwise(case):
+    N, w, s = case
+    H, d = 2, 64
+    _, k, v = synth.chunk_qkv(31, 0, 0, 1, N, H * d, DEV)
+    kv = ispa.LocalKV(k, v, N, w, s)
+    torch.cuda.synchronize()
+    k_ref, v_ref = oracle.evict_local(k.cpu().view(torch.int16).numpy(), v.cpu().view(torch.int16).numpy(), N, w, s)
+    assert kv.rows == k_ref.shape[0]
+    assert np.array_equal(bits(kv.k[: kv.rows]), k_ref)
+    assert np.array_equal(bits(kv.v[: kv.rows]), v_ref)
+
+
+def _sorted_rows(a):
+    return a[np.lexsort(a.T[::-1])]
+
+
+@pytest.mark.parametrize("sink", [0, 64])
+def test_ring_follows_the_local_set(sink):
+    # cache of 5 chunks of 64 keys, window of 3 chunks; then chunks of 64, 100
+    # (a ragged one), 250 (more than the window) and 64 keys arrive
+    H, d, w = 2, 64, 192
+    _, k, v = synth.chunk_qkv(32, 0, 0, 1, 320, H * d, DEV)
+    kv = ispa.LocalKV(k, v, 320, w, sink)
+    hist = oracle.LocalHistory(k.cpu().view(torch.int16).numpy(), v.cpu().view(torch.int16).numpy(), 320, w, sink)
+    for i, n in enumerate((64, 100, 250, 64)):
+        _, kn, vn = synth.chunk_qkv(33 + i, 0, 0, 1, n, H * d, DEV)
+        kv.append(kn, vn)
+        hist.append(kn.cpu().view(torch.int16).numpy(), vn.cpu().view(torch.int16).numpy())
+        torch.cuda.synchronize()
+        k_ref, v_ref = hist.rows()
+        assert kv.rows == k_ref.shape[0]
+        # the ring holds the local set, in ring order: compare the row multisets
+        # and the sink rows in place
+        kk, vv = bits(kv.k[: kv.rows]), bits(kv.v[: kv.rows])
+        assert np.array_equal(_sorted_rows(kk), _sorted_rows(k_ref))
+        assert np.array_equal(_sorted_rows(np.concatenate([kk, vv], 1)),
+                              _sorted_rows(np.concatenate([k_ref, v_ref], 1)))
+        assert np.array_equal(kk[:kv.sink], k_ref[:kv.sink])
+
+
+def test_attention_over_the_ring():
+    # an L-Layer after eviction: each new chunk is appended, then its queries
+    # attend to everything the layer holds; the reference is plain attention
+    # over the local set of the whole sequence (Eq. 7)
+    H, d, w, s, n = 2, 128, 1000, 64, 300
+    _, k, v = synth.chunk_qkv(40, 0, 0, 1, 2000, H * d, DEV)
+    kv = ispa.LocalKV(k, v, 2000, w, s)
+    k_all, v_all = k.cpu(), v.cpu()
+    for i in range(3):
+        q, kn, vn = synth.chunk_qkv(41 + i, 0, 0, n, n, H * d, DEV)
+        kv.append(kn, vn)
+        k_all = torch.cat([k_all, kn.cpu()])
+        v_all = torch.cat([v_all, vn.cpu()])
+        out, lse = kv.attend(q, H)
+        torch.cuda.synchronize()
+        N = k_all.shape[0]
+        ref = oracle.chunk_attention(f64(q), f64(k_all), f64(v_all), N, w, H, sink_len=s, branches=("local",))
+        assert_attn(f64(out), ref["local"][0], f"ring chunk {i}")
+        assert_lse(f64(lse), ref["local"][1], f"ring chunk {i} lse")
