@@ -43,6 +43,7 @@ from .absorb import (
     feasibility_direct,
     select_layers,
     inject,
+    project,
 )
 from .kvcache import evict_local, LocalHistory
 from .budget import kv_retained_fraction, n_local_layers
@@ -62,6 +63,7 @@ __all__ = [
     "feasibility_direct",
     "select_layers",
     "inject",
+    "project",
     "evict_local",
     "LocalHistory",
     "kv_retained_fraction",

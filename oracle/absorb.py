@@ -10,7 +10,9 @@ Definitions followed (arXiv 2607.00712):
 * Sec. 3.2, last paragraph: the method only sums A_loc^T A_loc and A_loc^T R
   over the warmup rows and solves one D x D system at the end of warmup.
 * Sec. 3.3: layers are ranked by eps ascending and the K lowest become
-  L-Layers; each of them takes W_new = W + dW in place.
+  L-Layers; each of them takes W_new = W + dW in place and from then on
+  projects its local attention output with it: Y = A_loc W_new (Sec. 3.1
+  step 3).
 
 Readings where the paper is silent (each listed in the design doc):
 
@@ -166,3 +168,14 @@ def inject(W, dW, transposed=False):
     if W.shape != d.shape:
         raise ValueError("weight and dW shapes differ")
     return (W + d).astype(np.float32)
+
+
+def project(a, w, transposed=False):
+    """The output projection Y = A W of Eq. 4 (Sec. 3.1 step 3 with W_new).
+
+    ``a`` [n, D_in]; ``w`` [D_in, D_out], or with ``transposed`` the
+    linear-layer weight [D_out, D_in] (Y = A W^T). float64.
+    """
+    a = np.asarray(a, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    return a @ (w.T if transposed else w)

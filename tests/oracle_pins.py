@@ -410,6 +410,22 @@ def pin_inject(inject, bf16_round):
     assert bf16_round(inject(one, np.full((1, 1), 3 * 2.0 ** -9, np.float32)))[0, 0] == 1.0 + 2.0 ** -7
 
 
+def pin_project(project):
+    # hand example, both weight layouts
+    a = np.array([[1.0, 2.0, 0.5]])
+    w = np.array([[1.0, 0.0], [0.0, 1.0], [2.0, -2.0]])        # [D_in = 3, D_out = 2]
+    assert np.array_equal(project(a, w), np.array([[2.0, 1.0]]))
+    assert np.array_equal(project(a, w.T.copy(), transposed=True), np.array([[2.0, 1.0]]))
+    # identity weight, and agreement with an explicit triple loop
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((5, 4))
+    assert np.array_equal(project(x, np.eye(4)), x)
+    m = rng.standard_normal((4, 3))
+    loop = np.array([[sum(x[i, k] * m[k, j] for k in range(4)) for j in range(3)] for i in range(5)])
+    assert np.allclose(project(x, m), loop, rtol=1e-14, atol=1e-14)
+    assert np.allclose(project(x, m.T.copy(), transposed=True), loop, rtol=1e-14, atol=1e-14)
+
+
 def pin_evict_local(evict_local):
     rows = np.arange(10, dtype=np.float32)[:, None] * np.ones((1, 4), np.float32)
     k, v = evict_local(rows, -rows, 10, 3, 2)

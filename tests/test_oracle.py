@@ -92,6 +92,10 @@ def test_inject():
     P.pin_inject(oracle.inject, oracle.bf16_round)
 
 
+def test_project():
+    P.pin_project(oracle.project)
+
+
 def test_evict_local():
     P.pin_evict_local(oracle.evict_local)
 

@@ -47,6 +47,7 @@ def absorb_pins(m):
         lambda: P.pin_feasibility(m.Stats, m.solve_modulation, m.feasibility, m.feasibility_direct, m.residual),
         lambda: P.pin_select_layers(m.select_layers),
         lambda: P.pin_inject(m.inject, m.bf16_round),
+        lambda: P.pin_project(m.project),
     ]
 
 
@@ -89,6 +90,7 @@ MUTATIONS = [
     ("oracle.absorb", "self.s += float(np.sum(r * r))", "self.s += float(np.sum(np.abs(r)))", absorb_pins),
     ("oracle.absorb", "        d = d.T", "        pass", absorb_pins),
     ("oracle.absorb", "return (W + d).astype(np.float32)", "return (W - d).astype(np.float32)", absorb_pins),
+    ("oracle.absorb", "return a @ (w.T if transposed else w)", "return a @ (w if transposed else w.T)", absorb_pins),
     # kvcache
     ("oracle.kvcache", "return k[local], v[local]", "return k[local], k[local]", kvcache_pins),
     ("oracle.kvcache", "k = np.concatenate(self.k, axis=0)", "k = self.k[-1]", kvcache_pins),
