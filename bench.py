@@ -161,11 +161,18 @@ def absorb_run(ispa, w, k, v, dw, dev, reps=10):
             torch.empty((w["sink"] + w["window"], D), dtype=torch.bfloat16, device=dev))
     ev = timed(lambda: ispa.LocalKV(k, v, w["cache_len"], w["window"], w["sink"], ring=ring))
     rows = ispa.LocalKV(k, v, w["cache_len"], w["window"], w["sink"], ring=ring).rows
+    # the L-Layer's output projection of one chunk with the modulated weight
+    a = k[: w["n_q"]]
+    y = torch.empty((w["n_q"], D), dtype=torch.bfloat16, device=dev)
+    pj = timed(lambda: ispa.project(a, weight, out=y))
     inj_bytes = D * D * (2 + 4 + 2)
     ev_bytes = rows * D * 2 * 2 * 2
+    pj_flop = 2.0 * w["n_q"] * D * D
     return {"inject_ms": round(inj, 4), "inject_gbs": round(inj_bytes / inj / 1e6, 1),
             "evict_ms": round(ev, 4), "evict_gbs": round(ev_bytes / ev / 1e6, 1),
-            "hbm_peak_gbs": PEAK_HBM_GBS}
+            "hbm_peak_gbs": PEAK_HBM_GBS,
+            "project_ms": round(pj, 4), "project_tflops": round(pj_flop / pj / 1e9, 1),
+            "project_frac": round(pj_flop / pj / 1e9 / PEAK_BF16_TFLOPS, 4)}
 
 
 def hbm_copy(steps, warmup, nbytes=1 << 30):

@@ -13,8 +13,8 @@
  *   ispa_solve_modulation  dW = (G + lambda I)^-1 C and the feasibility score
  *                          eps (Sec. 3.2, Eq. 5-6)
  * and the layer absorption that follows warmup (Sec. 3.3): ranking by eps,
- * the in-place weight update W + dW, and the L-Layer cache after the
- * permanent eviction of the history.
+ * the in-place weight update W + dW, the L-Layer cache after the permanent
+ * eviction of the history, and the L-Layer's output projection.
  *
  * Conventions shared by every call
  *   - Matrices are row-major with the last dimension contiguous.
@@ -294,6 +294,21 @@ int ispa_kv_evict(const void* k_cache, const void* v_cache, int64_t cache_len, i
  */
 int ispa_kv_ring_append(void* k_ring, void* v_ring, int64_t sink_rows, int64_t window, int64_t head,
                         const void* k_new, const void* v_new, int64_t n_new, int32_t hidden, hipStream_t stream);
+
+/*
+ * The output projection an L-Layer applies after absorption (Sec. 3.1 step 3
+ * with W_new = W + dW of Sec. 3.3; Y = A W of Eq. 4), in the linear-layer
+ * layout of the weight: y = a weight^T.
+ *   a        device bf16 [n_rows, d_in] (the attention output, heads concatenated)
+ *   weight   device bf16 [d_out, d_in] (e.g. after ispa_inject_modulation with
+ *            transposed != 0)
+ *   y        device [n_rows, d_out] of y_dtype (ISPA_DTYPE_F32 or ISPA_DTYPE_BF16,
+ *            rounded to nearest even); must not overlap a or weight
+ *   d_in     a multiple of 32; fp32 accumulation
+ * a and weight 16-byte aligned. Asynchronous on `stream`.
+ */
+int ispa_project(const void* a, const void* weight, int64_t n_rows, int32_t d_in, int32_t d_out, void* y,
+                 int32_t y_dtype, hipStream_t stream);
 
 #ifdef __cplusplus
 }

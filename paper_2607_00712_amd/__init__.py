@@ -11,6 +11,7 @@ works without the library, but every call raises if it is not built.
     attn_merge(out_a, lse_a, out_b, lse_b) -> (out, lse)
     select_layers(eps, k) -> indices;  inject_modulation(weight, delta_w, transposed)
     LocalKV(k_cache, v_cache, cache_len, window, sink_len): evict, append, attend
+    project(a, weight, out_dtype) -> a @ weight^T  (the L-Layer's output projection)
     Stats(d_in, d_out, max_rows).accum(x, y_full, y_local)
     Stats.solve(lam) -> (delta_w, eps)
 """
@@ -21,7 +22,7 @@ import os
 import torch
 
 __all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "status_string",
-           "select_layers", "inject_modulation", "LocalKV",
+           "select_layers", "inject_modulation", "LocalKV", "project",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
            "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
 
@@ -55,6 +56,7 @@ _SIGNATURES = {
     "ispa_kv_evict": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_p, _c_p, ctypes.POINTER(_c_i64),
                                      _c_p]),
     "ispa_kv_ring_append": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i32, _c_p]),
+    "ispa_project": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i32, _c_i32, _c_p, _c_i32, _c_p]),
     "ispa_stats_workspace_bytes": (_c_sz, [_c_i32, _c_i32, _c_i64]),
     "ispa_stats_create": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_p, _c_sz, _c_i32, _c_i32, _c_i64, _c_p]),
     "ispa_stats_reset": (ctypes.c_int, [_c_p]),
@@ -417,3 +419,25 @@ class LocalKV:
         chunk first: the keys of the current chunk are part of its local set)."""
         n = self.rows
         return attn_chunk(q, self.k, self.v, n, n, n_heads, **kw)
+
+
+def project(a, weight, out=None, out_dtype=torch.float32):
+    """y = a weight^T with weight in the linear-layer layout [d_out, d_in] (ispa_project)."""
+    L = lib()
+    _require(a, "a", torch.bfloat16)
+    _require(weight, "weight", torch.bfloat16, a.device)
+    n, d_in = a.shape
+    d_out, k = weight.shape
+    if k != d_in:
+        raise ValueError("weight must be [d_out, d_in] with the d_in of a")
+    if out is None:
+        out = torch.empty((n, d_out), dtype=out_dtype, device=a.device)
+    if out.dtype not in _DT:
+        raise TypeError("out must be fp32 or bf16")
+    _require(out, "out", out.dtype, a.device)
+    if tuple(out.shape) != (n, d_out):
+        raise ValueError(f"out must have shape {(n, d_out)}")
+    st = L.ispa_project(_ptr(a), _ptr(weight), int(n), int(d_in), int(d_out), _ptr(out), _DT[out.dtype],
+                        _stream(a.device))
+    _check(st, "ispa_project")
+    return out

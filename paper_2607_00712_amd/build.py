@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libispa.so")
 
-SOURCES = ["ispa_abi.cpp", "attn_chunk.hip", "stats.hip", "solve.hip", "absorb.hip"]
+SOURCES = ["ispa_abi.cpp", "attn_chunk.hip", "stats.hip", "solve.hip", "absorb.hip", "project.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

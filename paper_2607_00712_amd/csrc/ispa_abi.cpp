@@ -415,4 +415,25 @@ int ispa_kv_ring_append(void* k_ring, void* v_ring, int64_t sink_rows, int64_t w
              : ISPA_ERR_HIP;
 }
 
+
+int ispa_project(const void* a, const void* weight, int64_t n_rows, int32_t d_in, int32_t d_out, void* y,
+                 int32_t y_dtype, hipStream_t stream) {
+  if (y_dtype != ISPA_DTYPE_BF16 && y_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (!a || !weight || !y) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(a) || !aligned16(weight) || ((uintptr_t)y & 3u)) return ISPA_ERR_INVALID_ARG;
+  if (n_rows < 1 || n_rows > ((int64_t)1 << 31) || d_in < 32 || d_in % 32 != 0 || d_in > 65536 || d_out < 1 ||
+      d_out > 65536)
+    return ISPA_ERR_INVALID_ARG;
+  const size_t ybytes = (size_t)n_rows * d_out * (y_dtype == ISPA_DTYPE_BF16 ? 2 : 4);
+  auto overlap = [](const void* p, size_t np, const void* q, size_t nq) {
+    return (const char*)p < (const char*)q + nq && (const char*)q < (const char*)p + np;
+  };
+  if (overlap(y, ybytes, a, (size_t)n_rows * d_in * 2) || overlap(y, ybytes, weight, (size_t)d_out * d_in * 2))
+    return ISPA_ERR_INVALID_ARG;
+  return ispa::launch_project(a, weight, n_rows, d_in, d_out, y, y_dtype == ISPA_DTYPE_BF16, ispa::attn_cu_count(),
+                              stream) == hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
+}
+
 }  // extern "C"

@@ -98,6 +98,12 @@ hipError_t launch_inject(void* W, int dtype, bool transposed, const float* dW, i
 hipError_t launch_kv_copy(const void* k_src, const void* v_src, void* k_dst, void* v_dst, int64_t row_bytes,
                           const int64_t* src, const int64_t* dst, const int64_t* n, int n_seg, hipStream_t stream);
 
+// ---- projection (project.hip) ----
+// y = a w^T: a bf16 [n, d_in], w bf16 [d_out, d_in], y fp32 or bf16 [n, d_out];
+// d_in a multiple of 32
+hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
+                          int n_cu, hipStream_t stream);
+
 // ---- solve (solve.hip) ----
 struct SolveWork {
   float* L;          // [d, d] factor (lower triangle)

@@ -1,0 +1,273 @@
+// Output projection of an L-Layer for gfx950 (CDNA4).
+//
+// Operation (arXiv 2607.00712, Sec. 3.1 step 3 with Eq. 4): after absorption an
+// L-Layer projects its local attention output with the modulated weight,
+// Y = A W_new. The weight is taken in the linear-layer layout W_lin = W_new^T
+// [d_out, d_in] (the layout ispa_inject_modulation updates with dW^T), so
+// Y = A W_lin^T and both operands have the contraction dimension contiguous.
+//
+// proj_kernel (bf16 MFMA 32x32x16, fp32 accumulation): output tile 256 rows x
+// TN columns (TN = 256 or 128, whichever fills the chip better), 8 waves (two
+// per SIMD); wave w owns rows 64 (w / 2) .. +63 and columns (TN / 2)(w % 2) ..
+// +TN/2 - 1. Stages of 32 k go HBM -> LDS by direct buffer loads into a ring of
+// 4 buffers, 3 stages ahead of the MFMAs, one barrier per stage. LDS rows are
+// 64 bytes (four 16-byte chunks of 8 k); the chunk index is XOR-swizzled with
+// (row / 4) mod 4 so that each 16-lane group of an operand read (16
+// consecutive rows, one chunk) covers all 64 banks. Rows past n_rows or d_out
+// read as zero through the buffer descriptors and are never stored.
+#include "ispa_internal.h"
+
+namespace ispa {
+namespace {
+
+constexpr int kPThreads = 512;
+constexpr int kPM = 256;          // tile rows (rows of A)
+constexpr int kPK = 32;           // k per stage
+constexpr int kPRing = 4;         // stage buffers
+constexpr int kPRowBytes = kPK * 2;
+
+template <int TN>
+struct PCfg {
+  static constexpr int sideA = kPM * kPRowBytes;
+  static constexpr int sideB = TN * kPRowBytes;
+  static constexpr int stage = sideA + sideB;
+  static constexpr int loadsA = sideA / (kPThreads * 16);
+  static constexpr int loadsB = sideB / (kPThreads * 16);
+  static constexpr int loads = loadsA + loadsB;  // direct loads per thread per stage
+  static constexpr int nb = TN / 64;             // 32-column blocks per wave
+};
+
+struct ProjArgs {
+  const uint16_t* a;  // [n, d_in]
+  const uint16_t* w;  // [d_out, d_in]
+  void* y;            // [n, d_out], fp32 or bf16
+  int64_t n;
+  int d_in, d_out;
+  int tiles_m, tiles_n;
+  int y_bf16;
+};
+
+__device__ __forceinline__ int pswz(int row) { return (row >> 2) & 3; }
+__device__ __forceinline__ uint32_t p_lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(ISPA_LDS const void*)p;
+}
+__device__ __forceinline__ f32x16 p_mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+template <int N>
+__device__ __forceinline__ void p_vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
+
+// Direct loads of one side of a stage: rows [row0, row0 + NL * 128) x k
+// [k0, k0 + 32) of a row-major bf16 matrix (ld), rows >= rows_end zero. Load q
+// of wave w covers 16-byte slot (q * 8 + w) * 64 + lane: row = slot / 4,
+// stored chunk = slot % 4.
+template <int NL>
+__device__ __forceinline__ void p_stage_side(const uint16_t* src, int64_t ld, int64_t row0, int64_t rows_end, int k0,
+                                             char* dst, int wave, int lane) {
+  int64_t nrec = rows_end > row0 ? ((rows_end - row0 - 1) * ld) * 2 + kPRowBytes : 0;
+  if (nrec > 0x7fffffff) nrec = 0x7fffffff;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src + row0 * ld + k0), 0, (int)nrec, 0x00020000);
+#pragma unroll
+  for (int q = 0; q < NL; ++q) {
+    const int slot = (q * 8 + wave) * 64 + lane;
+    const int row = slot >> 2;
+    const int c = (slot & 3) ^ pswz(row);
+    const int voff = (int)((row * ld + c * 8) * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * 8 + wave) * 1024), 16, voff, 0, 0, 0);
+  }
+}
+
+// Operand read addresses of this lane for stage buffer 0: [block][k-slice].
+template <int TN>
+struct PAddr {
+  uint32_t a[2][2];
+  uint32_t b[PCfg<TN>::nb][2];
+};
+template <int TN>
+__device__ __forceinline__ void p_addr(PAddr<TN>& ad, uint32_t base, int wr, int wc, int lane) {
+  const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = 64 * wr + 32 * i + r;
+      ad.a[i][ks] = base + row * kPRowBytes + (((2 * ks + h) ^ pswz(row)) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < PCfg<TN>::nb; ++j) {
+      const int row = (TN / 2) * wc + 32 * j + r;
+      ad.b[j][ks] = base + PCfg<TN>::sideA + row * kPRowBytes + (((2 * ks + h) ^ pswz(row)) << 4);
+    }
+  }
+}
+
+// The operand reads of one 16-k slice (inline asm: through the builtin the
+// compiler would also wait for the direct loads filling other buffers).
+template <int TN, int IMM>
+__device__ __forceinline__ void p_issue(const PAddr<TN>& ad, int ks, u32x4 (&ra)[2], u32x4 (&rb)[PCfg<TN>::nb]) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(ra[i]) : "v"(ad.a[i][ks]), "i"(IMM));
+#pragma unroll
+  for (int j = 0; j < PCfg<TN>::nb; ++j)
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(rb[j]) : "v"(ad.b[j][ks]), "i"(IMM));
+}
+__device__ __forceinline__ void p_wait0(u32x4 (&ra)[2], u32x4 (&rb)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(ra[0]), "+v"(ra[1]), "+v"(rb[0]), "+v"(rb[1]), "+v"(rb[2]), "+v"(rb[3]));
+}
+__device__ __forceinline__ void p_wait0(u32x4 (&ra)[2], u32x4 (&rb)[2]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(ra[0]), "+v"(ra[1]), "+v"(rb[0]), "+v"(rb[1]));
+}
+
+template <int TN>
+struct PTile {
+  int64_t row0;  // rows of A / Y
+  int col0;      // rows of W / columns of Y
+  int steps, wave, lane;
+};
+
+template <int TN>
+__device__ __forceinline__ void p_load(const ProjArgs& a, const PTile<TN>& t, char* smem, int s) {
+  char* d = smem + (s % kPRing) * PCfg<TN>::stage;
+  p_stage_side<PCfg<TN>::loadsA>(a.a, a.d_in, t.row0, a.n, s * kPK, d, t.wave, t.lane);
+  p_stage_side<PCfg<TN>::loadsB>(a.w, a.d_in, t.col0, a.d_out, s * kPK, d + PCfg<TN>::sideA, t.wave, t.lane);
+}
+
+// Stage s from ring buffer BUF: loads of stage s + 3, the 2 x nb x 2 MFMAs of
+// this wave, then wait for stage s + 1 and synchronise. Buffers 2 and 3 use
+// the second address set (LDS offsets are 16-bit immediates).
+template <int TN, int BUF>
+__device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN>& t, char* smem, const PAddr<TN>& ad,
+                                        f32x16 (&acc)[2][PCfg<TN>::nb], int s) {
+  using C = PCfg<TN>;
+  constexpr int kOff = (BUF & 1) * C::stage;
+  if (s + 3 < t.steps) p_load<TN>(a, t, smem, s + 3);
+  u32x4 ra[2], rb[C::nb];
+  p_issue<TN, kOff>(ad, 0, ra, rb);
+  p_wait0(ra, rb);
+  bf16x8 af[2], bf[C::nb];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) af[i] = __builtin_bit_cast(bf16x8, ra[i]);
+#pragma unroll
+  for (int j = 0; j < C::nb; ++j) bf[j] = __builtin_bit_cast(bf16x8, rb[j]);
+  p_issue<TN, kOff>(ad, 1, ra, rb);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = p_mfma(af[i], bf[j], acc[i][j]);
+  p_wait0(ra, rb);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) af[i] = __builtin_bit_cast(bf16x8, ra[i]);
+#pragma unroll
+  for (int j = 0; j < C::nb; ++j) bf[j] = __builtin_bit_cast(bf16x8, rb[j]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = p_mfma(af[i], bf[j], acc[i][j]);
+  // stage s + 1 must have landed; stages s + 2 and s + 3 may still be in flight
+  const int younger = t.steps - (s + 2);
+  if (younger >= 2) {
+    p_vm_wait<2 * C::loads>();
+  } else if (younger == 1) {
+    p_vm_wait<C::loads>();
+  } else {
+    p_vm_wait<0>();
+  }
+  __builtin_amdgcn_s_barrier();
+}
+
+template <int TN>
+__global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) void proj_kernel(ProjArgs a) {
+  using C = PCfg<TN>;
+  __shared__ __attribute__((aligned(1024))) char smem[kPRing * C::stage];
+  // XCD-aware order: each XCD takes a contiguous run of tiles (row panels of A
+  // shared through its L2)
+  const int n_items = a.tiles_m * a.tiles_n;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+  if (item >= n_items) return;
+  PTile<TN> t;
+  t.row0 = (int64_t)(item / a.tiles_n) * kPM;
+  t.col0 = (item % a.tiles_n) * TN;
+  t.lane = threadIdx.x & 63;
+  t.wave = threadIdx.x >> 6;
+  t.steps = a.d_in / kPK;
+  const int wr = t.wave >> 1, wc = t.wave & 1;
+  const uint32_t lds0 = p_lds_addr(smem);
+  PAddr<TN> ad, ad2;
+  p_addr<TN>(ad, lds0, wr, wc, t.lane);
+  p_addr<TN>(ad2, lds0 + 2 * C::stage, wr, wc, t.lane);
+
+  f32x16 acc[2][C::nb];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = f32x16{};
+
+  for (int s = 0; s < 3 && s < t.steps; ++s) p_load<TN>(a, t, smem, s);
+  if (t.steps >= 3) {
+    p_vm_wait<2 * C::loads>();
+  } else if (t.steps == 2) {
+    p_vm_wait<C::loads>();
+  } else {
+    p_vm_wait<0>();
+  }
+  __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
+  for (int s = 0; s < t.steps; s += kPRing) {
+    p_stage<TN, 0>(a, t, smem, ad, acc, s);
+    if (s + 1 < t.steps) p_stage<TN, 1>(a, t, smem, ad, acc, s + 1);
+    if (s + 2 < t.steps) p_stage<TN, 2>(a, t, smem, ad2, acc, s + 2);
+    if (s + 3 < t.steps) p_stage<TN, 3>(a, t, smem, ad2, acc, s + 3);
+  }
+
+  // lane holds column (lane % 32) and rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each block
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < C::nb; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t orow = t.row0 + 64 * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
+        const int ocol = t.col0 + (TN / 2) * wc + 32 * j + (t.lane & 31);
+        if (orow < a.n && ocol < a.d_out) {
+          if (a.y_bf16)
+            ((__bf16*)a.y)[orow * a.d_out + ocol] = (__bf16)acc[i][j][r];
+          else
+            ((float*)a.y)[orow * a.d_out + ocol] = acc[i][j][r];
+        }
+      }
+}
+
+}  // namespace
+
+hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
+                          int n_cu, hipStream_t stream) {
+  ProjArgs p;
+  p.a = (const uint16_t*)a;
+  p.w = (const uint16_t*)w;
+  p.y = y;
+  p.n = n;
+  p.d_in = d_in;
+  p.d_out = d_out;
+  p.y_bf16 = y_bf16;
+  p.tiles_m = (int)((n + kPM - 1) / kPM);
+  // the tile width that leaves the fewest idle workgroup slots in the last round
+  const int n256 = p.tiles_m * ((d_out + 255) / 256), n128 = p.tiles_m * ((d_out + 127) / 128);
+  const int cu = n_cu > 0 ? n_cu : 256;
+  const double f256 = (double)n256 / (cu * ((n256 + cu - 1) / cu));
+  const double f128 = (double)n128 / (cu * ((n128 + cu - 1) / cu));
+  const bool wide = f256 >= f128;
+  p.tiles_n = wide ? (d_out + 255) / 256 : (d_out + 127) / 128;
+  const int items = p.tiles_m * p.tiles_n;
+  const int grid = (items + 7) / 8 * 8;
+  if (wide)
+    hipLaunchKernelGGL(proj_kernel<256>, dim3(grid), dim3(kPThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(proj_kernel<128>, dim3(grid), dim3(kPThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace ispa

@@ -101,3 +101,44 @@ def test_attention_over_the_ring():
         ref = oracle.chunk_attention(f64(q), f64(k_all), f64(v_all), N, w, H, sink_len=s, branches=("local",))
         assert_attn(f64(out), ref["local"][0], f"ring chunk {i}")
         assert_lse(f64(lse), ref["local"][1], f"ring chunk {i} lse")
+
+
+# the L-Layer's output projection y = a W^T (W in the linear-layer layout),
+# fp32 accumulation: compared with the fp64 oracle on the same bf16 operands
+@pytest.mark.parametrize("shape", [(64, 128, 64), (300, 256, 200), (4680, 1536, 1536), (777, 5120, 640),
+                                   (1, 32, 8)])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_projection(shape, out_dtype):
+    n, d_in, d_out = shape
+    g = torch.Generator().manual_seed(n + d_in + d_out)
+    a = torch.randn((n, d_in), generator=g).to(torch.bfloat16)
+    w = (torch.randn((d_out, d_in), generator=g) / d_in ** 0.5).to(torch.bfloat16)
+    y = ispa.project(a.to(DEV), w.to(DEV), out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    ref = oracle.project(f64(a), f64(w), transposed=True)
+    # fp32 accumulation: |err| <= d_in * 2^-24 * sum_k |a_k w_k| (a loose bound);
+    # bf16 output adds half an ulp of the result
+    scale = np.abs(f64(a)) @ np.abs(f64(w)).T
+    tol = d_in * 2.0 ** -24 * scale
+    if out_dtype == torch.bfloat16:
+        tol = tol + 2.0 ** -8 * np.abs(ref)
+    err = np.abs(f64(y) - ref)
+    assert np.all(err <= tol + 1e-30), f"max excess {np.max(err - tol):.3e}"
+
+
+def test_absorbed_layer_projection():
+    # dW injected into a bf16 linear weight, then the projection: equals the
+    # oracle's A (W + dW) on the rounded weight
+    n, d = 500, 256
+    g = torch.Generator().manual_seed(77)
+    a = torch.randn((n, d), generator=g).to(torch.bfloat16)
+    w = (torch.randn((d, d), generator=g) / 16).to(torch.bfloat16)      # [d_out, d_in]
+    dw = torch.randn((d, d), generator=g) * 0.01                         # [d_in, d_out]
+    w_dev = w.to(DEV)
+    ispa.inject_modulation(w_dev, dw.to(DEV), transposed=True)
+    y = ispa.project(a.to(DEV), w_dev)
+    torch.cuda.synchronize()
+    w_new = oracle.bf16_round(oracle.inject(w.float().numpy(), dw.numpy(), transposed=True))
+    ref = oracle.project(f64(a), w_new, transposed=True)
+    scale = np.abs(f64(a)) @ np.abs(w_new.astype(np.float64)).T
+    assert np.all(np.abs(f64(y) - ref) <= d * 2.0 ** -24 * scale + 1e-30)
