@@ -18,6 +18,7 @@ follows:
   Sec. 3.3).
 * ``kvcache``    -- what an L-Layer's cache holds after the permanent
   eviction (Sec. 3.3; the local set of Eq. 7 as chunks keep arriving).
+* ``w8a8``       -- int8 quantisation of the linear layers (Sec. 4, Fig. 7).
 * ``budget``     -- KV-cache accounting for a given L-Layer budget
   (Sec. 4, Table 1/2 "KVCache" column; K = xN).
 
@@ -46,6 +47,7 @@ from .absorb import (
     project,
 )
 from .kvcache import evict_local, LocalHistory
+from .w8a8 import quantize_rows, dequantize_rows, project_w8a8
 from .budget import kv_retained_fraction, n_local_layers
 
 __all__ = [
@@ -66,6 +68,9 @@ __all__ = [
     "project",
     "evict_local",
     "LocalHistory",
+    "quantize_rows",
+    "dequantize_rows",
+    "project_w8a8",
     "kv_retained_fraction",
     "n_local_layers",
 ]

@@ -426,6 +426,39 @@ def pin_project(project):
     assert np.allclose(project(x, m.T.copy(), transposed=True), loop, rtol=1e-14, atol=1e-14)
 
 
+def pin_quantize_rows(quantize_rows, dequantize_rows):
+    q, s = quantize_rows(np.array([[1.0, -2.0, 0.5, 127.0]], np.float32))
+    assert list(q[0]) == [1, -2, 0, 127] and s[0] == 1.0          # 0.5 rounds to even 0
+    q, s = quantize_rows(np.array([[2.5, 3.5, -2.5, 127.0]], np.float32))
+    assert list(q[0]) == [2, 4, -2, 127]                           # half to even, both signs
+    q, s = quantize_rows(np.array([[-254.0, 1.0], [0.0, 0.0]], np.float32))
+    assert list(q[0]) == [-127, 0] and s[0] == 2.0                 # 1 / 2 = 0.5 -> 0
+    assert list(q[1]) == [0, 0] and s[1] == 1.0                    # all-zero row
+    # every code within half a step of its value, and the absmax maps to +-127
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal((6, 50)) * rng.uniform(0.01, 100, (6, 1))).astype(np.float32)
+    q, s = quantize_rows(x)
+    err = np.abs(dequantize_rows(q, s).astype(np.float64) - x)
+    assert np.all(err <= 0.5 * s[:, None] * (1 + 1e-6))
+    assert np.all(np.max(np.abs(q.astype(np.int32)), axis=1) == 127)
+
+
+def pin_project_w8a8(project_w8a8):
+    qa = np.array([[1, -2, 3], [127, 0, -127]], np.int8)
+    qw = np.array([[1, 1, 1], [2, 0, -1]], np.int8)               # [d_out = 2, d_in = 3]
+    sa = np.array([1.0, 0.5], np.float32)
+    sw = np.array([2.0, 0.25], np.float32)
+    want = np.array([[2 * 2.0, -1 * 0.25], [0 * 0.5 * 2.0, 381 * 0.5 * 0.25]], np.float32)
+    assert np.array_equal(project_w8a8(qa, sa, qw, sw), want)
+    # a loop over the codes
+    rng = np.random.default_rng(6)
+    a = rng.integers(-127, 128, (4, 9)).astype(np.int8)
+    w = rng.integers(-127, 128, (3, 9)).astype(np.int8)
+    one = np.ones(4, np.float32), np.ones(3, np.float32)
+    loop = [[sum(int(a[i, k]) * int(w[j, k]) for k in range(9)) for j in range(3)] for i in range(4)]
+    assert np.array_equal(project_w8a8(a, one[0], w, one[1]), np.array(loop, np.float32))
+
+
 def pin_evict_local(evict_local):
     rows = np.arange(10, dtype=np.float32)[:, None] * np.ones((1, 4), np.float32)
     k, v = evict_local(rows, -rows, 10, 3, 2)

@@ -96,6 +96,14 @@ def test_project():
     P.pin_project(oracle.project)
 
 
+def test_quantize_rows():
+    P.pin_quantize_rows(oracle.quantize_rows, oracle.dequantize_rows)
+
+
+def test_project_w8a8():
+    P.pin_project_w8a8(oracle.project_w8a8)
+
+
 def test_evict_local():
     P.pin_evict_local(oracle.evict_local)
 

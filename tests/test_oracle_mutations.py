@@ -51,6 +51,11 @@ def absorb_pins(m):
     ]
 
 
+def w8a8_pins(m):
+    return [lambda: P.pin_quantize_rows(m.quantize_rows, m.dequantize_rows),
+            lambda: P.pin_project_w8a8(m.project_w8a8)]
+
+
 def kvcache_pins(m):
     return [lambda: P.pin_evict_local(m.evict_local),
             lambda: P.pin_local_history(m.LocalHistory)]
@@ -91,6 +96,14 @@ MUTATIONS = [
     ("oracle.absorb", "        d = d.T", "        pass", absorb_pins),
     ("oracle.absorb", "return (W + d).astype(np.float32)", "return (W - d).astype(np.float32)", absorb_pins),
     ("oracle.absorb", "return a @ (w.T if transposed else w)", "return a @ (w if transposed else w.T)", absorb_pins),
+    # w8a8
+    ("oracle.w8a8", "q = np.rint((x / scale[:, None]).astype(np.float32))",
+     "q = np.floor((x / scale[:, None]).astype(np.float32) + 0.5)", w8a8_pins),
+    ("oracle.w8a8", "(amax / np.float32(127.0))", "(amax / np.float32(128.0))", w8a8_pins),
+    ("oracle.w8a8", "acc = np.asarray(qa, dtype=np.int64) @ np.asarray(qw, dtype=np.int64).T",
+     "acc = np.asarray(qa, dtype=np.int64) @ np.asarray(qw, dtype=np.int64).T[:, ::-1]", w8a8_pins),
+    ("oracle.w8a8", "y = acc.astype(np.float32) * np.asarray(sa, dtype=np.float32)[:, None]",
+     "y = acc.astype(np.float32)", w8a8_pins),
     # kvcache
     ("oracle.kvcache", "return k[local], v[local]", "return k[local], k[local]", kvcache_pins),
     ("oracle.kvcache", "k = np.concatenate(self.k, axis=0)", "k = self.k[-1]", kvcache_pins),
@@ -118,7 +131,8 @@ def test_planted_mistake_is_caught(module_name, old, new, pins):
 
 def test_unmutated_copies_pass():
     for name, pins in (("oracle.attention", attention_pins), ("oracle.absorb", absorb_pins),
-                       ("oracle.kvcache", kvcache_pins), ("oracle.budget", budget_pins)):
+                       ("oracle.kvcache", kvcache_pins), ("oracle.w8a8", w8a8_pins),
+                       ("oracle.budget", budget_pins)):
         m = mutant(name, "\"\"\"", "\"\"\"")
         for pin in pins(m):
             pin()
