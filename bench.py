@@ -41,6 +41,7 @@ WORKLOADS = {
 }
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
+PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA
 PEAK_HBM_GBS = 8000.0
 
 # HBM bytes of one dual-stream attention call (the attention kernel plus the
@@ -165,6 +166,13 @@ def absorb_run(ispa, w, k, v, dw, dev, reps=10):
     a = k[: w["n_q"]]
     y = torch.empty((w["n_q"], D), dtype=torch.bfloat16, device=dev)
     pj = timed(lambda: ispa.project(a, weight, out=y))
+    # its W8A8 form (Sec. 4): per-token codes of the chunk's activations, then
+    # the int8 projection with per-channel weight codes
+    qa = torch.empty((w["n_q"], D), dtype=torch.int8, device=dev)
+    sa = torch.empty((w["n_q"],), dtype=torch.float32, device=dev)
+    qw, sw = ispa.quantize_rows(weight)
+    qt = timed(lambda: ispa.quantize_rows(a, q=qa, scale=sa))
+    pj8 = timed(lambda: ispa.project_w8a8(qa, sa, qw, sw, out=y))
     inj_bytes = D * D * (2 + 4 + 2)
     ev_bytes = rows * D * 2 * 2 * 2
     pj_flop = 2.0 * w["n_q"] * D * D
@@ -172,7 +180,10 @@ def absorb_run(ispa, w, k, v, dw, dev, reps=10):
             "evict_ms": round(ev, 4), "evict_gbs": round(ev_bytes / ev / 1e6, 1),
             "hbm_peak_gbs": PEAK_HBM_GBS,
             "project_ms": round(pj, 4), "project_tflops": round(pj_flop / pj / 1e9, 1),
-            "project_frac": round(pj_flop / pj / 1e9 / PEAK_BF16_TFLOPS, 4)}
+            "project_frac": round(pj_flop / pj / 1e9 / PEAK_BF16_TFLOPS, 4),
+            "quantize_ms": round(qt, 4), "quantize_gbs": round(w["n_q"] * D * (2 + 1) / qt / 1e6, 1),
+            "project_w8a8_ms": round(pj8, 4), "project_w8a8_tops": round(pj_flop / pj8 / 1e9, 1),
+            "project_w8a8_frac": round(pj_flop / pj8 / 1e9 / PEAK_INT8_TOPS, 4)}
 
 
 def hbm_copy(steps, warmup, nbytes=1 << 30):

@@ -310,6 +310,39 @@ int ispa_kv_ring_append(void* k_ring, void* v_ring, int64_t sink_rows, int64_t w
 int ispa_project(const void* a, const void* weight, int64_t n_rows, int32_t d_in, int32_t d_out, void* y,
                  int32_t y_dtype, hipStream_t stream);
 
+/*
+ * Symmetric per-row int8 quantisation for the W8A8 form of the linear layers
+ * (Sec. 4 combines the method with W8A8 and reports it compatible; the scheme
+ * is not stated there): for each row, scale = absmax / 127 (1 for an all-zero
+ * row) and code = clamp(round_half_even(x / scale), -127, 127), the division
+ * and the rounding in IEEE fp32.
+ *   x       device [rows, cols] of x_dtype (ISPA_DTYPE_BF16 or ISPA_DTYPE_F32),
+ *           finite values, 16-byte aligned; rows are activations (one scale
+ *           per token) or the rows of a linear weight [d_out, d_in] (one
+ *           scale per output channel)
+ *   q       device int8 [rows, cols], 8-byte aligned
+ *   scale   device fp32 [rows]
+ *   cols    a multiple of 8
+ * q and scale must not overlap x or each other. Asynchronous on `stream`.
+ */
+int ispa_quantize_rows(const void* x, int32_t x_dtype, int64_t rows, int32_t cols, int8_t* q, float* scale,
+                       hipStream_t stream);
+
+/*
+ * The W8A8 form of ispa_project: y = (q_a q_w^T) * scale_a[row] * scale_w[col]
+ * with the codes of ispa_quantize_rows; the product is exact in int32 and the
+ * dequantisation is fp32(acc) * scale_a, then * scale_w, one fp32 rounding
+ * each (and one more to bf16 for a bf16 y).
+ *   q_a, scale_a   device int8 [n_rows, d_in] and fp32 [n_rows]
+ *   q_w, scale_w   device int8 [d_out, d_in] and fp32 [d_out]
+ *   y              device [n_rows, d_out] of y_dtype (ISPA_DTYPE_F32 or
+ *                  ISPA_DTYPE_BF16); must not overlap the inputs
+ *   d_in           a multiple of 64, at most 65536 (no int32 overflow)
+ * q_a and q_w 16-byte aligned. Asynchronous on `stream`.
+ */
+int ispa_project_w8a8(const int8_t* q_a, const float* scale_a, const int8_t* q_w, const float* scale_w, int64_t n_rows,
+                      int32_t d_in, int32_t d_out, void* y, int32_t y_dtype, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

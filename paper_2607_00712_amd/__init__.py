@@ -22,7 +22,7 @@ import os
 import torch
 
 __all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "status_string",
-           "select_layers", "inject_modulation", "LocalKV", "project",
+           "select_layers", "inject_modulation", "LocalKV", "project", "quantize_rows", "project_w8a8",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
            "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
 
@@ -57,6 +57,8 @@ _SIGNATURES = {
                                      _c_p]),
     "ispa_kv_ring_append": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i32, _c_p]),
     "ispa_project": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i32, _c_i32, _c_p, _c_i32, _c_p]),
+    "ispa_quantize_rows": (ctypes.c_int, [_c_p, _c_i32, _c_i64, _c_i32, _c_p, _c_p, _c_p]),
+    "ispa_project_w8a8": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_p, _c_i64, _c_i32, _c_i32, _c_p, _c_i32, _c_p]),
     "ispa_stats_workspace_bytes": (_c_sz, [_c_i32, _c_i32, _c_i64]),
     "ispa_stats_create": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_p, _c_sz, _c_i32, _c_i32, _c_i64, _c_p]),
     "ispa_stats_reset": (ctypes.c_int, [_c_p]),
@@ -440,4 +442,51 @@ def project(a, weight, out=None, out_dtype=torch.float32):
     st = L.ispa_project(_ptr(a), _ptr(weight), int(n), int(d_in), int(d_out), _ptr(out), _DT[out.dtype],
                         _stream(a.device))
     _check(st, "ispa_project")
+    return out
+
+
+def quantize_rows(x, q=None, scale=None):
+    """Symmetric per-row int8 codes and fp32 scales of x [rows, cols], bf16 or
+    fp32 (ispa_quantize_rows). Returns (q, scale)."""
+    L = lib()
+    if not isinstance(x, torch.Tensor) or x.dtype not in _DT:
+        raise TypeError("x must be a bf16 or fp32 torch.Tensor")
+    _require(x, "x", x.dtype)
+    rows, cols = x.shape
+    if q is None:
+        q = torch.empty((rows, cols), dtype=torch.int8, device=x.device)
+    if scale is None:
+        scale = torch.empty((rows,), dtype=torch.float32, device=x.device)
+    _require(q, "q", torch.int8, x.device)
+    _require(scale, "scale", torch.float32, x.device, ndim=1)
+    if tuple(q.shape) != (rows, cols) or scale.shape[0] != rows:
+        raise ValueError("q must be [rows, cols] and scale [rows]")
+    st = L.ispa_quantize_rows(_ptr(x), _DT[x.dtype], int(rows), int(cols), _ptr(q), _ptr(scale), _stream(x.device))
+    _check(st, "ispa_quantize_rows")
+    return q, scale
+
+
+def project_w8a8(q_a, scale_a, q_w, scale_w, out=None, out_dtype=torch.float32):
+    """y = (q_a q_w^T) * scale_a[row] * scale_w[col] (ispa_project_w8a8): the
+    W8A8 form of project, with the codes of quantize_rows."""
+    L = lib()
+    _require(q_a, "q_a", torch.int8)
+    dev = q_a.device
+    _require(q_w, "q_w", torch.int8, dev)
+    _require(scale_a, "scale_a", torch.float32, dev, ndim=1)
+    _require(scale_w, "scale_w", torch.float32, dev, ndim=1)
+    n, d_in = q_a.shape
+    d_out, k = q_w.shape
+    if k != d_in or scale_a.shape[0] != n or scale_w.shape[0] != d_out:
+        raise ValueError("q_w must be [d_out, d_in], scale_a [n] and scale_w [d_out]")
+    if out is None:
+        out = torch.empty((n, d_out), dtype=out_dtype, device=dev)
+    if out.dtype not in _DT:
+        raise TypeError("out must be fp32 or bf16")
+    _require(out, "out", out.dtype, dev)
+    if tuple(out.shape) != (n, d_out):
+        raise ValueError(f"out must have shape {(n, d_out)}")
+    st = L.ispa_project_w8a8(_ptr(q_a), _ptr(scale_a), _ptr(q_w), _ptr(scale_w), int(n), int(d_in), int(d_out),
+                             _ptr(out), _DT[out.dtype], _stream(dev))
+    _check(st, "ispa_project_w8a8")
     return out

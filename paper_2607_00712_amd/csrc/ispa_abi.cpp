@@ -19,6 +19,11 @@ constexpr size_t kWsAlign = 256;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// byte ranges [p, p + np) and [q, q + nq) intersect
+bool overlaps(const void* p, size_t np, const void* q, size_t nq) {
+  return (const char*)p < (const char*)q + nq && (const char*)q < (const char*)p + np;
+}
+
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Workspace layout of a statistics handle (offsets in bytes, 256-aligned).
@@ -77,7 +82,7 @@ const char* ispa_status_string(int status) {
   }
 }
 
-int ispa_abi_version(void) { return 101; }
+int ispa_abi_version(void) { return 102; }
 
 }  // extern "C"
 
@@ -425,13 +430,44 @@ int ispa_project(const void* a, const void* weight, int64_t n_rows, int32_t d_in
       d_out > 65536)
     return ISPA_ERR_INVALID_ARG;
   const size_t ybytes = (size_t)n_rows * d_out * (y_dtype == ISPA_DTYPE_BF16 ? 2 : 4);
-  auto overlap = [](const void* p, size_t np, const void* q, size_t nq) {
-    return (const char*)p < (const char*)q + nq && (const char*)q < (const char*)p + np;
-  };
-  if (overlap(y, ybytes, a, (size_t)n_rows * d_in * 2) || overlap(y, ybytes, weight, (size_t)d_out * d_in * 2))
+  if (overlaps(y, ybytes, a, (size_t)n_rows * d_in * 2) || overlaps(y, ybytes, weight, (size_t)d_out * d_in * 2))
     return ISPA_ERR_INVALID_ARG;
   return ispa::launch_project(a, weight, n_rows, d_in, d_out, y, y_dtype == ISPA_DTYPE_BF16, ispa::attn_cu_count(),
                               stream) == hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
+}
+
+int ispa_quantize_rows(const void* x, int32_t x_dtype, int64_t rows, int32_t cols, int8_t* q, float* scale,
+                       hipStream_t stream) {
+  if (x_dtype != ISPA_DTYPE_BF16 && x_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (!x || !q || !scale) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(x) || ((uintptr_t)q & 7u) || ((uintptr_t)scale & 3u)) return ISPA_ERR_INVALID_ARG;
+  if (rows < 1 || rows > ((int64_t)1 << 31) || cols < 8 || cols % 8 != 0) return ISPA_ERR_INVALID_ARG;
+  const size_t xb = (size_t)rows * cols * (x_dtype == ISPA_DTYPE_F32 ? 4 : 2), qb = (size_t)rows * cols,
+               sb = (size_t)rows * 4;
+  if (overlaps(q, qb, x, xb) || overlaps(scale, sb, x, xb) || overlaps(q, qb, scale, sb)) return ISPA_ERR_INVALID_ARG;
+  return ispa::launch_quantize_rows(x, x_dtype == ISPA_DTYPE_BF16, rows, cols, q, scale, stream) == hipSuccess
+             ? ISPA_OK
+             : ISPA_ERR_HIP;
+}
+
+int ispa_project_w8a8(const int8_t* q_a, const float* scale_a, const int8_t* q_w, const float* scale_w, int64_t n_rows,
+                      int32_t d_in, int32_t d_out, void* y, int32_t y_dtype, hipStream_t stream) {
+  if (y_dtype != ISPA_DTYPE_BF16 && y_dtype != ISPA_DTYPE_F32) return ISPA_ERR_UNSUPPORTED;
+  if (!q_a || !scale_a || !q_w || !scale_w || !y) return ISPA_ERR_INVALID_ARG;
+  if (!aligned16(q_a) || !aligned16(q_w) || ((uintptr_t)y & 3u) || ((uintptr_t)scale_a & 3u) ||
+      ((uintptr_t)scale_w & 3u))
+    return ISPA_ERR_INVALID_ARG;
+  if (n_rows < 1 || n_rows > ((int64_t)1 << 31) || d_in < 64 || d_in % 64 != 0 || d_in > 65536 || d_out < 1 ||
+      d_out > 65536)
+    return ISPA_ERR_INVALID_ARG;
+  const size_t ybytes = (size_t)n_rows * d_out * (y_dtype == ISPA_DTYPE_BF16 ? 2 : 4);
+  if (overlaps(y, ybytes, q_a, (size_t)n_rows * d_in) || overlaps(y, ybytes, q_w, (size_t)d_out * d_in) ||
+      overlaps(y, ybytes, scale_a, (size_t)n_rows * 4) || overlaps(y, ybytes, scale_w, (size_t)d_out * 4))
+    return ISPA_ERR_INVALID_ARG;
+  return ispa::launch_project_w8a8(q_a, scale_a, q_w, scale_w, n_rows, d_in, d_out, y, y_dtype == ISPA_DTYPE_BF16,
+                                   ispa::attn_cu_count(), stream) == hipSuccess
              ? ISPA_OK
              : ISPA_ERR_HIP;
 }

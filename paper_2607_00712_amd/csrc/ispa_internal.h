@@ -103,6 +103,14 @@ hipError_t launch_kv_copy(const void* k_src, const void* v_src, void* k_dst, voi
 // d_in a multiple of 32
 hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
                           int n_cu, hipStream_t stream);
+// W8A8: y = (qa qw^T) * sa[row] * sw[col]; qa int8 [n, d_in], qw int8
+// [d_out, d_in]; d_in a multiple of 64
+hipError_t launch_project_w8a8(const int8_t* qa, const float* sa, const int8_t* qw, const float* sw, int64_t n,
+                               int d_in, int d_out, void* y, int y_bf16, int n_cu, hipStream_t stream);
+// per-row int8 codes and scales of x (fp32 or bf16) [rows, cols]; cols a
+// multiple of 8, x 16-byte aligned
+hipError_t launch_quantize_rows(const void* x, int x_bf16, int64_t rows, int cols, int8_t* q, float* scale,
+                                hipStream_t stream);
 
 // ---- solve (solve.hip) ----
 struct SolveWork {

@@ -15,6 +15,13 @@
 // (row / 4) mod 4 so that each 16-lane group of an operand read (16
 // consecutive rows, one chunk) covers all 64 banks. Rows past n_rows or d_out
 // read as zero through the buffer descriptors and are never stored.
+//
+// The same kernel computes the W8A8 form (Sec. 4 pairs the method with int8
+// linear layers): int8 codes of A and W_lin, int8 MFMA 32x32x32 with int32
+// accumulation, 64 k per stage so that LDS rows stay 64 bytes, and the
+// dequantisation y = (float(acc) * s_a[row]) * s_w[col] in the epilogue.
+// quant_rows_kernel produces the codes: one wave per row, symmetric scale
+// absmax / 127, codes rint(x / scale) clamped to +-127.
 #include "ispa_internal.h"
 
 namespace ispa {
@@ -22,9 +29,8 @@ namespace {
 
 constexpr int kPThreads = 512;
 constexpr int kPM = 256;          // tile rows (rows of A)
-constexpr int kPK = 32;           // k per stage
+constexpr int kPRowBytes = 64;    // bytes of k per row per stage (32 bf16 or 64 int8)
 constexpr int kPRing = 4;         // stage buffers
-constexpr int kPRowBytes = kPK * 2;
 
 template <int TN>
 struct PCfg {
@@ -37,22 +43,45 @@ struct PCfg {
   static constexpr int nb = TN / 64;             // 32-column blocks per wave
 };
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
 struct ProjArgs {
-  const uint16_t* a;  // [n, d_in]
-  const uint16_t* w;  // [d_out, d_in]
+  const char* a;      // [n, d_in] bf16 or int8
+  const char* w;      // [d_out, d_in] bf16 or int8
+  const float* sa;    // int8 only: [n] scales of the rows of a
+  const float* sw;    // int8 only: [d_out] scales of the rows of w
   void* y;            // [n, d_out], fp32 or bf16
   int64_t n;
-  int d_in, d_out;
+  int ld;             // bytes per row of a and w
+  int d_out;
   int tiles_m, tiles_n;
   int y_bf16;
+};
+
+// bf16 x bf16 -> fp32 or int8 x int8 -> int32, 32x32 output blocks; both
+// operands take 16 bytes of k per lane with the same k order, so one LDS
+// layout serves both
+template <bool I8>
+struct PMath {
+  using acc_t = f32x16;
+  static __device__ __forceinline__ acc_t mma(u32x4 a, u32x4 b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  }
+};
+template <>
+struct PMath<true> {
+  using acc_t = i32x16;
+  static __device__ __forceinline__ acc_t mma(u32x4 a, u32x4 b, acc_t c) {
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0,
+                                                 0, 0);
+  }
 };
 
 __device__ __forceinline__ int pswz(int row) { return (row >> 2) & 3; }
 __device__ __forceinline__ uint32_t p_lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(ISPA_LDS const void*)p;
-}
-__device__ __forceinline__ f32x16 p_mfma(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 template <int N>
 __device__ __forceinline__ void p_vm_wait() {
@@ -60,23 +89,23 @@ __device__ __forceinline__ void p_vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
 }
 
-// Direct loads of one side of a stage: rows [row0, row0 + NL * 128) x k
-// [k0, k0 + 32) of a row-major bf16 matrix (ld), rows >= rows_end zero. Load q
-// of wave w covers 16-byte slot (q * 8 + w) * 64 + lane: row = slot / 4,
-// stored chunk = slot % 4.
+// Direct loads of one side of a stage: rows [row0, row0 + NL * 128) x bytes
+// [k0, k0 + 64) of a row-major matrix (ld bytes per row), rows >= rows_end
+// zero. Load q of wave w covers 16-byte slot (q * 8 + w) * 64 + lane: row =
+// slot / 4, stored chunk = slot % 4.
 template <int NL>
-__device__ __forceinline__ void p_stage_side(const uint16_t* src, int64_t ld, int64_t row0, int64_t rows_end, int k0,
+__device__ __forceinline__ void p_stage_side(const char* src, int64_t ld, int64_t row0, int64_t rows_end, int k0,
                                              char* dst, int wave, int lane) {
-  int64_t nrec = rows_end > row0 ? ((rows_end - row0 - 1) * ld) * 2 + kPRowBytes : 0;
+  int64_t nrec = rows_end > row0 ? (rows_end - row0 - 1) * ld + kPRowBytes : 0;
   if (nrec > 0x7fffffff) nrec = 0x7fffffff;
   const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src + row0 * ld + k0), 0, (int)nrec, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(src + row0 * ld + k0), 0, (int)nrec, 0x00020000);
 #pragma unroll
   for (int q = 0; q < NL; ++q) {
     const int slot = (q * 8 + wave) * 64 + lane;
     const int row = slot >> 2;
     const int c = (slot & 3) ^ pswz(row);
-    const int voff = (int)((row * ld + c * 8) * 2);
+    const int voff = (int)(row * ld + c * 16);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * 8 + wave) * 1024), 16, voff, 0, 0, 0);
   }
 }
@@ -105,7 +134,7 @@ __device__ __forceinline__ void p_addr(PAddr<TN>& ad, uint32_t base, int wr, int
   }
 }
 
-// The operand reads of one 16-k slice (inline asm: through the builtin the
+// The operand reads of one 32-byte k slice (inline asm: through the builtin the
 // compiler would also wait for the direct loads filling other buffers).
 template <int TN, int IMM>
 __device__ __forceinline__ void p_issue(const PAddr<TN>& ad, int ks, u32x4 (&ra)[2], u32x4 (&rb)[PCfg<TN>::nb]) {
@@ -132,41 +161,36 @@ struct PTile {
 template <int TN>
 __device__ __forceinline__ void p_load(const ProjArgs& a, const PTile<TN>& t, char* smem, int s) {
   char* d = smem + (s % kPRing) * PCfg<TN>::stage;
-  p_stage_side<PCfg<TN>::loadsA>(a.a, a.d_in, t.row0, a.n, s * kPK, d, t.wave, t.lane);
-  p_stage_side<PCfg<TN>::loadsB>(a.w, a.d_in, t.col0, a.d_out, s * kPK, d + PCfg<TN>::sideA, t.wave, t.lane);
+  p_stage_side<PCfg<TN>::loadsA>(a.a, a.ld, t.row0, a.n, s * kPRowBytes, d, t.wave, t.lane);
+  p_stage_side<PCfg<TN>::loadsB>(a.w, a.ld, t.col0, a.d_out, s * kPRowBytes, d + PCfg<TN>::sideA, t.wave, t.lane);
 }
 
 // Stage s from ring buffer BUF: loads of stage s + 3, the 2 x nb x 2 MFMAs of
 // this wave, then wait for stage s + 1 and synchronise. Buffers 2 and 3 use
 // the second address set (LDS offsets are 16-bit immediates).
-template <int TN, int BUF>
+template <int TN, bool I8, int BUF>
 __device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN>& t, char* smem, const PAddr<TN>& ad,
-                                        f32x16 (&acc)[2][PCfg<TN>::nb], int s) {
+                                        typename PMath<I8>::acc_t (&acc)[2][PCfg<TN>::nb], int s) {
   using C = PCfg<TN>;
   constexpr int kOff = (BUF & 1) * C::stage;
   if (s + 3 < t.steps) p_load<TN>(a, t, smem, s + 3);
-  u32x4 ra[2], rb[C::nb];
+  u32x4 ra[2], rb[C::nb], fa[2], fb[C::nb];
   p_issue<TN, kOff>(ad, 0, ra, rb);
   p_wait0(ra, rb);
-  bf16x8 af[2], bf[C::nb];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) af[i] = __builtin_bit_cast(bf16x8, ra[i]);
+  for (int i = 0; i < 2; ++i) fa[i] = ra[i];
 #pragma unroll
-  for (int j = 0; j < C::nb; ++j) bf[j] = __builtin_bit_cast(bf16x8, rb[j]);
+  for (int j = 0; j < C::nb; ++j) fb[j] = rb[j];
   p_issue<TN, kOff>(ad, 1, ra, rb);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < C::nb; ++j) acc[i][j] = p_mfma(af[i], bf[j], acc[i][j]);
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = PMath<I8>::mma(fa[i], fb[j], acc[i][j]);
   p_wait0(ra, rb);
-#pragma unroll
-  for (int i = 0; i < 2; ++i) af[i] = __builtin_bit_cast(bf16x8, ra[i]);
-#pragma unroll
-  for (int j = 0; j < C::nb; ++j) bf[j] = __builtin_bit_cast(bf16x8, rb[j]);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < C::nb; ++j) acc[i][j] = p_mfma(af[i], bf[j], acc[i][j]);
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = PMath<I8>::mma(ra[i], rb[j], acc[i][j]);
   // stage s + 1 must have landed; stages s + 2 and s + 3 may still be in flight
   const int younger = t.steps - (s + 2);
   if (younger >= 2) {
@@ -179,7 +203,7 @@ __device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN>& t, c
   __builtin_amdgcn_s_barrier();
 }
 
-template <int TN>
+template <int TN, bool I8>
 __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) void proj_kernel(ProjArgs a) {
   using C = PCfg<TN>;
   __shared__ __attribute__((aligned(1024))) char smem[kPRing * C::stage];
@@ -194,18 +218,18 @@ __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   t.col0 = (item % a.tiles_n) * TN;
   t.lane = threadIdx.x & 63;
   t.wave = threadIdx.x >> 6;
-  t.steps = a.d_in / kPK;
+  t.steps = a.ld / kPRowBytes;
   const int wr = t.wave >> 1, wc = t.wave & 1;
   const uint32_t lds0 = p_lds_addr(smem);
   PAddr<TN> ad, ad2;
   p_addr<TN>(ad, lds0, wr, wc, t.lane);
   p_addr<TN>(ad2, lds0 + 2 * C::stage, wr, wc, t.lane);
 
-  f32x16 acc[2][C::nb];
+  typename PMath<I8>::acc_t acc[2][C::nb];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < C::nb; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < C::nb; ++j) acc[i][j] = typename PMath<I8>::acc_t{};
 
   for (int s = 0; s < 3 && s < t.steps; ++s) p_load<TN>(a, t, smem, s);
   if (t.steps >= 3) {
@@ -217,43 +241,99 @@ __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   }
   __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
   for (int s = 0; s < t.steps; s += kPRing) {
-    p_stage<TN, 0>(a, t, smem, ad, acc, s);
-    if (s + 1 < t.steps) p_stage<TN, 1>(a, t, smem, ad, acc, s + 1);
-    if (s + 2 < t.steps) p_stage<TN, 2>(a, t, smem, ad2, acc, s + 2);
-    if (s + 3 < t.steps) p_stage<TN, 3>(a, t, smem, ad2, acc, s + 3);
+    p_stage<TN, I8, 0>(a, t, smem, ad, acc, s);
+    if (s + 1 < t.steps) p_stage<TN, I8, 1>(a, t, smem, ad, acc, s + 1);
+    if (s + 2 < t.steps) p_stage<TN, I8, 2>(a, t, smem, ad2, acc, s + 2);
+    if (s + 3 < t.steps) p_stage<TN, I8, 3>(a, t, smem, ad2, acc, s + 3);
   }
 
   // lane holds column (lane % 32) and rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each block
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < C::nb; ++j) {
+    const int ocol = t.col0 + (TN / 2) * wc + 32 * j + (t.lane & 31);
+    if (ocol >= a.d_out) continue;
+    const float scol = I8 ? a.sw[ocol] : 1.0f;
 #pragma unroll
-    for (int j = 0; j < C::nb; ++j)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t orow = t.row0 + 64 * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
-        const int ocol = t.col0 + (TN / 2) * wc + 32 * j + (t.lane & 31);
-        if (orow < a.n && ocol < a.d_out) {
-          if (a.y_bf16)
-            ((__bf16*)a.y)[orow * a.d_out + ocol] = (__bf16)acc[i][j][r];
+        if (orow < a.n) {
+          float v;
+          if constexpr (I8)
+            v = ((float)acc[i][j][r] * a.sa[orow]) * scol;
           else
-            ((float*)a.y)[orow * a.d_out + ocol] = acc[i][j][r];
+            v = acc[i][j][r];
+          if (a.y_bf16)
+            ((__bf16*)a.y)[orow * a.d_out + ocol] = (__bf16)v;
+          else
+            ((float*)a.y)[orow * a.d_out + ocol] = v;
         }
       }
+  }
+}
+
+// Codes and scale of one row per wave: pass 1 takes the absmax, pass 2
+// re-reads the row (from cache) and writes the codes, 8 values per lane per
+// iteration (cols a multiple of 8, rows 16-byte aligned).
+template <typename T>
+__global__ __launch_bounds__(256) void quant_rows_kernel(const T* __restrict__ x, int64_t rows, int cols,
+                                                         int8_t* __restrict__ q, float* __restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const T* xr = x + row * cols;
+  auto load8 = [&](int c, float (&v)[8]) {
+    if constexpr (sizeof(T) == 2) {
+      const u32x4 u = *(const u32x4*)(xr + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] = __uint_as_float(u[e] << 16);
+        v[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+      }
+    } else {
+      const f32x4 u0 = *(const f32x4*)(xr + c), u1 = *(const f32x4*)(xr + c + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = u0[e];
+        v[4 + e] = u1[e];
+      }
+    }
+  };
+  float m = 0.0f;
+  for (int c = lane * 8; c < cols; c += 512) {
+    float v[8];
+    load8(c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(v[e]));
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  const float s = m > 0.0f ? m / 127.0f : 1.0f;
+  if (lane == 0) scale[row] = s;
+  int8_t* qr = q + row * cols;
+  for (int c = lane * 8; c < cols; c += 512) {
+    float v[8];
+    load8(c, v);
+    u32x2 out;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float r = fminf(fmaxf(rintf(v[4 * h + e] / s), -127.0f), 127.0f);
+        word |= ((uint32_t)(int)r & 0xffu) << (8 * e);
+      }
+      out[h] = word;
+    }
+    *(u32x2*)(qr + c) = out;
+  }
 }
 
 }  // namespace
 
-hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
-                          int n_cu, hipStream_t stream) {
-  ProjArgs p;
-  p.a = (const uint16_t*)a;
-  p.w = (const uint16_t*)w;
-  p.y = y;
-  p.n = n;
-  p.d_in = d_in;
-  p.d_out = d_out;
-  p.y_bf16 = y_bf16;
-  p.tiles_m = (int)((n + kPM - 1) / kPM);
+static hipError_t launch_proj(ProjArgs p, bool i8, int d_out, int n_cu, hipStream_t stream) {
+  p.tiles_m = (int)((p.n + kPM - 1) / kPM);
   // the tile width that leaves the fewest idle workgroup slots in the last round
   const int n256 = p.tiles_m * ((d_out + 255) / 256), n128 = p.tiles_m * ((d_out + 127) / 128);
   const int cu = n_cu > 0 ? n_cu : 256;
@@ -263,10 +343,54 @@ hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int
   p.tiles_n = wide ? (d_out + 255) / 256 : (d_out + 127) / 128;
   const int items = p.tiles_m * p.tiles_n;
   const int grid = (items + 7) / 8 * 8;
-  if (wide)
-    hipLaunchKernelGGL(proj_kernel<256>, dim3(grid), dim3(kPThreads), 0, stream, p);
+  if (wide && i8)
+    hipLaunchKernelGGL((proj_kernel<256, true>), dim3(grid), dim3(kPThreads), 0, stream, p);
+  else if (wide)
+    hipLaunchKernelGGL((proj_kernel<256, false>), dim3(grid), dim3(kPThreads), 0, stream, p);
+  else if (i8)
+    hipLaunchKernelGGL((proj_kernel<128, true>), dim3(grid), dim3(kPThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL(proj_kernel<128>, dim3(grid), dim3(kPThreads), 0, stream, p);
+    hipLaunchKernelGGL((proj_kernel<128, false>), dim3(grid), dim3(kPThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
+                          int n_cu, hipStream_t stream) {
+  ProjArgs p{};
+  p.a = (const char*)a;
+  p.w = (const char*)w;
+  p.y = y;
+  p.n = n;
+  p.ld = d_in * 2;
+  p.d_out = d_out;
+  p.y_bf16 = y_bf16;
+  return launch_proj(p, false, d_out, n_cu, stream);
+}
+
+hipError_t launch_project_w8a8(const int8_t* qa, const float* sa, const int8_t* qw, const float* sw, int64_t n,
+                               int d_in, int d_out, void* y, int y_bf16, int n_cu, hipStream_t stream) {
+  ProjArgs p{};
+  p.a = (const char*)qa;
+  p.w = (const char*)qw;
+  p.sa = sa;
+  p.sw = sw;
+  p.y = y;
+  p.n = n;
+  p.ld = d_in;
+  p.d_out = d_out;
+  p.y_bf16 = y_bf16;
+  return launch_proj(p, true, d_out, n_cu, stream);
+}
+
+hipError_t launch_quantize_rows(const void* x, int x_bf16, int64_t rows, int cols, int8_t* q, float* scale,
+                                hipStream_t stream) {
+  const unsigned grid = (unsigned)((rows + 3) / 4);
+  if (x_bf16)
+    hipLaunchKernelGGL(quant_rows_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream, (const uint16_t*)x, rows, cols,
+                       q, scale);
+  else
+    hipLaunchKernelGGL(quant_rows_kernel<float>, dim3(grid), dim3(256), 0, stream, (const float*)x, rows, cols, q,
+                       scale);
   return hipGetLastError();
 }
 

@@ -38,7 +38,7 @@ def test_status_strings(L):
     for code in (0, -1, -2, -3, -4, -5):
         assert ispa.status_string(code).startswith("ISPA")
     assert "unknown" in ispa.status_string(7)
-    assert L.ispa_abi_version() == 101
+    assert L.ispa_abi_version() == 102
 
 
 def _attn(L, **kw):
@@ -144,3 +144,17 @@ def test_absorption_argument_errors(L):
     assert L.ispa_kv_evict(p(16), p(32), 10, 3, 0, 16, p(16), p(128), None, p(0)) == E  # ring == cache
     assert L.ispa_kv_ring_append(p(16), p(32), 0, 0, 0, p(64), p(128), 4, 16, p(0)) == E  # window 0
     assert L.ispa_kv_ring_append(p(16), p(32), 0, 4, -1, p(64), p(128), 4, 16, p(0)) == E
+    # projection and its W8A8 form: the host checks reject before any launch
+    assert L.ispa_project(p(256), p(512), 4, 48, 8, p(4096), 0, p(0)) == E             # d_in % 32
+    assert L.ispa_project(p(256), p(512), 4, 32, 8, p(4096), 5, p(0)) == U
+    assert L.ispa_project(p(256), p(512), 4, 32, 8, p(256), 1, p(0)) == E              # y overlaps a
+    assert L.ispa_quantize_rows(p(256), 3, 4, 16, p(4096), p(8192), p(0)) == U
+    assert L.ispa_quantize_rows(p(256), 0, 4, 12, p(4096), p(8192), p(0)) == E         # cols % 8
+    assert L.ispa_quantize_rows(p(264), 0, 4, 16, p(4096), p(8192), p(0)) == E         # x alignment
+    assert L.ispa_quantize_rows(p(256), 0, 4, 16, p(264), p(8192), p(0)) == E          # q overlaps x
+    assert L.ispa_quantize_rows(p(256), 0, 4, 16, p(4096), p(4100), p(0)) == E         # scale overlaps q
+    assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 96, 8, p(8192), 1, p(0)) == E  # d_in % 64
+    assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 64, 8, p(8192), 2, p(0)) == U
+    assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 64, 8, p(2048), 1, p(0)) == E  # y over q_w
+    assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 0, 64, 8, p(8192), 1, p(0)) == E  # no rows
+    assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 65600, 8, p(1 << 40), 1, p(0)) == E
