@@ -18,9 +18,9 @@
 //   never overwritten (other workgroups of the same launch read them); their
 //   inverses go to Dinv.
 // Factor + inverse of one 64 x 64 block (one wave, the others wait): 32 x 32
-//   sub-blocks, each factored right-looking with a row per lane in registers
-//   and the column multipliers broadcast through LDS, then inverted
-//   column-wise; the off-diagonal pieces are 32 x 32 x 32 MFMA products.
+//   sub-blocks, each reduced in registers with the pivot row broadcast by
+//   readlane, the inverse formed in the same instructions by the other half of
+//   the wave; the off-diagonal pieces are 32 x 32 x 32 MFMA products.
 // Triangular solves in block LDL^T form over 256-blocks (details below): the
 //   inverses X_I of the 256 x 256 diagonal blocks of L and P_I = X_I^T X_I,
 //   Lh = L diag(X_I) below the 256-block diagonal (its transpose mirrored into
@@ -117,110 +117,97 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Scratch of one 32 x 32 factorisation: the current column's multipliers,
-// aligned for 16-byte broadcast reads, and a dense copy of the factor.
-struct F32Scratch {
-  float col[32];
-  float Ld[32][32];
-};
-
-// One wave: factor the 32 x 32 block S[o..o+31][o..o+31] (lower part) in place
-// (zero above) and write its inverse, lower triangular, to M[o..][o..].
-// Right-looking, a row per lane (lanes 32..63 mirror 0..31): at step j lane i
-// keeps a[m] = A[i][j + m] in registers; the multipliers l_cj of column j are
-// broadcast through LDS (lane c writes its l_cj at col[c - j - 1], everybody
-// reads col[0..31] with 16-byte loads) and the update shifts the row by one, so
-// register indices stay static inside a compact loop. Pivots use the hardware
-// square root and reciprocal (about 1 ulp). The inverse is formed column-wise
-// (a column per lane) from the dense copy of the factor. Sets *bad on a
-// non-positive pivot.
-__device__ void factor32(Tile& S, Tile& M, int o, int lane, int* bad, F32Scratch& w) {
+// One wave: factor the 32 x 32 SPD block S[o..o+31][o..o+31] (lower part
+// valid) into L, in place with zeros above the diagonal, and write L^-1 (lower
+// triangular) to M[o..][o..]. No LDS traffic inside the elimination:
+//   lanes 0..31   x = row i of the symmetric matrix being reduced,
+//   lanes 32..63  x = column i - 32 of the inverse being formed by forward
+//                 substitution, starting from the unit vector.
+// At step j the pivot p_j = (row j)[j] and s_c = (row j)[c] = (column j)[c]
+// (symmetry) come from lane j by readlane, and both kinds of lane apply the
+// same update x[c] -= (x[j] / p_j) s_c for c > j: the Schur complement for a
+// row, the substitution step m_c -= L_cj m_j / L_jj for an inverse column.
+// Afterwards L[i][j] = x[j] / sqrt(p_j) (j < i), L[i][i] = sqrt(p_i) and
+// L^-1[r][col] = x[r] / sqrt(p_r). Hardware square root and reciprocal (about
+// 1 ulp). Sets *bad on a non-positive pivot (then replaced by 1).
+__device__ __forceinline__ void factor32(Tile& S, Tile& M, int o, int lane, int* bad) {
   const int i = lane & 31;
   const bool lo = lane < 32;
-  float a[32];
+  float x[32];
 #pragma unroll
-  for (int c = 0; c < 32; ++c) a[c] = S[o + i][o + c];
+  for (int c = 0; c < 32; ++c) {
+    float v = S[o + max(i, c)][o + min(i, c)];
+    asm volatile("" : "+v"(v));  // every lane loads: no branch around the read
+    x[c] = lo ? v : (c == i ? 1.f : 0.f);
+  }
+  float lj[32];
   int neg = 0;
+#pragma unroll
   for (int j = 0; j < 32; ++j) {
-    float piv = readlane_f(a[0], j);
+    float piv = readlane_f(x[j], j);
     neg |= !(piv > 0.f);
     piv = piv > 0.f ? piv : 1.f;
-    const float ljj = __builtin_amdgcn_sqrtf(piv);
-    const float lij = i > j ? a[0] * __builtin_amdgcn_rcpf(ljj) : (i == j ? ljj : 0.f);
-    if (lo) {
-      w.Ld[i][j] = lij;
-      if (i > j) w.col[i - j - 1] = lij;
-    }
-    wave_sync();
-    float cb[32];
+    lj[j] = piv;
+    // the pivot row first (independent readlanes), then the updates
+    float sr[32];
 #pragma unroll
-    for (int m = 0; m < 32; m += 4) {
-      const f32x4 v = *(const f32x4*)(&w.col[m]);
-      cb[m] = v[0];
-      cb[m + 1] = v[1];
-      cb[m + 2] = v[2];
-      cb[m + 3] = v[3];
-    }
-    // a[m] <- A[i][j + 1 + m] - l_ij l_{j+1+m, j}; entries past column 31 are
-    // stale but never reach a[0]
+    for (int c = j + 1; c < 32; ++c) sr[c] = readlane_f(x[c], j);
+    const float coef = x[j] * __builtin_amdgcn_rcpf(piv);
 #pragma unroll
-    for (int m = 0; m < 31; ++m) a[m] = fmaf(-lij, cb[m], a[m + 1]);
-    a[31] = 0.f;
-    wave_sync();
+    for (int c = j + 1; c < 32; ++c) x[c] = fmaf(-coef, sr[c], x[c]);
   }
   if (neg && lane == 0) *bad = 1;
-  // factor back into S (zero above the diagonal)
-  if (lo) {
+  // one store per element: row i of L for lanes 0..31, column i of L^-1 for the rest
+  float* dst = lo ? &S[o + i][o] : &M[o][o + i];
+  const int step = lo ? 1 : kLd;
 #pragma unroll
-    for (int c = 0; c < 32; ++c) S[o + i][o + c] = w.Ld[i][c];
-  }
-  wave_sync();
-  // inverse: lane j owns column j; M[r][j] = (d_rj - sum_{p<r} L_rp M_pj) / L_rr
-  const int j = i;
-  float m[32];
-#pragma unroll
-  for (int r = 0; r < 32; ++r) {
-    float acc = r == j ? 1.f : 0.f;
-#pragma unroll
-    for (int p = 0; p < r; ++p) acc = fmaf(-w.Ld[r][p], m[p], acc);
-    m[r] = acc * __builtin_amdgcn_rcpf(w.Ld[r][r]);
-  }
-  if (lo) {
-#pragma unroll
-    for (int r = 0; r < 32; ++r) M[o + r][o + j] = m[r];
+  for (int c = 0; c < 32; ++c) {
+    const float l = __builtin_amdgcn_sqrtf(lj[c]);
+    const float v = x[c] * __builtin_amdgcn_rcpf(l);
+    dst[c * step] = lo ? (c < i ? v : (c == i ? l : 0.f)) : (c >= i ? v : 0.f);
   }
   wave_sync();
 }
 
-// Factor the 64 x 64 SPD block in S (lower part valid) into L (in place, zero
-// above) and write L^-1 to M. All threads call; wave 0 works.
-__device__ void factor64(Tile& S, Tile& M, Tile& T, int nb, int* bad, F32Scratch& w) {
+// Factor the 64 x 64 SPD block in S (lower part valid, zero above) into L (in
+// place) and write L^-1 to M; T is scratch. All threads call; wave 0 factors.
+// With P given, waves 1..3 meanwhile apply P -= Q R^T (the panel block's own
+// rank-64 update, independent of the factor), quadrant q on wave 1 + q % 3.
+__device__ void factor64(Tile& S, Tile& M, Tile& T, int nb, int* bad, Tile* P, const Tile* Q, const Tile* R) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // a ragged last block: identity beyond nb keeps the factorisation defined
-  for (int e = threadIdx.x; e < kNb * kNb; e += kThreads) {
-    const int r = e >> 6, c = e & 63;
-    if (r >= nb || c >= nb) S[r][c] = r == c ? 1.f : 0.f;
-    M[r][c] = 0.f;
+  if (nb < kNb) {
+    for (int e = threadIdx.x; e < kNb * kNb; e += kThreads) {
+      const int r = e >> 6, c = e & 63;
+      if (r >= nb || c >= nb) S[r][c] = r == c ? 1.f : 0.f;
+    }
   }
+  // the quadrant of L^-1 above the diagonal; factor32 writes the other three
+  for (int e = threadIdx.x; e < 32 * 32; e += kThreads) M[e >> 5][32 + (e & 31)] = 0.f;
   __syncthreads();
   if (wave == 0) {
-    factor32(S, M, 0, lane, bad, w);
-    // L10 = S10 . M00^T
-    f32x16 acc = {};
-    mma<false, true>(acc, S, 32, 0, M, 0, 0, 32, lane);
-    wave_sync();
+    // one copy of the (large, unrolled) 32 x 32 factor: S00, then S11
+#pragma nounroll
+    for (int o = 0; o < kNb; o += 32) {
+      if (o > 0) {
+        // L10 = S10 . M00^T
+        f32x16 acc = {};
+        mma<false, true>(acc, S, 32, 0, M, 0, 0, 32, lane);
+        wave_sync();
 #pragma unroll
-    for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][lane & 31] = acc[r];
-    wave_sync();
-    // S11 -= L10 . L10^T
-    acc = f32x16{};
-    mma<false, true>(acc, S, 32, 0, S, 32, 0, 32, lane);
+        for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][lane & 31] = acc[r];
+        wave_sync();
+        // S11 -= L10 . L10^T
+        acc = f32x16{};
+        mma<false, true>(acc, S, 32, 0, S, 32, 0, 32, lane);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][32 + (lane & 31)] -= acc[r];
-    wave_sync();
-    factor32(S, M, 32, lane, bad, w);
+        for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][32 + (lane & 31)] -= acc[r];
+        wave_sync();
+      }
+      factor32(S, M, o, lane, bad);
+    }
     // M10 = -M11 . L10 . M00 : T = L10 . M00, then M10 = -M11 . T
-    acc = f32x16{};
+    f32x16 acc = {};
     mma<false, false>(acc, S, 32, 0, M, 0, 0, 32, lane);
 #pragma unroll
     for (int r = 0; r < 16; ++r) T[acc_row(r, lane)][lane & 31] = acc[r];
@@ -229,6 +216,14 @@ __device__ void factor64(Tile& S, Tile& M, Tile& T, int nb, int* bad, F32Scratch
     mma<false, false>(acc, M, 32, 32, T, 0, 0, 32, lane);
 #pragma unroll
     for (int r = 0; r < 16; ++r) M[32 + acc_row(r, lane)][lane & 31] = -acc[r];
+  } else if (P) {
+    for (int q = wave - 1; q < 4; q += 3) {
+      const int r0 = (q >> 1) * 32, c0 = (q & 1) * 32;
+      f32x16 acc = {};
+      mma<false, true>(acc, *Q, r0, 0, *R, c0, 0, kNb, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) (*P)[r0 + acc_row(r, lane)][c0 + (lane & 31)] -= acc[r];
+    }
   }
   __syncthreads();
 }
@@ -277,8 +272,7 @@ __global__ void solve_init_kernel(const float* G, float* L, const float* C, floa
 
 // Cholesky launch k: trailing lower block triangle from block k+1.
 __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int* status) {
-  __shared__ Tile S, M, T, U, V;
-  __shared__ __attribute__((aligned(16))) F32Scratch fw;
+  __shared__ Tile S, M, T, U, V, P;
   __shared__ int bad;
   const int nblk = (n + kNb - 1) / kNb;
   int ti, tj;
@@ -322,30 +316,29 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   }
   put(S, fs);
   if (k >= 0) put(V, fv);
+  if (off) {
+    put(P, ft);
+    if (k >= 0) put(U, fu);
+  }
   __syncthreads();
   if (k >= 0) {
     quad_store(S, quad<false, true>(V, V), -1.f, true);
     __syncthreads();
   }
-  factor64(S, M, T, nd, &bad, fw);
+  // factor the diagonal block; an off-diagonal workgroup's other waves form
+  // A_rd - L_rk L_dk^T meanwhile
+  factor64(S, M, T, nd, &bad, off && k >= 0 ? &P : nullptr, &U, &V);
   if (!off) {
     store_tile(M, Dinv + (int64_t)d * kNb * kNb, kNb, kNb, kNb);
     if (threadIdx.x == 0 && bad) atomicOr(status, 1);
     return;
   }
   // L_rd = (A_rd - L_rk L_dk^T) . M^T
-  put(T, ft);
-  if (k >= 0) put(U, fu);
+  const f32x16 x = quad<false, true>(P, M);
   __syncthreads();
-  if (k >= 0) {
-    quad_store(T, quad<false, true>(U, V), -1.f, true);
-    __syncthreads();
-  }
-  const f32x16 x = quad<false, true>(T, M);
+  quad_store(P, x, 1.f, false);
   __syncthreads();
-  quad_store(T, x, 1.f, false);
-  __syncthreads();
-  store_tile(T, Lrt, n, rr, nd);
+  store_tile(P, Lrt, n, rr, nd);
 }
 
 // ---------------------------------------------------------------- 256-block
