@@ -62,6 +62,32 @@ __device__ __forceinline__ void mma(f32x16& acc, const float (*A)[kLd], int a0, 
 // accumulator element r of lane l sits at (row, col) of the 32 x 32 quadrant
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// 16 x 16 pieces (v_mfma_f32_16x16x4f32): lane l supplies A[l % 16][k + l / 16]
+// and B[k + l / 16][l % 16]; accumulator element r of lane l sits at row
+// 4 (l / 16) + r, column l % 16.
+// acc = op(A)[a0 .., ak ..] op(B)[bk .., b0 ..] over K, same conventions as mma.
+template <bool TA, bool TB, int K>
+__device__ __forceinline__ f32x4 mma16(const float (*A)[kLd], int a0, int ak, const float (*B)[kLd], int b0, int bk,
+                                       int lane) {
+  const int i = lane & 15, kq = lane >> 4;
+  f32x4 acc = {};
+#pragma unroll
+  for (int k = 0; k < K; k += 4) {
+    const float a = TA ? A[ak + k + kq][a0 + i] : A[a0 + i][ak + k + kq];
+    const float b = TB ? B[b0 + i][bk + k + kq] : B[bk + k + kq][b0 + i];
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+  }
+  return acc;
+}
+// D[r0 ..][c0 ..] (16 x 16) = sign * acc, or += sign * acc
+__device__ __forceinline__ void put16(Tile& D, int r0, int c0, const f32x4& acc, float sign, bool add, int lane) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float& d = D[r0 + 4 * (lane >> 4) + r][c0 + (lane & 15)];
+    d = add ? d + sign * acc[r] : sign * acc[r];
+  }
+}
+
 // A 64 x 64 block of a row-major matrix (ld) in flight: four 16-byte pieces per
 // thread. Rows >= rows_ok or cols >= cols_ok read as zero (ragged last block).
 // Row starts are 16-byte aligned and cols_ok is a multiple of 4 (dimensions are
@@ -185,37 +211,10 @@ __device__ void factor64(Tile& S, Tile& M, Tile& T, int nb, int* bad, Tile* P, c
   // the quadrant of L^-1 above the diagonal; factor32 writes the other three
   for (int e = threadIdx.x; e < 32 * 32; e += kThreads) M[e >> 5][32 + (e & 31)] = 0.f;
   __syncthreads();
+  // the 32 x 32 products below are split over the four waves, 16 x 16 each
+  const int qr = 16 * (wave >> 1), qc = 16 * (wave & 1);
   if (wave == 0) {
-    // one copy of the (large, unrolled) 32 x 32 factor: S00, then S11
-#pragma nounroll
-    for (int o = 0; o < kNb; o += 32) {
-      if (o > 0) {
-        // L10 = S10 . M00^T
-        f32x16 acc = {};
-        mma<false, true>(acc, S, 32, 0, M, 0, 0, 32, lane);
-        wave_sync();
-#pragma unroll
-        for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][lane & 31] = acc[r];
-        wave_sync();
-        // S11 -= L10 . L10^T
-        acc = f32x16{};
-        mma<false, true>(acc, S, 32, 0, S, 32, 0, 32, lane);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) S[32 + acc_row(r, lane)][32 + (lane & 31)] -= acc[r];
-        wave_sync();
-      }
-      factor32(S, M, o, lane, bad);
-    }
-    // M10 = -M11 . L10 . M00 : T = L10 . M00, then M10 = -M11 . T
-    f32x16 acc = {};
-    mma<false, false>(acc, S, 32, 0, M, 0, 0, 32, lane);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) T[acc_row(r, lane)][lane & 31] = acc[r];
-    wave_sync();
-    acc = f32x16{};
-    mma<false, false>(acc, M, 32, 32, T, 0, 0, 32, lane);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) M[32 + acc_row(r, lane)][lane & 31] = -acc[r];
+    factor32(S, M, 0, lane, bad);
   } else if (P) {
     for (int q = wave - 1; q < 4; q += 3) {
       const int r0 = (q >> 1) * 32, c0 = (q & 1) * 32;
@@ -225,6 +224,26 @@ __device__ void factor64(Tile& S, Tile& M, Tile& T, int nb, int* bad, Tile* P, c
       for (int r = 0; r < 16; ++r) (*P)[r0 + acc_row(r, lane)][c0 + (lane & 31)] -= acc[r];
     }
   }
+  __syncthreads();
+  // L10 = S10 . M00^T (in place: all reads before the stores)
+  {
+    const f32x4 acc = mma16<false, true, 32>(S, 32 + qr, 0, M, qc, 0, lane);
+    __syncthreads();
+    put16(S, 32 + qr, qc, acc, 1.f, false, lane);
+  }
+  __syncthreads();
+  // S11 -= L10 . L10^T and T = L10 . M00 (for M10 = -M11 . L10 . M00)
+  {
+    const f32x4 u = mma16<false, true, 32>(S, 32 + qr, 0, S, 32 + qc, 0, lane);
+    const f32x4 t = mma16<false, false, 32>(S, 32 + qr, 0, M, qc, 0, lane);
+    put16(S, 32 + qr, 32 + qc, u, -1.f, true, lane);
+    put16(T, qr, qc, t, 1.f, false, lane);
+  }
+  __syncthreads();
+  if (wave == 0) factor32(S, M, 32, lane, bad);
+  __syncthreads();
+  // M10 = -M11 . T
+  put16(M, 32 + qr, qc, mma16<false, false, 32>(M, 32 + qr, 32, T, qc, 0, lane), -1.f, false, lane);
   __syncthreads();
 }
 
