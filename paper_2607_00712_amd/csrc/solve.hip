@@ -289,39 +289,89 @@ __global__ void solve_init_kernel(const float* G, float* L, const float* C, floa
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
-// Cholesky launch k: trailing lower block triangle from block k+1.
+// Trailing update of launch k for a 2 x 2 group of 64-blocks with top-left block
+// (R, T), R >= T >= k + 2: A_rt -= L_rk L_tk^T, block (R + w / 2, T + w % 2) on
+// wave w (blocks past the matrix or above the diagonal are skipped). The four
+// waves share L_rk (rows of blocks R, R + 1) and L_tk staged in LDS; each
+// wave's C block is loaded into registers at the start and stored at the end.
+// The k order per accumulator is that of a single-block update.
+__device__ void trailing_2x2(float* L, int n, int nblk, int k, int R, int T, Tile* tiles) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, h = lane >> 5;
+  float (*Ub)[kLd] = tiles[0];  // [128][kLd]: rows of blocks R, R + 1 (two consecutive tiles)
+  float (*Vb)[kLd] = tiles[2];  // [128][kLd]: rows of blocks T, T + 1
+  const int br = R + (wave >> 1), bc = T + (wave & 1);
+  const bool mine = br < nblk && bc <= br;
+  float c[2][2][16];
+  if (mine) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = br * kNb + 32 * i + acc_row(r, lane), col = bc * kNb + 32 * j + l32;
+          c[i][j][r] = row < n && col < n ? L[(int64_t)row * n + col] : 0.f;
+        }
+  }
+  {
+    Frag f0, f1, f2, f3;
+    fetch(f0, L + (int64_t)R * kNb * n + k * kNb, n, min(kNb, n - R * kNb), kNb);
+    fetch(f1, L + (int64_t)(R + 1) * kNb * n + k * kNb, n, min(kNb, n - (R + 1) * kNb), kNb);
+    fetch(f2, L + (int64_t)T * kNb * n + k * kNb, n, min(kNb, n - T * kNb), kNb);
+    fetch(f3, L + (int64_t)(T + 1) * kNb * n + k * kNb, n, min(kNb, n - (T + 1) * kNb), kNb);
+    put(tiles[0], f0);
+    put(tiles[1], f1);
+    put(tiles[2], f2);
+    put(tiles[3], f3);
+  }
+  __syncthreads();
+  if (!mine) return;
+  const int qr = (wave >> 1) * kNb, qc = (wave & 1) * kNb;
+  f32x16 acc[2][2] = {};
+#pragma unroll
+  for (int kk = 0; kk < kNb; kk += 2) {
+    float a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[i] = Ub[qr + 32 * i + l32][kk + h];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) b[j] = Vb[qc + 32 * j + l32][kk + h];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma_f32(a[i], b[j], acc[i][j]);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = br * kNb + 32 * i + acc_row(r, lane), col = bc * kNb + 32 * j + l32;
+        if (row < n && col < n) L[(int64_t)row * n + col] = c[i][j][r] - acc[i][j][r];
+      }
+}
+
+// Cholesky launch k (k = -1 .. nblk - 2): workgroups 0 .. m - 1 own the next
+// panel column, blocks (k + 1 + i, k + 1); the others the trailing triangle from
+// block k + 2 in 2 x 2 groups of blocks (the first launch has no trailing part).
 __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int* status) {
-  __shared__ Tile S, M, T, U, V, P;
+  __shared__ __attribute__((aligned(16))) Tile tiles[6];
   __shared__ int bad;
   const int nblk = (n + kNb - 1) / kNb;
-  int ti, tj;
-  if (k < 0) {
-    ti = blockIdx.x;  // first launch: the first panel column only
-    tj = 0;
-  } else {
-    tri_index(blockIdx.x, ti, tj);
+  const int m = nblk - 1 - k;
+  if ((int)blockIdx.x >= m) {
+    int ti, tj;
+    tri_index((int)blockIdx.x - m, ti, tj);
+    trailing_2x2(L, n, nblk, k, k + 2 + 2 * ti, k + 2 + 2 * tj, tiles);
+    return;
   }
-  const int r = k + 1 + ti, t = k + 1 + tj;  // block coordinates, r >= t
-  if (r >= nblk) return;
-  const int rr = min(kNb, n - r * kNb), rt = min(kNb, n - t * kNb);
+  Tile &S = tiles[0], &M = tiles[1], &T = tiles[2], &U = tiles[3], &V = tiles[4], &P = tiles[5];
+  const int r = k + 1 + (int)blockIdx.x, t = k + 1;  // block coordinates
+  const int rr = min(kNb, n - r * kNb);
   float* Lrt = L + (int64_t)r * kNb * n + t * kNb;
   if (threadIdx.x == 0) bad = 0;
 
-  if (t > k + 1) {
-    // plain trailing update A_rt -= L_rk L_tk^T
-    Frag fu, fv, ft;
-    fetch(fu, L + (int64_t)r * kNb * n + k * kNb, n, rr, kNb);
-    fetch(fv, L + (int64_t)t * kNb * n + k * kNb, n, rt, kNb);
-    fetch(ft, Lrt, n, rr, rt);
-    put(U, fu);
-    put(V, fv);
-    put(T, ft);
-    __syncthreads();
-    quad_store(T, quad<false, true>(U, V), -1.f, true);
-    __syncthreads();
-    store_tile(T, Lrt, n, rr, rt);
-    return;
-  }
   // next panel column: updated diagonal block, factor, inverse
   const int d = k + 1;
   const int nd = min(kNb, n - d * kNb);
@@ -914,8 +964,9 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
                        w.status);
   }
   for (int k = -1; k <= nblk - 2; ++k) {
-    const int m = nblk - 1 - k;  // blocks in the trailing triangle
-    const int grid = k < 0 ? nblk : m * (m + 1) / 2;
+    const int m = nblk - 1 - k;                   // blocks of the next panel column
+    const int groups = (nblk - 2 - k + 1) / 2;    // 2 x 2 groups per side of the trailing triangle
+    const int grid = m + (k < 0 ? 0 : groups * (groups + 1) / 2);
     hipLaunchKernelGGL(chol_step_kernel, dim3(grid), dim3(kThreads), 0, stream, L, w.dinv, d, k, w.status);
   }
   // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above
