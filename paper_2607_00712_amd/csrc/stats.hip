@@ -9,8 +9,9 @@
 //   and X = bf16_rne(x) when x arrives in fp32. When x is the very same buffer
 //   as y_local (the attention output itself, the pre-projection reading) the
 //   y_local values already loaded are reused for X.
-//   Vector loads of 4 elements per thread per step, a grid-stride loop sized to
-//   the device, wavefront shuffles then one fp64 atomic per workgroup.
+//   8 elements per thread per step (all loads issued before use), a
+//   grid-stride loop over 2 workgroups per CU, wavefront shuffles then one
+//   fp64 atomic per workgroup.
 //
 // gram_kernel (bf16 MFMA 32x32x16, fp32 accumulation):
 //   G += X^T X on the lower block triangle of 256x256 tiles, C += X^T R.
@@ -65,30 +66,37 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
     const void* y_full, const void* y_local, int64_t n_r, uint16_t* r_out, const float* x_f32,
     int64_t n_x, uint16_t* x_out, int x_from_y_local, double* sq_norm) {
   __shared__ double red[kThreads / 64];
-  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
+  const int64_t stride = (int64_t)gridDim.x * kThreads * 8;
   float part = 0.f;
-  const int64_t n_r4 = n_r & ~(int64_t)3;
-  for (int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 4; i < n_r4; i += stride) {
-    float f[4], l[4];
+  const int64_t n_r8 = n_r & ~(int64_t)7;
+  // 8 elements per thread and step: the four loads are in flight together
+  for (int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 8; i < n_r8; i += stride) {
+    float f[8], l[8];
     load4<YT>(y_full, i, f);
+    load4<YT>(y_full, i + 4, f + 4);
     load4<YT>(y_local, i, l);
-    uint16_t r[4];
+    load4<YT>(y_local, i + 4, l + 4);
+    uint16_t r[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       r[j] = f2bf_rne(f[j] - l[j]);
       const float rv = bf2f(r[j]);
       part = fmaf(rv, rv, part);
     }
-    *(u32x2*)(r_out + i) = u32x2{(uint32_t)r[0] | ((uint32_t)r[1] << 16),
-                                 (uint32_t)r[2] | ((uint32_t)r[3] << 16)};
+    u32x4 rw;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rw[j] = (uint32_t)r[2 * j] | ((uint32_t)r[2 * j + 1] << 16);
+    *(u32x4*)(r_out + i) = rw;
     if (x_from_y_local) {
-      *(u32x2*)(x_out + i) = u32x2{(uint32_t)f2bf_rne(l[0]) | ((uint32_t)f2bf_rne(l[1]) << 16),
-                                   (uint32_t)f2bf_rne(l[2]) | ((uint32_t)f2bf_rne(l[3]) << 16)};
+      u32x4 xw;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xw[j] = (uint32_t)f2bf_rne(l[2 * j]) | ((uint32_t)f2bf_rne(l[2 * j + 1]) << 16);
+      *(u32x4*)(x_out + i) = xw;
     }
   }
-  // ragged tail (fewer than 4 elements), handled by the first workgroup
-  if (blockIdx.x == 0 && threadIdx.x < (int)(n_r - n_r4)) {
-    const int64_t i = n_r4 + threadIdx.x;
+  // ragged tail (fewer than 8 elements), handled by the first workgroup
+  if (blockIdx.x == 0 && threadIdx.x < (int)(n_r - n_r8)) {
+    const int64_t i = n_r8 + threadIdx.x;
     const float l = load1<YT>(y_local, i);
     const uint16_t r = f2bf_rne(load1<YT>(y_full, i) - l);
     r_out[i] = r;
@@ -99,7 +107,7 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
   // separate fp32 -> bf16 conversion of x when it is its own buffer
   if (x_f32 != nullptr && !x_from_y_local) {
     const int64_t n_x4 = n_x & ~(int64_t)3;
-    for (int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 4; i < n_x4; i += stride) {
+    for (int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 4; i < n_x4; i += stride / 2) {
       const f32x4 t = *(const f32x4*)(x_f32 + i);
       *(u32x2*)(x_out + i) = u32x2{(uint32_t)f2bf_rne(t[0]) | ((uint32_t)f2bf_rne(t[1]) << 16),
                                    (uint32_t)f2bf_rne(t[2]) | ((uint32_t)f2bf_rne(t[3]) << 16)};
@@ -457,8 +465,11 @@ hipError_t launch_discrepancy(const void* x, int x_dtype, const void* y_full, co
                         d_in == d_out;
   const float* x_f32 = x_dtype == ISPA_DTYPE_F32 ? (const float*)x : nullptr;
   const int64_t n_max = n_r > n_x ? n_r : n_x;
-  int64_t grid = (n_max / 4 + kThreads - 1) / kThreads;
-  if (grid > 2048) grid = 2048;  // 8 workgroups per CU, grid-stride beyond
+  int64_t grid = (n_max / 8 + kThreads - 1) / kThreads;
+  // 2 workgroups per CU, grid-stride beyond: more workgroups only add fp64
+  // atomics on the one norm accumulator, which serialise (measured: 256-512
+  // workgroups best, 2048 +14 us at the 1.3B chunk)
+  if (grid > 512) grid = 512;
   if (grid < 1) grid = 1;
   if (y_dtype == ISPA_DTYPE_F32) {
     hipLaunchKernelGGL(discrepancy_kernel<ISPA_DTYPE_F32>, dim3((unsigned)grid), dim3(kThreads), 0,
