@@ -35,9 +35,9 @@ import torch  # noqa: E402
 
 WORKLOADS = {
     "1.3b": dict(name="wan1.3b-chunk-warmup-step", heads=12, head_dim=128, n_q=4680, cache_len=32760,
-                 window=9360, sink=0, lam=1e-3),
+                 window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
     "14b": dict(name="14b-chunk-warmup-step", heads=40, head_dim=128, n_q=4680, cache_len=98280,
-                window=9360, sink=0, lam=1e-3),
+                window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
 }
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
@@ -94,6 +94,12 @@ def gpu_run(w, steps, warmup, only="all"):
 
     run = {p: only in ("all", p) for p in ("attn_dual", "attn_local", "accum_stats", "solve")}
 
+    # a layer's warmup is T_warm = 4 chunks (Sec. 4.1): the statistics restart
+    # every 4 steps, as for the next layer (at 14B one chunk has fewer rows
+    # than D, so G + lambda I accumulated without end would become singular in
+    # fp32 and the solve would report NOT_SPD)
+    chunk = [0]
+
     def step(ev=None):
         if ev is not None:
             ev[0].record()
@@ -108,6 +114,9 @@ def gpu_run(w, steps, warmup, only="all"):
         if ev is not None:
             ev[2].record()
         if run["accum_stats"]:
+            if chunk[0] % w["t_warm_chunks"] == 0:
+                stats.reset()
+            chunk[0] += 1
             stats.accum(out_l, out, out_l)
         if ev is not None:
             ev[3].record()
@@ -298,7 +307,7 @@ def main():
             "heads": w["heads"], "head_dim": w["head_dim"], "chunk_queries": w["n_q"],
             "cache_len": w["cache_len"], "window": w["window"], "sink": w["sink"],
             "d": w["heads"] * w["head_dim"], "lambda": w["lam"],
-            "step": "F-Layer dual attention + L-Layer attention + accum_stats + solve",
+            "step": "F-Layer dual attention + L-Layer attention + accum_stats + solve (statistics restart every 4 chunks)",
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
