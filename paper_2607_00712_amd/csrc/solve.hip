@@ -143,12 +143,13 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// One wave: factor the 32 x 32 SPD block S[o..o+31][o..o+31] (lower part
-// valid) into L, in place with zeros above the diagonal, and write L^-1 (lower
-// triangular) to M[o..][o..]. No LDS traffic inside the elimination:
-//   lanes 0..31   x = row i of the symmetric matrix being reduced,
-//   lanes 32..63  x = column i - 32 of the inverse being formed by forward
-//                 substitution, starting from the unit vector.
+// One wave: factor the N x N SPD block S[o..o+N-1][o..o+N-1] (N = 16 or 32,
+// lower part valid) into L, in place with zeros above the diagonal, and write
+// L^-1 (lower triangular) to M[o..][o..]. No LDS traffic inside the elimination:
+//   lanes 0..N-1    x = row i of the symmetric matrix being reduced,
+//   lanes N..2N-1   x = column i - N of the inverse being formed by forward
+//                   substitution, starting from the unit vector
+// (for N = 16 lanes 32..63 repeat lanes 0..31 and store nothing).
 // At step j the pivot p_j = (row j)[j] and s_c = (row j)[c] = (column j)[c]
 // (symmetry) come from lane j by readlane, and both kinds of lane apply the
 // same update x[c] -= (x[j] / p_j) s_c for c > j: the Schur complement for a
@@ -156,41 +157,73 @@ __device__ __forceinline__ void wave_sync() {
 // Afterwards L[i][j] = x[j] / sqrt(p_j) (j < i), L[i][i] = sqrt(p_i) and
 // L^-1[r][col] = x[r] / sqrt(p_r). Hardware square root and reciprocal (about
 // 1 ulp). Sets *bad on a non-positive pivot (then replaced by 1).
-__device__ __forceinline__ void factor32(Tile& S, Tile& M, int o, int lane, int* bad) {
-  const int i = lane & 31;
-  const bool lo = lane < 32;
-  float x[32];
+template <int N>
+__device__ __forceinline__ void factor_reg(Tile& S, Tile& M, int o, int lane, int* bad) {
+  const int i = lane % N;
+  const bool lo = (lane / N) % 2 == 0;
+  float x[N];
 #pragma unroll
-  for (int c = 0; c < 32; ++c) {
+  for (int c = 0; c < N; ++c) {
     float v = S[o + max(i, c)][o + min(i, c)];
     asm volatile("" : "+v"(v));  // every lane loads: no branch around the read
     x[c] = lo ? v : (c == i ? 1.f : 0.f);
   }
-  float lj[32];
+  float lj[N];
   int neg = 0;
 #pragma unroll
-  for (int j = 0; j < 32; ++j) {
+  for (int j = 0; j < N; ++j) {
     float piv = readlane_f(x[j], j);
     neg |= !(piv > 0.f);
     piv = piv > 0.f ? piv : 1.f;
     lj[j] = piv;
     // the pivot row first (independent readlanes), then the updates
-    float sr[32];
+    float sr[N];
 #pragma unroll
-    for (int c = j + 1; c < 32; ++c) sr[c] = readlane_f(x[c], j);
+    for (int c = j + 1; c < N; ++c) sr[c] = readlane_f(x[c], j);
     const float coef = x[j] * __builtin_amdgcn_rcpf(piv);
 #pragma unroll
-    for (int c = j + 1; c < 32; ++c) x[c] = fmaf(-coef, sr[c], x[c]);
+    for (int c = j + 1; c < N; ++c) x[c] = fmaf(-coef, sr[c], x[c]);
   }
   if (neg && lane == 0) *bad = 1;
-  // one store per element: row i of L for lanes 0..31, column i of L^-1 for the rest
+  // one store per element: row i of L for the row lanes, column i of L^-1 for the rest
   float* dst = lo ? &S[o + i][o] : &M[o][o + i];
   const int step = lo ? 1 : kLd;
+  if (lane < 2 * N) {
 #pragma unroll
-  for (int c = 0; c < 32; ++c) {
-    const float l = __builtin_amdgcn_sqrtf(lj[c]);
-    const float v = x[c] * __builtin_amdgcn_rcpf(l);
-    dst[c * step] = lo ? (c < i ? v : (c == i ? l : 0.f)) : (c >= i ? v : 0.f);
+    for (int c = 0; c < N; ++c) {
+      const float l = __builtin_amdgcn_sqrtf(lj[c]);
+      const float v = x[c] * __builtin_amdgcn_rcpf(l);
+      dst[c * step] = lo ? (c < i ? v : (c == i ? l : 0.f)) : (c >= i ? v : 0.f);
+    }
+  }
+  wave_sync();
+}
+
+// One wave: the 32 x 32 factor and inverse at offset o from two 16 x 16 register
+// factors: L00 and M00; L10 = S10 M00^T; S11 -= L10 L10^T with T = L10 M00
+// beside it (T in the upper-right 16 x 16 of this block of M, zero again at the
+// end); L11 and M11; M10 = -M11 T. The 16-wide eliminations issue a third of the
+// readlanes and FMAs of one 32-wide elimination, and the products are four
+// 16x16x4 MFMAs each.
+__device__ __forceinline__ void factor32(Tile& S, Tile& M, int o, int lane, int* bad) {
+  factor_reg<16>(S, M, o, lane, bad);
+  {
+    const f32x4 l10 = mma16<false, true, 16>(S, o + 16, o, M, o, o, lane);
+    put16(S, o + 16, o, l10, 1.f, false, lane);  // in place: its reads are issued before
+  }
+  wave_sync();
+  {
+    const f32x4 u = mma16<false, true, 16>(S, o + 16, o, S, o + 16, o, lane);
+    const f32x4 t = mma16<false, false, 16>(S, o + 16, o, M, o, o, lane);
+    put16(S, o + 16, o + 16, u, -1.f, true, lane);
+    put16(M, o, o + 16, t, 1.f, false, lane);
+  }
+  wave_sync();
+  factor_reg<16>(S, M, o + 16, lane, bad);
+  {
+    const f32x4 m10 = mma16<false, false, 16>(M, o + 16, o + 16, M, o + 16, o, lane);
+    put16(M, o + 16, o, m10, -1.f, false, lane);
+    put16(M, o, o + 16, f32x4{}, 1.f, false, lane);
   }
   wave_sync();
 }
