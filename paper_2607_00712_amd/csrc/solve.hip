@@ -306,18 +306,12 @@ __device__ __forceinline__ void tri_index(int t, int& ti, int& tj) {
   tj = t - ti * (ti + 1) / 2;
 }
 
-// L = lower(G) + lambda I (upper part zero), Bw = C, status = 0.
-__global__ void solve_init_kernel(const float* G, float* L, const float* C, float* Bw, int n, int n_out,
-                                  float lambda, int* status) {
-  const int64_t nn = (int64_t)n * n, nc = (int64_t)n * n_out;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nn + nc;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    if (i < nn) {
-      const int r = (int)(i / n), c = (int)(i % n);
-      L[i] = c < r ? G[i] : (c == r ? G[i] + lambda : 0.f);
-    } else {
-      Bw[i - nn] = C[i - nn];
-    }
+// L = lower(G) + lambda I (upper part zero), status = 0.
+__global__ void solve_init_kernel(const float* G, float* L, int n, float lambda, int* status) {
+  const int64_t nn = (int64_t)n * n;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nn; i += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(i / n), c = (int)(i % n);
+    L[i] = c < r ? G[i] : (c == r ? G[i] + lambda : 0.f);
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
@@ -549,7 +543,8 @@ struct GemmJob {
   float* C;
   int M;
   int64_t lda, ldc;
-  int sub;  // 1: C -= A B, 0: C = A B
+  int sub;                    // 1: C -= A B, 0: C = A B
+  const float* Cin = nullptr;  // with sub: read the minuend here instead of C (same ldc)
 };
 struct GemmArgs {
   GemmJob job[2];
@@ -565,8 +560,9 @@ template <int WM, int WN, int QM, int QN, bool A_MK>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
   constexpr int TM = WM * QM * 32, TN = WN * QN * 32;
   constexpr int SA = TM + 32, SB = TN + 32;  // row strides: the two k rows of an operand read sit 32 banks apart
-  constexpr int NA = kKc * TM / 4 / kThreads, NB = kKc * TN / 4 / kThreads;
-  static_assert(WM * WN == kThreads / 64 && NA >= 1 && NB >= 1, "tile shape");
+  constexpr int kA4 = kKc * TM / 4;  // 16-byte pieces of an A chunk
+  constexpr int NA = (kA4 + kThreads - 1) / kThreads, NB = kKc * TN / 4 / kThreads;
+  static_assert(WM * WN == kThreads / 64 && NB >= 1 && kA4 % 64 == 0, "tile shape");
   __shared__ __attribute__((aligned(16))) float As[2][kKc][SA];
   __shared__ __attribute__((aligned(16))) float Bs[2][kKc][SB];
 
@@ -601,6 +597,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < NA; ++q) {
       const int e = threadIdx.x + q * kThreads;
+      if (e >= kA4) break;  // (wave-uniform: kA4 is a multiple of 64)
       if (A_MK) {
         const int m = e / (kKc / 4), k = (e % (kKc / 4)) * 4;
         ra[q] = (m0 + m < M && k0 + k < K) ? *(const f32x4*)(A + (int64_t)(m0 + m) * lda + k0 + k)
@@ -623,6 +620,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < NA; ++q) {
       const int e = threadIdx.x + q * kThreads;
+      if (e >= kA4) break;
       if (A_MK) {
         const int m = e / (kKc / 4), k = (e % (kKc / 4)) * 4;
 #pragma unroll
@@ -888,6 +886,8 @@ __global__ __launch_bounds__(kThreads) void gemm_ring_kernel(GemmArgs g) {
   t.lda = second ? g.job[1].lda : g.job[0].lda;
   const int64_t ldc = second ? g.job[1].ldc : g.job[0].ldc;
   const int sub = second ? g.job[1].sub : g.job[0].sub;
+  const float* Cin = second ? g.job[1].Cin : g.job[0].Cin;
+  if (Cin == nullptr) Cin = C;
   t.m0 = (tt / tiles_n) * TM;
   t.n0 = (tt % tiles_n) * TN;
   if (t.m0 >= t.M) return;
@@ -940,8 +940,8 @@ __global__ __launch_bounds__(kThreads) void gemm_ring_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) {
         const int row = t.m0 + wm0 + 32 * i + acc_row(r, lane);
         if (row < t.M && col < t.N) {
-          float* p = C + (int64_t)row * ldc + col;
-          *p = sub ? *p - acc[i][j][r] : acc[i][j][r];
+          const int64_t o = (int64_t)row * ldc + col;
+          C[o] = sub ? Cin[o] - acc[i][j][r] : acc[i][j][r];
         }
       }
     }
@@ -990,11 +990,10 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
   float* L = w.L;
   float* Y = w.work;
   {
-    const int64_t total = (int64_t)d * d + (int64_t)d * d_out;
+    const int64_t total = (int64_t)d * d;
     int grid = (int)((total + 255) / 256);
     if (grid > 8192) grid = 8192;
-    hipLaunchKernelGGL(solve_init_kernel, dim3(grid), dim3(256), 0, stream, G, L, C, Y, d, d_out, lambda,
-                       w.status);
+    hipLaunchKernelGGL(solve_init_kernel, dim3(grid), dim3(256), 0, stream, G, L, d, lambda, w.status);
   }
   for (int k = -1; k <= nblk - 2; ++k) {
     const int m = nblk - 1 - k;                   // blocks of the next panel column
@@ -1016,7 +1015,8 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 1, false>), dim3(16, nb), dim3(kThreads), 0, stream, g);
   }
   if (nb > 1) {
-    // Lh_rI = L_rI X_I in place: a workgroup owns 64 rows x the whole 256-block
+    // Lh_rI = L_rI X_I in place: a workgroup owns 32 rows x the whole 256-block
+    // (all of its A is read before any of its C is written)
     GemmArgs g = {};
     float* first = L + (int64_t)kBb * d;  // rows of block 1, columns of block 0
     g.job[0] = GemmJob{first, first, d - kBb, d, d, 0};
@@ -1028,7 +1028,7 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     g.batch_a = g.batch_c = (int64_t)kBb * d + kBb;
     g.batch_b = (int64_t)kBb * kBb;
     g.batch_dm = -kBb;
-    hipLaunchKernelGGL((gemm_kernel<1, 4, 2, 2, true>), dim3((d - kBb + 63) / 64, nb - 1), dim3(kThreads), 0,
+    hipLaunchKernelGGL((gemm_kernel<1, 4, 1, 2, true>), dim3((d - kBb + 31) / 32, nb - 1), dim3(kThreads), 0,
                        stream, g);
     hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk), dim3(kThreads), 0, stream, L, d);
   }
@@ -1038,13 +1038,15 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     GemmArgs g = {};
     const int below = d - (I + 1) * kBb;
     int j = 0;
+    // the first step reads the right-hand side C itself (Y = C before any update)
+    const float* Yin = I == 0 ? C : Y;
     if (below > 0) {
       g.job[j++] = GemmJob{L + (int64_t)I * kBb * d + (int64_t)(I + 1) * kBb, Y + (int64_t)(I + 1) * kBb * d_out,
-                           below, d, d_out, 1};
+                           below, d, d_out, 1, Yin + (int64_t)(I + 1) * kBb * d_out};
     }
     g.job[j++] = GemmJob{pinv + (int64_t)I * kBb * kBb, delta_w + (int64_t)I * kBb * d_out, kI, kBb, d_out, 0};
     g.n_jobs = j;
-    g.B = Y + (int64_t)I * kBb * d_out;
+    g.B = Yin + (int64_t)I * kBb * d_out;
     g.N = d_out;
     g.K = kI;
     g.ldb = d_out;
