@@ -91,6 +91,8 @@ def gpu_run(w, steps, warmup, only="all"):
     lse_L = torch.empty_like(lse)
     stats = ispa.Stats(D, D, max_rows=w["n_q"], device=dev)
     dw = torch.empty((D, D), dtype=torch.float32, device=dev)
+    eps_dev = torch.zeros((1,), dtype=torch.float64, device=dev)
+    status_dev = torch.zeros((1,), dtype=torch.int32, device=dev)
 
     run = {p: only in ("all", p) for p in ("attn_dual", "attn_local", "accum_stats", "solve")}
 
@@ -121,7 +123,10 @@ def gpu_run(w, steps, warmup, only="all"):
         if ev is not None:
             ev[3].record()
         if run["solve"]:
-            stats.solve(w["lam"], delta_w=dw)
+            # the solve that does not wait: eps and the status word stay in
+            # device memory (a warmup reads the scores of all layers at once
+            # for the ranking); checked once after the timed steps
+            stats.solve_async(w["lam"], delta_w=dw, eps=eps_dev, status=status_dev)
         if ev is not None:
             ev[4].record()
 
@@ -141,6 +146,9 @@ def gpu_run(w, steps, warmup, only="all"):
         parts["attn_local"].append(ev[1].elapsed_time(ev[2]))
         parts["accum_stats"].append(ev[2].elapsed_time(ev[3]))
         parts["solve"].append(ev[3].elapsed_time(ev[4]))
+    if run["solve"]:
+        if int(status_dev.item()) != 0 or not math.isfinite(float(eps_dev.item())):
+            raise RuntimeError("solve: G + lambda I not positive definite in the timed steps")
     avg = {k2: sum(v2) / len(v2) for k2, v2 in parts.items()}
     ms_step = (t1 - t0) * 1e3 / steps
     if only == "all":

@@ -24,7 +24,8 @@
  *     enqueues, except the statistics workspace, which the handle uses until
  *     ispa_stats_destroy.
  *   - Work is enqueued on the caller's HIP stream (0 = the null stream) and
- *     runs asynchronously; only ispa_solve_modulation waits for the device.
+ *     runs asynchronously; only ispa_solve_modulation waits for the device
+ *     (ispa_solve_modulation_async is its variant that does not).
  *   - Argument errors are reported before anything is enqueued, so a failing
  *     call writes nothing.
  *   - The return value is a status code (ISPA_OK or a negative ISPA_ERR_*).
@@ -237,6 +238,20 @@ int ispa_accum_stats(ispa_stats* handle, const void* x, int32_t x_dtype,
  * ISPA_ERR_NOT_SPD (delta_w then unspecified) if a pivot is not positive.
  */
 int ispa_solve_modulation(ispa_stats* handle, float lambda, float* delta_w, double* eps_out);
+
+/*
+ * ispa_solve_modulation without the wait: enqueues the same work on the
+ * handle's stream and returns. When it has run, eps_dev holds eps of Eq. 6
+ * (the value ispa_solve_modulation reports) and status_dev holds 0, or 1 when
+ * a pivot was not positive (delta_w and eps are then unspecified). For a
+ * caller that reads the scores of many layers at once (the ranking of
+ * Sec. 3.3) instead of waiting once per layer.
+ *   eps_dev     device double (8-byte aligned) or NULL
+ *   status_dev  device int32 (4-byte aligned) or NULL
+ * Argument errors are returned before anything is enqueued.
+ */
+int ispa_solve_modulation_async(ispa_stats* handle, float lambda, float* delta_w, double* eps_dev,
+                                int32_t* status_dev);
 
 /* ---------------------------------------------------------- absorption */
 /*

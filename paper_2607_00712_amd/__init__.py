@@ -67,6 +67,7 @@ _SIGNATURES = {
                                         ctypes.POINTER(_c_p), ctypes.POINTER(_c_i64)]),
     "ispa_accum_stats": (ctypes.c_int, [_c_p, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64]),
     "ispa_solve_modulation": (ctypes.c_int, [_c_p, _c_f32, _c_p, ctypes.POINTER(ctypes.c_double)]),
+    "ispa_solve_modulation_async": (ctypes.c_int, [_c_p, _c_f32, _c_p, _c_p, _c_p]),
 }
 
 _lib = None
@@ -327,6 +328,24 @@ class Stats:
         _check(lib().ispa_solve_modulation(self._handle(), float(lam), _ptr(delta_w), ctypes.byref(eps)),
                "ispa_solve_modulation")
         return delta_w, eps.value
+
+    def solve_async(self, lam=1e-3, delta_w=None, eps=None, status=None):
+        """The same solve without waiting (ispa_solve_modulation_async): returns
+        (delta_w, eps, status) with eps a device fp64 [1] and status a device
+        int32 [1] (0, or 1 when G + lam I was not positive definite), valid once
+        the handle's stream has run the work."""
+        if delta_w is None:
+            delta_w = torch.empty((self.d_in, self.d_out), dtype=torch.float32, device=self.device)
+        if eps is None:
+            eps = torch.empty((1,), dtype=torch.float64, device=self.device)
+        if status is None:
+            status = torch.empty((1,), dtype=torch.int32, device=self.device)
+        _require(delta_w, "delta_w", torch.float32, self.device)
+        _require(eps, "eps", torch.float64, self.device, ndim=1)
+        _require(status, "status", torch.int32, self.device, ndim=1)
+        _check(lib().ispa_solve_modulation_async(self._handle(), float(lam), _ptr(delta_w), _ptr(eps), _ptr(status)),
+               "ispa_solve_modulation_async")
+        return delta_w, eps, status
 
     def close(self):
         if self._h:

@@ -82,7 +82,7 @@ const char* ispa_status_string(int status) {
   }
 }
 
-int ispa_abi_version(void) { return 102; }
+int ispa_abi_version(void) { return 103; }
 
 }  // extern "C"
 
@@ -319,29 +319,44 @@ int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* 
   return ISPA_OK;
 }
 
-int ispa_solve_modulation(ispa_stats* h, float lambda, float* delta_w, double* eps_out) {
+namespace {
+// Enqueue the solve of handle h; eps and the status word land in the
+// workspace scalars [4], [5] and, when given, in eps_dev / status_dev.
+int enqueue_solve(ispa_stats* h, float lambda, float* delta_w, double* eps_dev, int32_t* status_dev) {
   if (!valid_handle(h)) return ISPA_ERR_STATE;
   if (!delta_w || !aligned16(delta_w)) return ISPA_ERR_INVALID_ARG;
   if (!(lambda >= 0.f) || isinf(lambda)) return ISPA_ERR_INVALID_ARG;
+  if (((uintptr_t)eps_dev & 7u) || ((uintptr_t)status_dev & 3u)) return ISPA_ERR_INVALID_ARG;
   ispa::SolveWork w;
   w.L = (float*)(h->ws + h->lay.L);
   w.work = (float*)(h->ws + h->lay.W);
   w.dinv = (float*)(h->ws + h->lay.Dinv);
   w.status = (int*)(h->ws + h->lay.status);
-  w.scalars = (double*)(h->ws + h->lay.scalars) + 2;
+  w.scalars = (double*)(h->ws + h->lay.scalars);
+  w.eps_out = eps_dev;
+  w.status_out = status_dev;
   const float* G = (const float*)(h->ws + h->lay.G);
   const float* C = (const float*)(h->ws + h->lay.C);
-  if (ispa::launch_solve(G, C, h->d_in, h->d_out, lambda, delta_w, w, h->stream) != hipSuccess) return ISPA_ERR_HIP;
-  // scalars: [0] s = sum ||R||^2, [1] unused, [2] <dW, C>, [3] ||dW||^2
-  int status = 0;
-  double sc[4] = {0, 0, 0, 0};
-  if (hipMemcpyAsync(&status, w.status, sizeof(int), hipMemcpyDeviceToHost, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+  return ispa::launch_solve(G, C, h->d_in, h->d_out, lambda, delta_w, w, h->stream) == hipSuccess ? ISPA_OK
+                                                                                                   : ISPA_ERR_HIP;
+}
+}  // namespace
+
+int ispa_solve_modulation(ispa_stats* h, float lambda, float* delta_w, double* eps_out) {
+  const int st = enqueue_solve(h, lambda, delta_w, nullptr, nullptr);
+  if (st != ISPA_OK) return st;
+  // one copy of the scalars: [4] eps, [5] the status word
+  double sc[6] = {0, 0, 0, 0, 0, 0};
   if (hipMemcpyAsync(sc, h->ws + h->lay.scalars, sizeof(sc), hipMemcpyDeviceToHost, h->stream) != hipSuccess)
     return ISPA_ERR_HIP;
   if (hipStreamSynchronize(h->stream) != hipSuccess) return ISPA_ERR_HIP;
-  if (status != 0) return ISPA_ERR_NOT_SPD;
-  if (eps_out) *eps_out = sc[0] - sc[2] - (double)lambda * sc[3];
+  if (sc[5] != 0.0) return ISPA_ERR_NOT_SPD;
+  if (eps_out) *eps_out = sc[4];
   return ISPA_OK;
+}
+
+int ispa_solve_modulation_async(ispa_stats* h, float lambda, float* delta_w, double* eps_dev, int32_t* status_dev) {
+  return enqueue_solve(h, lambda, delta_w, eps_dev, status_dev);
 }
 
 

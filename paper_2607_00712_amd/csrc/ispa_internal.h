@@ -118,7 +118,9 @@ struct SolveWork {
   float* work;       // [d, d_out] right-hand side being reduced
   float* dinv;       // [ceil(d/64), 64, 64] inverses of the diagonal blocks of L
   int* status;       // device int: 0 ok, 1 not SPD
-  double* scalars;   // device: [0] <dW, C>, [1] ||dW||^2
+  double* scalars;   // device: [0] s (input), then [2] <dW, C>, [3] ||dW||^2, [4] eps, [5] status
+  double* eps_out = nullptr;  // optional device copies of eps and the status word
+  int* status_out = nullptr;
 };
 size_t solve_dinv_bytes(int d);
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda,

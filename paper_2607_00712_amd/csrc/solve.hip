@@ -725,7 +725,13 @@ __global__ __launch_bounds__(kThreads) void eps_partial_kernel(const float* dw, 
     part[2 * blockIdx.x + 1] = b;
   }
 }
-__global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part, int n_part, double* scalars) {
+// sc: [0] s = sum ||R||^2 (from the statistics), then written here: [2] <dW, C>,
+// [3] ||dW||^2, [4] eps = s - <dW, C> - lambda ||dW||^2 (Eq. 6; each operation
+// rounded on its own), [5] the status word as a double. eps_out / status_out,
+// when given, receive eps and the status word as well.
+__global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part, int n_part, double* sc,
+                                                             double lambda, const int* status, double* eps_out,
+                                                             int* status_out) {
   __shared__ double red[2][kThreads / 64];
   double a = 0, b = 0;
   for (int i = threadIdx.x; i < n_part; i += kThreads) {
@@ -734,8 +740,14 @@ __global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part,
   }
   block_sum2(a, b, red);
   if (threadIdx.x == 0) {
-    scalars[0] = a;
-    scalars[1] = b;
+    const double e = __dsub_rn(__dsub_rn(sc[0], a), __dmul_rn(lambda, b));
+    const int st = *status;
+    sc[2] = a;
+    sc[3] = b;
+    sc[4] = e;
+    sc[5] = (double)st;
+    if (eps_out) *eps_out = e;
+    if (status_out) *status_out = st;
   }
 }
 
@@ -1070,7 +1082,7 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
   const int64_t n = (int64_t)d * d_out;
   hipLaunchKernelGGL(eps_partial_kernel, dim3(kEpsBlocks), dim3(kThreads), 0, stream, delta_w, C, n, (double*)pinv);
   hipLaunchKernelGGL(eps_final_kernel, dim3(1), dim3(kThreads), 0, stream, (const double*)pinv, kEpsBlocks,
-                     w.scalars);
+                     w.scalars, (double)lambda, (const int*)w.status, w.eps_out, w.status_out);
   return hipGetLastError();
 }
 

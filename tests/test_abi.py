@@ -38,7 +38,7 @@ def test_status_strings(L):
     for code in (0, -1, -2, -3, -4, -5):
         assert ispa.status_string(code).startswith("ISPA")
     assert "unknown" in ispa.status_string(7)
-    assert L.ispa_abi_version() == 102
+    assert L.ispa_abi_version() == 103
 
 
 def _attn(L, **kw):
@@ -158,3 +158,9 @@ def test_absorption_argument_errors(L):
     assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 64, 8, p(2048), 1, p(0)) == E  # y over q_w
     assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 0, 64, 8, p(8192), 1, p(0)) == E  # no rows
     assert L.ispa_project_w8a8(p(256), p(1024), p(2048), p(3072), 4, 65600, 8, p(1 << 40), 1, p(0)) == E
+
+
+def test_async_solve_argument_errors(L):
+    # checked before anything is enqueued (no handle: state error; bad pointers)
+    p = lambda v: ctypes.c_void_p(v)
+    assert L.ispa_solve_modulation_async(None, 1e-3, p(256), None, None) == ispa.ISPA_ERR_STATE

@@ -119,3 +119,31 @@ def test_wan13b_solve():
     e = rel_fro(f64(dw), dw_ref)
     print(f"[solve] 1536 rel err {e:.3e}", flush=True)
     assert e <= DW_TOL
+
+
+def test_async_solve_matches_sync():
+    # the variant that does not wait: the same dW bit for bit, the same eps in
+    # device memory, and the status word instead of the NOT_SPD error
+    d, n = 776, 1600
+    x = rows(33, 0, n, d)
+    yf = synth.normal((n, d), synth.seed_of(33, 0, synth.Y_FULL), DEV, dtype=torch.float32)
+    yl = synth.normal((n, d), synth.seed_of(33, 0, synth.Y_LOCAL), DEV, dtype=torch.float32)
+    st = ispa.Stats(d, d, max_rows=n, device=DEV)
+    st.accum(x, yf, yl)
+    dw_sync, eps_sync = st.solve(0.25)
+    dw_async, eps_dev, status_dev = st.solve_async(0.25)
+    torch.cuda.synchronize()
+    assert torch.equal(dw_sync.view(torch.int32), dw_async.view(torch.int32))
+    assert int(status_dev.item()) == 0
+    assert float(eps_dev.item()) == eps_sync
+    # a zero column with lambda = 0: status 1 and no exception
+    x0 = rows(34, 0, 80, 64)
+    x0[:, 5] = 0
+    y0 = synth.normal((80, 64), synth.seed_of(34, 0, synth.Y_FULL), DEV, dtype=torch.float32)
+    st0 = ispa.Stats(64, 64, max_rows=80, device=DEV)
+    st0.accum(x0, y0, torch.zeros_like(y0))
+    _, _, status0 = st0.solve_async(0.0)
+    torch.cuda.synchronize()
+    assert int(status0.item()) == 1
+    with pytest.raises(ispa.NotSPDError):
+        st0.solve(0.0)
