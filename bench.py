@@ -283,7 +283,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the ISPA hot path here has no multi-GPU "
-              "path (heads or layers would shard with no exchange; see DESIGN.md).", file=sys.stderr)
+              "path (heads or layers would shard with no exchange).", file=sys.stderr)
         sys.exit(2)
     if args.only == "hbm_copy":
         print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)

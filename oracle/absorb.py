@@ -14,7 +14,7 @@ Definitions followed (arXiv 2607.00712):
   projects its local attention output with it: Y = A_loc W_new (Sec. 3.1
   step 3).
 
-Readings where the paper is silent (each listed in the design doc):
+Readings where the paper is silent:
 
 * X denotes the rows of A_loc that are fed to the statistics (one row per
   token of every warmup chunk, heads concatenated), already in bf16.

@@ -17,7 +17,7 @@ Definitions followed (arXiv 2607.00712):
 * Sec. 3.4, Eq. 11-12: the full output is the LSE-weighted combination of the
   two branches.
 
-Readings where the paper is silent (each listed in the design doc):
+Readings where the paper is silent:
 
 * the local set is ``[0, min(s, N)) U [max(N - w, 0), N)`` for a window of
   ``w`` keys and a sink of ``s`` keys; the history is ``[s, N - w)`` when that

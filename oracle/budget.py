@@ -2,8 +2,8 @@
 
 Sec. 4 (Tables 1 and 2) labels each variant ISPA-x with K = xN of the N
 layers turned into L-Layers, and prints the fraction of the KV cache kept.
-The paper does not state how that fraction is computed. Reading (listed in
-the design doc): every layer holds the same number of keys per cached frame; an
+The paper does not state how that fraction is computed. Reading: every
+layer holds the same number of keys per cached frame; an
 F-Layer keeps the full cache and an L-Layer keeps a fixed local part of it,
 a fraction ``r`` of the full cache. The kept fraction is then
 

@@ -6,7 +6,7 @@ sink prefix plus the most recent keys (Sec. 3.4, Eq. 7). The oracle states
 WHAT such a layer holds, not how it is stored: after every chunk it holds the
 local set of the whole key sequence generated so far.
 
-Reading (listed in the design doc): the local set keeps its definition of Eq. 7
+Reading: the local set keeps its definition of Eq. 7
 forever, with the sink taken from the first keys of the sequence and the
 window from its last ``window`` keys; keys are rows of the hidden layout
 [keys, H * d].

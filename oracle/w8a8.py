@@ -2,7 +2,7 @@
 
 Sec. 4 (efficiency, Fig. 7) combines ISPA with W8A8 quantisation of the
 linear layers and reports it as quantisation-friendly, without stating the
-scheme. Reading (listed in the design doc): symmetric int8 with one scale per row,
+scheme. Reading: symmetric int8 with one scale per row,
 per token for activations [n, d_in] and per output channel for the linear
 weight [d_out, d_in];
 

@@ -88,7 +88,7 @@ def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"libispa.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+            raise RuntimeError(f"libispa.so is not built ({LIB_PATH}); build it with python -m paper_2607_00712_amd.build")
         handle = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGNATURES.items():
             fn = getattr(handle, name)

@@ -1,6 +1,6 @@
 """Builds libispa.so (gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2607_00712_amd.build   (or __graft_entry__.build())
+Usage: python -m paper_2607_00712_amd.build
 """
 
 import os

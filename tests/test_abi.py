@@ -22,7 +22,7 @@ def declared_functions():
 @pytest.fixture(scope="module")
 def L():
     if not os.path.exists(ispa.LIB_PATH):
-        pytest.fail("libispa.so missing: run __graft_entry__.build() first")
+        pytest.fail("libispa.so missing: build it with python -m paper_2607_00712_amd.build first")
     return ispa.lib()
 
 
