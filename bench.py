@@ -40,6 +40,12 @@ WORKLOADS = {
                 window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
 }
 
+# the long streaming rollout at the 1.3B shape: 30 layers, half of them
+# L-Layers holding a window of 2 chunks, 60 chunks of 4680 queries
+ROLLOUT = dict(name="wan1.3b-rollout-60-chunks", heads=12, head_dim=128, n_q=4680, chunks=60, layers=30,
+               l_layers=15, window=9360, sink=0)
+KV_BYTES_PER_KEY = 2 * 2  # one bf16 key and one bf16 value element per hidden unit
+
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA
 PEAK_HBM_GBS = 8000.0
@@ -270,12 +276,136 @@ def cpu_baseline(w, budget_rows=512):
     }
 
 
+def rollout_run(reps=3, warmup=2):
+    """Streaming rollout (60 chunks, 30 layers): per chunk, every layer gets
+    fresh queries and appends its chunk of keys and values; F-Layers attend to
+    their whole cache (4680 n keys at chunk n), L-Layers to the ring of their
+    last 2 chunks (after the permanent eviction, Sec. 3.3). The all-F baseline
+    attends every layer to its whole cache: the F-Layers' launches are shared,
+    the L-Layers' full-cache launches are timed on the same keys and values.
+    Returns the JSON record."""
+    import synth
+    import paper_2607_00712_amd as ispa
+
+    w = ROLLOUT
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    H, n_q, win, sink = w["heads"], w["n_q"], w["window"], w["sink"]
+    D = H * w["head_dim"]
+    n_layers, n_l = w["layers"], w["l_layers"]
+    n_f = n_layers - n_l
+    cap = n_q * w["chunks"]
+    # full caches of every layer (an L-Layer's one only feeds the baseline and
+    # its own ring), and the L-Layers' rings of sink + window rows
+    kc = [torch.empty((cap, D), dtype=torch.bfloat16, device=dev) for _ in range(n_layers)]
+    vc = [torch.empty((cap, D), dtype=torch.bfloat16, device=dev) for _ in range(n_layers)]
+    rings = [(torch.empty((sink + win, D), dtype=torch.bfloat16, device=dev),
+              torch.empty((sink + win, D), dtype=torch.bfloat16, device=dev)) for _ in range(n_l)]
+    local = [None] * n_l
+    out = torch.empty((n_q, D), dtype=torch.float32, device=dev)
+    lse = torch.empty((H, n_q), dtype=torch.float32, device=dev)
+    per_key_layer = D * KV_BYTES_PER_KEY
+    res = {"chunk": [], "keys_f": [], "keys_l": [], "ispa_ms": [], "f_layers_ms": [], "l_layers_ms": [],
+           "all_f_ms": [], "kv_gb_ispa": [], "kv_gb_all_f": []}
+    fl_ispa = fl_allf = t_ispa = t_allf = 0.0
+    t_f60 = None
+    for n in range(1, w["chunks"] + 1):
+        N = n_q * n
+        qs = []
+        for layer in range(n_layers):
+            q, kn, vn = synth.rollout_chunk(layer, n, n_q, D, dev)
+            qs.append(q)
+            kc[layer][N - n_q:N].copy_(kn)
+            vc[layer][N - n_q:N].copy_(vn)
+            if layer >= n_f:
+                j = layer - n_f
+                if local[j] is None:
+                    local[j] = ispa.LocalKV(kc[layer], vc[layer], N, win, sink, ring=rings[j])
+                else:
+                    local[j].append(kn, vn)
+        torch.cuda.synchronize()
+
+        def f_layers():
+            for layer in range(n_f):
+                ispa.attn_chunk(qs[layer], kc[layer], vc[layer], N, N, H, out=out, lse=lse)
+
+        def l_layers():
+            for j in range(n_l):
+                r = local[j].rows
+                ispa.attn_chunk(qs[n_f + j], local[j].k, local[j].v, r, r, H, out=out, lse=lse)
+
+        def l_as_f():
+            for layer in range(n_f, n_layers):
+                ispa.attn_chunk(qs[layer], kc[layer], vc[layer], N, N, H, out=out, lse=lse)
+
+        for _ in range(warmup if n == 1 else 0):
+            f_layers(); l_layers(); l_as_f()
+        samples = []
+        for _ in range(reps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            ev[0].record(); f_layers(); ev[1].record(); l_layers(); ev[2].record(); l_as_f(); ev[3].record()
+            torch.cuda.synchronize()
+            samples.append([ev[i].elapsed_time(ev[i + 1]) for i in range(3)])
+        tf, tl, tx = (sorted(s[i] for s in samples)[len(samples) // 2] for i in range(3))
+        keys_l = min(N, win + min(sink, N))
+        res["chunk"].append(n)
+        res["keys_f"].append(N)
+        res["keys_l"].append(keys_l)
+        res["f_layers_ms"].append(round(tf, 4))
+        res["l_layers_ms"].append(round(tl, 4))
+        res["ispa_ms"].append(round(tf + tl, 4))
+        res["all_f_ms"].append(round(tf + tx, 4))
+        res["kv_gb_ispa"].append(round((n_f * N + n_l * keys_l) * per_key_layer / 1e9, 3))
+        res["kv_gb_all_f"].append(round(n_layers * N * per_key_layer / 1e9, 3))
+        fl_ispa += 4.0 * n_q * D * (n_f * N + n_l * keys_l)
+        fl_allf += 4.0 * n_q * D * n_layers * N
+        t_ispa += tf + tl
+        t_allf += tf + tx
+        if n == w["chunks"]:
+            t_f60 = tf / n_f
+        print(f"[rollout] chunk {n}: ISPA {tf + tl:.3f} ms, all-F {tf + tx:.3f} ms", file=sys.stderr, flush=True)
+    f60 = 4.0 * n_q * D * n_q * w["chunks"]
+    achieved = f60 / (t_f60 * 1e-3) / 1e12
+    return {
+        "metric": "streaming rollout attention TFLOP/s (15 F + 15 L layers, 60 chunks)",
+        "value": round(fl_ispa / (t_ispa * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": w["chunks"],
+        "warmup": warmup,
+        "ms_per_step": round(t_ispa / w["chunks"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w["name"], "heads": H, "head_dim": w["head_dim"], "chunk_queries": n_q,
+                   "layers": n_layers, "l_layers": n_l, "window": win, "sink": sink, "chunks": w["chunks"],
+                   "step": "one chunk: attention of every layer (F-Layers over the whole cache, L-Layers over "
+                           "their ring); median of %d timings per chunk" % reps},
+        "roofline": {"kernel": "attn_chunk_kernel<128> (F-Layer, full cache of 280800 keys, chunk 60)",
+                     "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "summary": {
+            "ispa_total_ms": round(t_ispa, 2), "all_f_total_ms": round(t_allf, 2),
+            "speedup_total": round(t_allf / t_ispa, 4),
+            "speedup_chunk60": round(res["all_f_ms"][-1] / res["ispa_ms"][-1], 4),
+            "flop_ispa": fl_ispa, "flop_all_f": fl_allf,
+            "all_f_tflops": round(fl_allf / (t_allf * 1e-3) / 1e12, 2),
+            "kv_ratio_chunk60": round(res["kv_gb_ispa"][-1] / res["kv_gb_all_f"][-1], 4),
+        },
+        "per_chunk": res,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="1.3b")
+    ap.add_argument("--workload", choices=sorted(WORKLOADS) + ["rollout"], default="1.3b",
+                    help="1.3b / 14b: one warmup step of one layer; rollout: the 60-chunk streaming "
+                         "rollout of 30 layers (per-chunk attention time and KV bytes against all F-Layers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy"],
                     default="all",
@@ -287,6 +417,9 @@ def main():
         sys.exit(2)
     if args.only == "hbm_copy":
         print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)
+        return
+    if args.workload == "rollout":
+        print(json.dumps(rollout_run(warmup=args.warmup)), flush=True)
         return
     w = WORKLOADS[args.workload]
     f = flops(w)

@@ -52,3 +52,10 @@ def chunk_qkv(workload, layer, chunk, n_q, cache_len, hidden, device="cpu",
         k[cache_len:] = 30.0
         v[cache_len:] = 1.0e4
     return q, k, v
+
+
+def rollout_chunk(layer, chunk, n_q, hidden, device="cpu", workload=5):
+    """One chunk of a streaming rollout for one layer: the chunk's queries and
+    the keys and values it appends to the layer's cache, each [n_q, hidden]
+    bf16, drawn fresh per (layer, chunk)."""
+    return tuple(normal((n_q, hidden), seed_of(workload, layer, chunk, t), device) for t in (Q, K, V))
