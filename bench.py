@@ -1,23 +1,28 @@
 """Benchmark of the ISPA hot path on one MI355X.
 
-One step is one pass of the whole hot path for one warmup chunk of one layer
-at the Wan-1.3B shape (12 heads x 128, d = 1536, chunk = 4680 queries):
+One step is one layer's warmup (T_warm = 12 latent frames = 4 chunks, Sec. 4.1)
+at the Wan-1.3B shape (12 heads x 128, d = 1536, chunk = 4680 queries): for
+each of the 4 chunks (distinct seeded inputs)
 
   1. F-Layer attention, dual stream: full cache of 7 chunks (32760 keys) and
      the local window of 2 chunks (9360 keys) from one pass;
   2. L-Layer attention over the local window only;
   3. statistics of the chunk: R = bf16(A_full - A_loc), G += X^T X,
      C += X^T R with X = bf16(A_loc) (4680 rows);
-  4. the closed-form solve dW = (G + 1e-3 I)^-1 C (d = 1536), which waits for
-     the device.
+
+then, once, 4. the closed-form solve dW = (G + 1e-3 I)^-1 C (d = 1536) over
+the 18720 accumulated rows, as the method solves once per layer at the end of
+its warmup (Sec. 3.2). The statistics restart at the next step (the next layer).
 
 Inputs are seeded synthetic N(0, 1) bf16 tensors already resident in HBM.
 `value` is the algorithmic TFLOP/s of the whole step (visible keys only for
 attention, the symmetric half of X^T X, D^3/3 + 2 D^2 D_out for the solve)
 divided by the measured step time. The roofline object covers the dominant
 call (the dual-stream attention: its kernel and, when the work is split over
-the chip, the merge kernel), timed with HIP events on the stream it runs on. `cpu_baseline` times the CPU oracle on a bounded sample of the same
-step. `--workload 14b` runs the 14B-like shape instead (40 heads, 98280 keys).
+the chip, the merge kernel), timed with HIP events on the stream it runs on.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same step.
+`--workload 14b` runs the 14B-like shape instead (40 heads, 98280 keys);
+`--workload rollout` the 60-chunk streaming rollout.
 """
 
 import argparse
@@ -34,9 +39,9 @@ if ROOT not in sys.path:
 import torch  # noqa: E402
 
 WORKLOADS = {
-    "1.3b": dict(name="wan1.3b-chunk-warmup-step", heads=12, head_dim=128, n_q=4680, cache_len=32760,
+    "1.3b": dict(name="wan1.3b-layer-warmup-step", heads=12, head_dim=128, n_q=4680, cache_len=32760,
                  window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
-    "14b": dict(name="14b-chunk-warmup-step", heads=40, head_dim=128, n_q=4680, cache_len=98280,
+    "14b": dict(name="14b-layer-warmup-step", heads=40, head_dim=128, n_q=4680, cache_len=98280,
                 window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
 }
 
@@ -80,7 +85,15 @@ def flops(w):
     return f
 
 
+def step_flops(w, f):
+    """Algorithmic flop of one step: T_warm chunks of attention and statistics, one solve."""
+    return w["t_warm_chunks"] * (f["attn_dual"] + f["attn_local"] + f["gram"]) + f["solve"]
+
+
 def gpu_run(w, steps, warmup, only="all"):
+    """Times `steps` layer warmups. Returns the wall-clock ms per step and the
+    per-part averages: ms per call for the attention calls and the statistics
+    (one per chunk), ms per solve."""
     import synth
     import paper_2607_00712_amd as ispa
 
@@ -88,7 +101,8 @@ def gpu_run(w, steps, warmup, only="all"):
     torch.cuda.set_device(dev)
     H, d = w["heads"], w["head_dim"]
     D = H * d
-    q, k, v = synth.chunk_qkv(2607, 0, 0, w["n_q"], w["cache_len"], D, dev)
+    n_chunks = w["t_warm_chunks"]
+    chunks = [synth.chunk_qkv(2607, 0, c, w["n_q"], w["cache_len"], D, dev) for c in range(n_chunks)]
     out = torch.empty((w["n_q"], D), dtype=torch.float32, device=dev)
     out_l = torch.empty_like(out)
     out_L = torch.empty_like(out)
@@ -101,45 +115,41 @@ def gpu_run(w, steps, warmup, only="all"):
     status_dev = torch.zeros((1,), dtype=torch.int32, device=dev)
 
     run = {p: only in ("all", p) for p in ("attn_dual", "attn_local", "accum_stats", "solve")}
-
-    # a layer's warmup is T_warm = 4 chunks (Sec. 4.1): the statistics restart
-    # every 4 steps, as for the next layer (at 14B one chunk has fewer rows
-    # than D, so G + lambda I accumulated without end would become singular in
-    # fp32 and the solve would report NOT_SPD)
-    chunk = [0]
+    names = ("attn_dual", "attn_local", "accum_stats")
 
     def step(ev=None):
+        # ev: per chunk 4 events around the three parts, then 1 after the solve
+        stats.reset()
+        for c, (q, k, v) in enumerate(chunks):
+            if ev is not None:
+                ev[3 * c].record()
+            if run["attn_dual"]:
+                ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"], dual=True,
+                                out=out, lse=lse, out_local=out_l, lse_local=lse_l)
+            if ev is not None:
+                ev[3 * c + 1].record()
+            if run["attn_local"]:
+                ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"],
+                                out=out_L, lse=lse_L)
+            if ev is not None:
+                ev[3 * c + 2].record()
+            if run["accum_stats"]:
+                stats.accum(out_l, out, out_l)
         if ev is not None:
-            ev[0].record()
-        if run["attn_dual"]:
-            ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"], dual=True,
-                            out=out, lse=lse, out_local=out_l, lse_local=lse_l)
-        if ev is not None:
-            ev[1].record()
-        if run["attn_local"]:
-            ispa.attn_chunk(q, k, v, w["cache_len"], w["window"], H, sink_len=w["sink"],
-                            out=out_L, lse=lse_L)
-        if ev is not None:
-            ev[2].record()
-        if run["accum_stats"]:
-            if chunk[0] % w["t_warm_chunks"] == 0:
-                stats.reset()
-            chunk[0] += 1
-            stats.accum(out_l, out, out_l)
-        if ev is not None:
-            ev[3].record()
+            ev[3 * n_chunks].record()
         if run["solve"]:
             # the solve that does not wait: eps and the status word stay in
             # device memory (a warmup reads the scores of all layers at once
             # for the ranking); checked once after the timed steps
             stats.solve_async(w["lam"], delta_w=dw, eps=eps_dev, status=status_dev)
         if ev is not None:
-            ev[4].record()
+            ev[3 * n_chunks + 1].record()
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    n_ev = 3 * n_chunks + 2
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
@@ -148,17 +158,17 @@ def gpu_run(w, steps, warmup, only="all"):
     t1 = time.perf_counter()
     parts = {"attn_dual": [], "attn_local": [], "accum_stats": [], "solve": []}
     for ev in events:
-        parts["attn_dual"].append(ev[0].elapsed_time(ev[1]))
-        parts["attn_local"].append(ev[1].elapsed_time(ev[2]))
-        parts["accum_stats"].append(ev[2].elapsed_time(ev[3]))
-        parts["solve"].append(ev[3].elapsed_time(ev[4]))
+        for c in range(n_chunks):
+            for j, name in enumerate(names):
+                parts[name].append(ev[3 * c + j].elapsed_time(ev[3 * c + j + 1]))
+        parts["solve"].append(ev[3 * n_chunks].elapsed_time(ev[3 * n_chunks + 1]))
     if run["solve"]:
         if int(status_dev.item()) != 0 or not math.isfinite(float(eps_dev.item())):
             raise RuntimeError("solve: G + lambda I not positive definite in the timed steps")
     avg = {k2: sum(v2) / len(v2) for k2, v2 in parts.items()}
     ms_step = (t1 - t0) * 1e3 / steps
     if only == "all":
-        avg["absorb"] = absorb_run(ispa, w, k, v, dw, dev)
+        avg["absorb"] = absorb_run(ispa, w, chunks[0][1], chunks[0][2], dw, dev)
     return ms_step, avg
 
 
@@ -261,16 +271,17 @@ def cpu_baseline(w, budget_rows=512):
     oracle.solve_modulation(G, st.C, w["lam"])
     t_solve = time.perf_counter() - t
     # scale each sampled part to a whole step
-    t_step = (t_attn / frac) + (t_stats / frac) + t_solve
-    total_flops = sum(f.values())
+    t_step = w["t_warm_chunks"] * ((t_attn / frac) + (t_stats / frac)) + t_solve
+    total_flops = step_flops(w, f)
     return {
         "value": total_flops / t_step / 1e12,
         "unit": "TFLOP/s",
         "cores": cores,
         "kind": "oracle",
         "sample": (f"fp64 numpy oracle: F-Layer dual + L-Layer attention and statistics for {budget_rows} "
-                   f"of {w['n_q']} query rows (all {H} heads, all keys), full {D}x{D} Cholesky solve; "
-                   f"attention and statistics time scaled by {w['n_q']}/{budget_rows}; measured "
+                   f"of {w['n_q']} query rows of one chunk (all {H} heads, all keys), full {D}x{D} Cholesky solve; "
+                   f"attention and statistics time scaled by {w['n_q']}/{budget_rows} and by the "
+                   f"{w['t_warm_chunks']} chunks of a step; measured "
                    f"{t_attn:.2f}s + {t_stats:.2f}s + {t_solve:.2f}s"),
         "ms_per_step_extrapolated": t_step * 1e3,
     }
@@ -424,7 +435,7 @@ def main():
     w = WORKLOADS[args.workload]
     f = flops(w)
     ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only)
-    total = sum(f.values())
+    total = step_flops(w, f)
     value = total / (ms_step * 1e-3) / 1e12
     attn_ms = avg["attn_dual"]
     mt = MEASURED_TRAFFIC.get(args.workload)
@@ -448,7 +459,9 @@ def main():
             "heads": w["heads"], "head_dim": w["head_dim"], "chunk_queries": w["n_q"],
             "cache_len": w["cache_len"], "window": w["window"], "sink": w["sink"],
             "d": w["heads"] * w["head_dim"], "lambda": w["lam"],
-            "step": "F-Layer dual attention + L-Layer attention + accum_stats + solve (statistics restart every 4 chunks)",
+            "step": "one layer's warmup: 4 chunks x (F-Layer dual attention + L-Layer attention + accum_stats), "
+                    "then one solve over the 18720 accumulated rows",
+            "t_warm_chunks": w["t_warm_chunks"],
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
@@ -470,7 +483,9 @@ def main():
             "gram_tflops": round(f["gram"] / avg["accum_stats"] / 1e9, 1),
             "solve_ms": round(avg["solve"], 4),
             "solve_tflops": round(f["solve"] / avg["solve"] / 1e9, 2),
+            "per": "attention and accum_stats: ms per chunk call (4 per step); solve: ms per step",
             "flop": {k2: v2 for k2, v2 in f.items()},
+            "flop_step": total,
             "absorb": avg.get("absorb"),
         },
     }
