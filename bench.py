@@ -85,9 +85,17 @@ def flops(w):
     return f
 
 
-def step_flops(w, f):
-    """Algorithmic flop of one step: T_warm chunks of attention and statistics, one solve."""
-    return w["t_warm_chunks"] * (f["attn_dual"] + f["attn_local"] + f["gram"]) + f["solve"]
+def step_flops(w, f, only="all"):
+    """Algorithmic flop of one step: T_warm chunks of attention and statistics,
+    one solve (with `only`, of that part alone)."""
+    per_chunk = {"attn_dual": f["attn_dual"], "attn_local": f["attn_local"], "accum_stats": f["gram"]}
+    total = 0.0
+    for part, fl in per_chunk.items():
+        if only in ("all", part):
+            total += w["t_warm_chunks"] * fl
+    if only in ("all", "solve"):
+        total += f["solve"]
+    return total
 
 
 def gpu_run(w, steps, warmup, only="all"):
@@ -435,7 +443,7 @@ def main():
     w = WORKLOADS[args.workload]
     f = flops(w)
     ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only)
-    total = step_flops(w, f)
+    total = step_flops(w, f, args.only)
     value = total / (ms_step * 1e-3) / 1e12
     attn_ms = avg["attn_dual"]
     mt = MEASURED_TRAFFIC.get(args.workload)
