@@ -40,9 +40,9 @@ import torch  # noqa: E402
 
 WORKLOADS = {
     "1.3b": dict(name="wan1.3b-layer-warmup-step", heads=12, head_dim=128, n_q=4680, cache_len=32760,
-                 window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
+                 window=9360, sink=0, lam=1e-3, t_warm_chunks=4, n_layers=30),
     "14b": dict(name="14b-layer-warmup-step", heads=40, head_dim=128, n_q=4680, cache_len=98280,
-                window=9360, sink=0, lam=1e-3, t_warm_chunks=4),
+                window=9360, sink=0, lam=1e-3, t_warm_chunks=4, n_layers=40),
 }
 
 # the long streaming rollout at the 1.3B shape: 30 layers, half of them
@@ -177,6 +177,7 @@ def gpu_run(w, steps, warmup, only="all"):
     ms_step = (t1 - t0) * 1e3 / steps
     if only == "all":
         avg["absorb"] = absorb_run(ispa, w, chunks[0][1], chunks[0][2], dw, dev)
+        avg["solve_all_layers"] = solve_all_run(ispa, w, stats, dev)
     return ms_step, avg
 
 
@@ -225,6 +226,59 @@ def absorb_run(ispa, w, k, v, dw, dev, reps=10):
             "quantize_ms": round(qt, 4), "quantize_gbs": round(w["n_q"] * D * (2 + 1) / qt / 1e6, 1),
             "project_w8a8_ms": round(pj8, 4), "project_w8a8_tops": round(pj_flop / pj8 / 1e9, 1),
             "project_w8a8_frac": round(pj_flop / pj8 / 1e9 / PEAK_INT8_TOPS, 4)}
+
+
+def solve_all_run(ispa, w, stats, dev, reps=3):
+    """The end of warmup solves every layer (Sec. 3.3, the eps ranking needs
+    all of them): n_layers systems of the step's size (copies of the step's
+    G, C and ||R||^2) by one batched call (ispa_solve_modulation_batch) and by
+    one call per layer, timed with HIP events."""
+    D = w["heads"] * w["head_dim"]
+    n = w["n_layers"]
+    G, C, S, _ = stats.views()
+    sb = ispa.StatsBatch(n, D, D, max_rows=1, device=dev)
+    for st in sb.layers:
+        g, c, s, _ = st.views()
+        g.copy_(G)
+        c.copy_(C)
+        s.copy_(S)
+    dw = torch.empty((n, D, D), dtype=torch.float32, device=dev)
+    eps = torch.empty((n,), dtype=torch.float64, device=dev)
+    status = torch.empty((n,), dtype=torch.int32, device=dev)
+
+    def batched():
+        sb.solve(w["lam"], delta_w=dw, eps=eps, status=status)
+
+    def one_by_one():
+        for i, st in enumerate(sb.layers):
+            st.solve_async(w["lam"], delta_w=dw[i], eps=eps[i:i + 1], status=status[i:i + 1])
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return sorted(ms)[len(ms) // 2]
+
+    t_b = timed(batched)
+    ok_b = int(status.sum().item()) == 0
+    t_1 = timed(one_by_one)
+    ok_1 = int(status.sum().item()) == 0
+    sb.close()
+    del sb
+    if not (ok_b and ok_1):
+        raise RuntimeError("solve of all layers: G + lambda I not positive definite")
+    flop = n * (D ** 3 / 3.0 + 2.0 * D * D * D)
+    return {"layers": n, "batched_ms": round(t_b, 3), "one_by_one_ms": round(t_1, 3),
+            "speedup": round(t_1 / t_b, 3), "batched_tflops": round(flop / t_b / 1e9, 2),
+            "batched_frac_fp32_peak": round(flop / t_b / 1e9 / 157.3, 4),
+            "one_by_one_tflops": round(flop / t_1 / 1e9, 2)}
 
 
 def hbm_copy(steps, warmup, nbytes=1 << 30):
@@ -495,6 +549,7 @@ def main():
             "flop": {k2: v2 for k2, v2 in f.items()},
             "flop_step": total,
             "absorb": avg.get("absorb"),
+            "solve_all_layers": avg.get("solve_all_layers"),
         },
     }
     if args.only != "all":

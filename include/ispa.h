@@ -253,6 +253,32 @@ int ispa_solve_modulation(ispa_stats* handle, float lambda, float* delta_w, doub
 int ispa_solve_modulation_async(ispa_stats* handle, float lambda, float* delta_w, double* eps_dev,
                                 int32_t* status_dev);
 
+/*
+ * The closed-form solves of several layers at once. At the end of warmup the
+ * method computes dW and eps of every layer so that the layers can be ranked
+ * by eps (Sec. 3.3); each layer's solve is the work of
+ * ispa_solve_modulation_async (same arithmetic, bitwise the same results), but
+ * one launch per step of the factorisation and of the sweeps covers every
+ * layer, so the latency-bound chain of panel factorisations is paid once.
+ *   handles     host array of n_layers statistics handles, 1 <= n_layers <=
+ *               4096, with equal d_in, d_out and max_rows and equally spaced
+ *               workspaces: workspace(i) = workspace(0) + i * stride, stride >=
+ *               ispa_stats_workspace_bytes (handles created on consecutive
+ *               equal slices of one buffer); all work is enqueued on the stream
+ *               of handles[0]
+ *   lambda      ridge weight, >= 0
+ *   delta_w     fp32 device output: n_layers consecutive [d_in, d_out]
+ *               row-major blocks, layer i at delta_w + i * d_in * d_out
+ *   eps_dev     device double [n_layers] (8-byte aligned) or NULL: eps of each
+ *               layer (Eq. 6)
+ *   status_dev  device int32 [n_layers] (4-byte aligned) or NULL: 0, or 1 when
+ *               that layer's G + lambda I had a pivot that was not positive
+ * Argument errors (INVALID_ARG, or STATE for a bad handle) are returned before
+ * anything is enqueued. Asynchronous; every layer's G and C are left intact.
+ */
+int ispa_solve_modulation_batch(ispa_stats* const* handles, int32_t n_layers, float lambda, float* delta_w,
+                                double* eps_dev, int32_t* status_dev);
+
 /* ---------------------------------------------------------- absorption */
 /*
  * Instance-specific layer selection (Sec. 3.3): the k layers with the lowest

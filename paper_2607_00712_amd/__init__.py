@@ -21,7 +21,8 @@ import os
 
 import torch
 
-__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "status_string",
+__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "StatsBatch",
+           "status_string",
            "select_layers", "inject_modulation", "LocalKV", "project", "quantize_rows", "project_w8a8",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
            "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
@@ -68,6 +69,7 @@ _SIGNATURES = {
     "ispa_accum_stats": (ctypes.c_int, [_c_p, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64]),
     "ispa_solve_modulation": (ctypes.c_int, [_c_p, _c_f32, _c_p, ctypes.POINTER(ctypes.c_double)]),
     "ispa_solve_modulation_async": (ctypes.c_int, [_c_p, _c_f32, _c_p, _c_p, _c_p]),
+    "ispa_solve_modulation_batch": (ctypes.c_int, [ctypes.POINTER(_c_p), _c_i32, _c_f32, _c_p, _c_p, _c_p]),
 }
 
 _lib = None
@@ -357,6 +359,67 @@ class Stats:
             self.close()
         except Exception:
             pass
+
+
+class StatsBatch:
+    """The warmup statistics of several layers on one workspace (equal
+    256-byte-aligned slices, one statistics handle per layer), solved together
+    by ispa_solve_modulation_batch. ``layers[i]`` is a Stats of layer i."""
+
+    def __init__(self, n_layers, d_in, d_out, max_rows=4680, device=None):
+        L = lib()
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        if dev.type != "cuda":
+            raise ValueError("StatsBatch lives on a HIP device")
+        self.device = dev if dev.index is not None else torch.device("cuda", torch.cuda.current_device())
+        self.n_layers = int(n_layers)
+        self.d_in, self.d_out, self.max_rows = int(d_in), int(d_out), int(max_rows)
+        if self.n_layers < 1:
+            raise ValueError("n_layers must be positive")
+        nbytes = L.ispa_stats_workspace_bytes(self.d_in, self.d_out, self.max_rows)
+        if nbytes == 0:
+            raise IspaError(ISPA_ERR_INVALID_ARG, "ispa_stats_workspace_bytes")
+        self.stride = (nbytes + 255) // 256 * 256
+        self.workspace = torch.empty(self.stride * self.n_layers + 256, dtype=torch.uint8, device=self.device)
+        pad = (-self.workspace.data_ptr()) % 256
+        self.layers = []
+        for i in range(self.n_layers):
+            st = Stats.__new__(Stats)
+            st.device, st.d_in, st.d_out, st.max_rows = self.device, self.d_in, self.d_out, self.max_rows
+            st.workspace = self.workspace
+            st._ws = self.workspace[pad + i * self.stride: pad + i * self.stride + nbytes]
+            st._h = ctypes.c_void_p(0)
+            _check(L.ispa_stats_create(ctypes.byref(st._h), _ptr(st._ws), nbytes, self.d_in, self.d_out,
+                                       self.max_rows, _stream(self.device)), "ispa_stats_create")
+            self.layers.append(st)
+
+    def solve(self, lam=1e-3, delta_w=None, eps=None, status=None):
+        """dW, eps and the status word of every layer (ispa_solve_modulation_batch),
+        without waiting: delta_w [n_layers, d_in, d_out] fp32, eps fp64 [n_layers],
+        status int32 [n_layers] (0, or 1 when that layer's G + lam I was not
+        positive definite), valid once the stream has run the work."""
+        n = self.n_layers
+        if delta_w is None:
+            delta_w = torch.empty((n, self.d_in, self.d_out), dtype=torch.float32, device=self.device)
+        if eps is None:
+            eps = torch.empty((n,), dtype=torch.float64, device=self.device)
+        if status is None:
+            status = torch.empty((n,), dtype=torch.int32, device=self.device)
+        _require(delta_w, "delta_w", torch.float32, self.device, ndim=3)
+        if tuple(delta_w.shape) != (n, self.d_in, self.d_out):
+            raise ValueError(f"delta_w must have shape {(n, self.d_in, self.d_out)}")
+        _require(eps, "eps", torch.float64, self.device, ndim=1)
+        _require(status, "status", torch.int32, self.device, ndim=1)
+        if eps.shape[0] < n or status.shape[0] < n:
+            raise ValueError("eps and status need n_layers entries")
+        hs = (_c_p * n)(*[st._handle() for st in self.layers])
+        _check(lib().ispa_solve_modulation_batch(hs, n, float(lam), _ptr(delta_w), _ptr(eps), _ptr(status)),
+               "ispa_solve_modulation_batch")
+        return delta_w, eps, status
+
+    def close(self):
+        for st in self.layers:
+            st.close()
 
 
 def select_layers(eps, k):

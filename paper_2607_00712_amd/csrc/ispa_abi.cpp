@@ -359,6 +359,39 @@ int ispa_solve_modulation_async(ispa_stats* h, float lambda, float* delta_w, dou
   return enqueue_solve(h, lambda, delta_w, eps_dev, status_dev);
 }
 
+int ispa_solve_modulation_batch(ispa_stats* const* handles, int32_t n_layers, float lambda, float* delta_w,
+                                double* eps_dev, int32_t* status_dev) {
+  if (!handles || n_layers < 1 || n_layers > 4096) return ISPA_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < n_layers; ++i)
+    if (!valid_handle(handles[i])) return ISPA_ERR_STATE;
+  const ispa_stats* h = handles[0];
+  const int64_t stride = n_layers > 1 ? (int64_t)(handles[1]->ws - h->ws) : 0;
+  if (n_layers > 1 && stride < (int64_t)h->lay.total) return ISPA_ERR_INVALID_ARG;
+  for (int32_t i = 1; i < n_layers; ++i) {
+    const ispa_stats* g = handles[i];
+    if (g->d_in != h->d_in || g->d_out != h->d_out || g->max_rows != h->max_rows) return ISPA_ERR_INVALID_ARG;
+    if (g->ws != h->ws + (size_t)i * (size_t)stride) return ISPA_ERR_INVALID_ARG;
+  }
+  if (!delta_w || !aligned16(delta_w)) return ISPA_ERR_INVALID_ARG;
+  if (!(lambda >= 0.f) || isinf(lambda)) return ISPA_ERR_INVALID_ARG;
+  if (((uintptr_t)eps_dev & 7u) || ((uintptr_t)status_dev & 3u)) return ISPA_ERR_INVALID_ARG;
+  ispa::SolveWork w;
+  w.L = (float*)(h->ws + h->lay.L);
+  w.work = (float*)(h->ws + h->lay.W);
+  w.dinv = (float*)(h->ws + h->lay.Dinv);
+  w.status = (int*)(h->ws + h->lay.status);
+  w.scalars = (double*)(h->ws + h->lay.scalars);
+  w.eps_out = eps_dev;
+  w.status_out = status_dev;
+  w.n_layers = n_layers;
+  w.ws_stride = stride;
+  w.dw_stride = (int64_t)h->d_in * h->d_out * (int64_t)sizeof(float);
+  const float* G = (const float*)(h->ws + h->lay.G);
+  const float* C = (const float*)(h->ws + h->lay.C);
+  return ispa::launch_solve(G, C, h->d_in, h->d_out, lambda, delta_w, w, h->stream) == hipSuccess ? ISPA_OK
+                                                                                                   : ISPA_ERR_HIP;
+}
+
 
 int ispa_select_layers(const double* eps, int32_t n_layers, int32_t k, int32_t* selected) {
   if (!eps || n_layers < 0 || n_layers > (1 << 20) || k < 0 || k > n_layers || (k > 0 && !selected))

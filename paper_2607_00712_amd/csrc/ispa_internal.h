@@ -119,8 +119,14 @@ struct SolveWork {
   float* dinv;       // [ceil(d/64), 64, 64] inverses of the diagonal blocks of L
   int* status;       // device int: 0 ok, 1 not SPD
   double* scalars;   // device: [0] s (input), then [2] <dW, C>, [3] ||dW||^2, [4] eps, [5] status
-  double* eps_out = nullptr;  // optional device copies of eps and the status word
+  double* eps_out = nullptr;  // optional device copies of eps and the status word ([n_layers] each)
   int* status_out = nullptr;
+  // batched solves: n_layers systems whose workspaces (every pointer above
+  // except the outputs) are ws_stride bytes apart and whose dW are dw_stride
+  // bytes apart
+  int n_layers = 1;
+  int64_t ws_stride = 0;
+  int64_t dw_stride = 0;
 };
 size_t solve_dinv_bytes(int d);
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda,

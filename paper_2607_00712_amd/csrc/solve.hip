@@ -28,6 +28,10 @@
 //   the forward and for the backward sweep, with no diagonal work in them.
 // Every product is fp32 MFMA (v_mfma_f32_32x32x2f32); the sweeps' GEMM stages
 // its operands HBM -> LDS with direct buffer loads in a 4-deep ring.
+// Several layers at once (the end of warmup solves every layer): every kernel
+// takes its layer from the last grid dimension and offsets its workspace
+// pointers by the layers' workspace stride (dW by its own stride), so one
+// launch per step covers all layers with each layer's arithmetic unchanged.
 #include "ispa_internal.h"
 
 #include <math.h>
@@ -40,6 +44,13 @@ constexpr int kThreads = 256;
 constexpr int kLd = 65;  // LDS row stride (floats) of a 64 x 64 tile
 
 typedef float Tile[kNb][kLd];
+
+// Batched solves (one per layer, the layer from the last grid dimension): the
+// layers' workspaces are `bytes` apart.
+template <class T>
+__device__ __forceinline__ T* at_layer(T* p, int64_t bytes, int layer) {
+  return (T*)((char*)p + bytes * layer);
+}
 
 __device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
@@ -307,7 +318,10 @@ __device__ __forceinline__ void tri_index(int t, int& ti, int& tj) {
 }
 
 // L = lower(G) + lambda I (upper part zero), status = 0.
-__global__ void solve_init_kernel(const float* G, float* L, int n, float lambda, int* status) {
+__global__ void solve_init_kernel(const float* G, float* L, int n, float lambda, int* status, int64_t ws) {
+  G = at_layer(G, ws, blockIdx.y);
+  L = at_layer(L, ws, blockIdx.y);
+  status = at_layer(status, ws, blockIdx.y);
   const int64_t nn = (int64_t)n * n;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nn; i += (int64_t)gridDim.x * blockDim.x) {
     const int r = (int)(i / n), c = (int)(i % n);
@@ -382,9 +396,13 @@ __device__ void trailing_2x2(float* L, int n, int nblk, int k, int R, int T, Til
 // Cholesky launch k (k = -1 .. nblk - 2): workgroups 0 .. m - 1 own the next
 // panel column, blocks (k + 1 + i, k + 1); the others the trailing triangle from
 // block k + 2 in 2 x 2 groups of blocks (the first launch has no trailing part).
-__global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int* status) {
+__global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int* status,
+                                                            int64_t ws) {
   __shared__ __attribute__((aligned(16))) Tile tiles[6];
   __shared__ int bad;
+  L = at_layer(L, ws, blockIdx.y);
+  Dinv = at_layer(Dinv, ws, blockIdx.y);
+  status = at_layer(status, ws, blockIdx.y);
   const int nblk = (n + kNb - 1) / kNb;
   const int m = nblk - 1 - k;
   if ((int)blockIdx.x >= m) {
@@ -466,9 +484,13 @@ __device__ __forceinline__ void quad_put(Tile& D, const f32x16& acc, float sign)
 // X_bb = Dinv_b and, for a > b, X_ab = -Dinv_a sum_{c=b}^{a-1} L_ac X_cb (64-block
 // indices inside the 256-block). Writes the full 256 x 64 strip of X_I (zeros
 // above the diagonal and in 64-blocks past the end of the matrix).
-__global__ __launch_bounds__(kThreads) void inv256_kernel(const float* L, const float* Dinv, float* Xinv, int n) {
+__global__ __launch_bounds__(kThreads) void inv256_kernel(const float* L, const float* Dinv, float* Xinv, int n,
+                                                         int64_t ws) {
   __shared__ Tile Xc[4];
   __shared__ Tile U;
+  L = at_layer(L, ws, blockIdx.z);
+  Dinv = at_layer(Dinv, ws, blockIdx.z);
+  Xinv = at_layer(Xinv, ws, blockIdx.z);
   const int nblk = (n + kNb - 1) / kNb;
   const int I = blockIdx.x, b = blockIdx.y;
   const int g0 = I * 4;                       // first 64-block of the 256-block
@@ -513,8 +535,9 @@ __global__ __launch_bounds__(kThreads) void inv256_kernel(const float* L, const 
 
 // Upper part of L from Lh: U[c][r] = L[r][c] for every (r, c) whose 256-block
 // row is below its 256-block column. One 64 x 64 tile per workgroup.
-__global__ __launch_bounds__(kThreads) void mirror_kernel(float* L, int n) {
+__global__ __launch_bounds__(kThreads) void mirror_kernel(float* L, int n, int64_t ws) {
   __shared__ Tile T;
+  L = at_layer(L, ws, blockIdx.y);
   const int nblk = (n + kNb - 1) / kNb;
   const int tr = blockIdx.x / nblk, tc = blockIdx.x % nblk;
   if (tr / 4 <= tc / 4) return;
@@ -545,6 +568,7 @@ struct GemmJob {
   int64_t lda, ldc;
   int sub;                    // 1: C -= A B, 0: C = A B
   const float* Cin = nullptr;  // with sub: read the minuend here instead of C (same ldc)
+  int64_t la = 0, lc = 0;      // bytes per layer (blockIdx.z) of A and of C / Cin
 };
 struct GemmArgs {
   GemmJob job[2];
@@ -554,6 +578,7 @@ struct GemmArgs {
   int64_t ldb;
   int64_t batch_a, batch_b, batch_c;
   int batch_dm;
+  int64_t lb;  // bytes per layer (blockIdx.z) of B
 };
 
 template <int WM, int WN, int QM, int QN, bool A_MK>
@@ -583,9 +608,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
   const int sub = second ? g.job[1].sub : g.job[0].sub;
   const int m0 = (t / tiles_n) * TM, n0 = (t % tiles_n) * TN;
   if (m0 >= M) return;
-  A += blockIdx.y * g.batch_a;
-  const float* B = g.B + blockIdx.y * g.batch_b;
-  C += blockIdx.y * g.batch_c;
+  const int layer = blockIdx.z;
+  A = at_layer(A, second ? g.job[1].la : g.job[0].la, layer) + blockIdx.y * g.batch_a;
+  const float* B = at_layer(g.B, g.lb, layer) + blockIdx.y * g.batch_b;
+  C = at_layer(C, second ? g.job[1].lc : g.job[0].lc, layer) + blockIdx.y * g.batch_c;
   const int N = g.N, K = g.K;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -706,8 +732,11 @@ __device__ __forceinline__ void block_sum2(double& a, double& b, double (*red)[k
   }
 }
 __global__ __launch_bounds__(kThreads) void eps_partial_kernel(const float* dw, const float* C, int64_t n,
-                                                               double* part) {
+                                                               double* part, int64_t ws, int64_t dws) {
   __shared__ double red[2][kThreads / 64];
+  dw = at_layer(dw, dws, blockIdx.y);
+  C = at_layer(C, ws, blockIdx.y);
+  part = at_layer(part, ws, blockIdx.y);
   double a = 0, b = 0;
   const int64_t n4 = n / 4;
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n4; i += (int64_t)gridDim.x * kThreads) {
@@ -731,8 +760,12 @@ __global__ __launch_bounds__(kThreads) void eps_partial_kernel(const float* dw, 
 // when given, receive eps and the status word as well.
 __global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part, int n_part, double* sc,
                                                              double lambda, const int* status, double* eps_out,
-                                                             int* status_out) {
+                                                             int* status_out, int64_t ws) {
   __shared__ double red[2][kThreads / 64];
+  const int layer = blockIdx.y;
+  part = at_layer(part, ws, layer);
+  sc = at_layer(sc, ws, layer);
+  status = at_layer(status, ws, layer);
   double a = 0, b = 0;
   for (int i = threadIdx.x; i < n_part; i += kThreads) {
     a += part[2 * i];
@@ -746,8 +779,8 @@ __global__ __launch_bounds__(kThreads) void eps_final_kernel(const double* part,
     sc[3] = b;
     sc[4] = e;
     sc[5] = (double)st;
-    if (eps_out) *eps_out = e;
-    if (status_out) *status_out = st;
+    if (eps_out) eps_out[layer] = e;
+    if (status_out) status_out[layer] = st;
   }
 }
 
@@ -903,7 +936,14 @@ __global__ __launch_bounds__(kThreads) void gemm_ring_kernel(GemmArgs g) {
   t.m0 = (tt / tiles_n) * TM;
   t.n0 = (tt % tiles_n) * TN;
   if (t.m0 >= t.M) return;
-  t.B = g.B;
+  {
+    const int layer = blockIdx.z;
+    const int64_t lc = second ? g.job[1].lc : g.job[0].lc;
+    t.A = at_layer(t.A, second ? g.job[1].la : g.job[0].la, layer);
+    C = at_layer(C, lc, layer);
+    Cin = at_layer(Cin, lc, layer);
+  }
+  t.B = at_layer(g.B, g.lb, blockIdx.z);
   t.ldb = g.ldb;
   t.N = g.N;
   t.K = g.K;
@@ -971,15 +1011,15 @@ size_t solve_dinv_bytes(int d) {
 
 namespace {
 
-// Launches C (-)= A B over 64 x 64 output tiles.
-hipError_t launch_gemm(const GemmArgs& g, int batches, hipStream_t stream) {
+// Launches C (-)= A B over 64 x 64 output tiles, for `layers` layers.
+hipError_t launch_gemm(const GemmArgs& g, int layers, hipStream_t stream) {
   int tiles = 0;
   for (int j = 0; j < g.n_jobs; ++j) tiles += ((g.job[j].M + 63) / 64) * ((g.N + 63) / 64);
   // 64 x 64 tiles at every size: 32 KB of LDS, so several workgroups share a CU
   // and hide each other's load latency, and the last round is finely grained
   // (measured against 128 x 128 and 128 x 64 tiles: the 5120-row solve takes
   // 5.1 ms with 64 x 64 tiles throughout, 6.2 ms with 128 x 128)
-  hipLaunchKernelGGL((gemm_ring_kernel<2, 2, 1, 1>), dim3(tiles, batches), dim3(kThreads), 0, stream, g);
+  hipLaunchKernelGGL((gemm_ring_kernel<2, 2, 1, 1>), dim3(tiles, 1, layers), dim3(kThreads), 0, stream, g);
   return hipGetLastError();
 }
 
@@ -993,30 +1033,36 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
   float* pinv = xinv + (size_t)nb * kBb * kBb;       // [nb][256][256]
   float* L = w.L;
   float* Y = w.work;
+  // layers: workspaces (G, C, L, Y, the inverses, status, scalars) `ws` bytes
+  // apart, the layers' dW `dws` bytes apart
+  const int nl = w.n_layers;
+  const int64_t ws = w.ws_stride, dws = w.dw_stride;
   {
     const int64_t total = (int64_t)d * d;
     int grid = (int)((total + 255) / 256);
     if (grid > 8192) grid = 8192;
-    hipLaunchKernelGGL(solve_init_kernel, dim3(grid), dim3(256), 0, stream, G, L, d, lambda, w.status);
+    hipLaunchKernelGGL(solve_init_kernel, dim3(grid, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
   }
   for (int k = -1; k <= nblk - 2; ++k) {
     const int m = nblk - 1 - k;                   // blocks of the next panel column
     const int groups = (nblk - 2 - k + 1) / 2;    // 2 x 2 groups per side of the trailing triangle
     const int grid = m + (k < 0 ? 0 : groups * (groups + 1) / 2);
-    hipLaunchKernelGGL(chol_step_kernel, dim3(grid), dim3(kThreads), 0, stream, L, w.dinv, d, k, w.status);
+    hipLaunchKernelGGL(chol_step_kernel, dim3(grid, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, w.status, ws);
   }
   // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above
-  hipLaunchKernelGGL(inv256_kernel, dim3(nb, 4), dim3(kThreads), 0, stream, L, w.dinv, xinv, d);
+  hipLaunchKernelGGL(inv256_kernel, dim3(nb, 4, nl), dim3(kThreads), 0, stream, L, w.dinv, xinv, d, ws);
   {
     GemmArgs g = {};
     g.job[0] = GemmJob{xinv, pinv, kBb, kBb, kBb, 0};
+    g.job[0].la = g.job[0].lc = ws;
+    g.lb = ws;
     g.n_jobs = 1;
     g.B = xinv;
     g.N = kBb;
     g.K = kBb;
     g.ldb = kBb;
     g.batch_a = g.batch_b = g.batch_c = (int64_t)kBb * kBb;
-    hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 1, false>), dim3(16, nb), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 1, false>), dim3(16, nb, nl), dim3(kThreads), 0, stream, g);
   }
   if (nb > 1) {
     // Lh_rI = L_rI X_I in place: a workgroup owns 32 rows x the whole 256-block
@@ -1024,6 +1070,8 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     GemmArgs g = {};
     float* first = L + (int64_t)kBb * d;  // rows of block 1, columns of block 0
     g.job[0] = GemmJob{first, first, d - kBb, d, d, 0};
+    g.job[0].la = g.job[0].lc = ws;
+    g.lb = ws;
     g.n_jobs = 1;
     g.B = xinv;
     g.N = kBb;
@@ -1032,9 +1080,9 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     g.batch_a = g.batch_c = (int64_t)kBb * d + kBb;
     g.batch_b = (int64_t)kBb * kBb;
     g.batch_dm = -kBb;
-    hipLaunchKernelGGL((gemm_kernel<1, 4, 1, 2, true>), dim3((d - kBb + 31) / 32, nb - 1), dim3(kThreads), 0,
+    hipLaunchKernelGGL((gemm_kernel<1, 4, 1, 2, true>), dim3((d - kBb + 31) / 32, nb - 1, nl), dim3(kThreads), 0,
                        stream, g);
-    hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk), dim3(kThreads), 0, stream, L, d);
+    hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk, nl), dim3(kThreads), 0, stream, L, d, ws);
   }
   // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I
   for (int I = 0; I < nb; ++I) {
@@ -1045,16 +1093,22 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     // the first step reads the right-hand side C itself (Y = C before any update)
     const float* Yin = I == 0 ? C : Y;
     if (below > 0) {
-      g.job[j++] = GemmJob{L + (int64_t)I * kBb * d + (int64_t)(I + 1) * kBb, Y + (int64_t)(I + 1) * kBb * d_out,
-                           below, d, d_out, 1, Yin + (int64_t)(I + 1) * kBb * d_out};
+      g.job[j] = GemmJob{L + (int64_t)I * kBb * d + (int64_t)(I + 1) * kBb, Y + (int64_t)(I + 1) * kBb * d_out,
+                         below, d, d_out, 1, Yin + (int64_t)(I + 1) * kBb * d_out};
+      g.job[j].la = g.job[j].lc = ws;
+      ++j;
     }
-    g.job[j++] = GemmJob{pinv + (int64_t)I * kBb * kBb, delta_w + (int64_t)I * kBb * d_out, kI, kBb, d_out, 0};
+    g.job[j] = GemmJob{pinv + (int64_t)I * kBb * kBb, delta_w + (int64_t)I * kBb * d_out, kI, kBb, d_out, 0};
+    g.job[j].la = ws;
+    g.job[j].lc = dws;
+    ++j;
     g.n_jobs = j;
+    g.lb = ws;
     g.B = Yin + (int64_t)I * kBb * d_out;
     g.N = d_out;
     g.K = kI;
     g.ldb = d_out;
-    const hipError_t e = launch_gemm(g, 1, stream);
+    const hipError_t e = launch_gemm(g, nl, stream);
     if (e != hipSuccess) return e;
   }
   // backward sweep: dW_I -= Lh_JI^T dW_J (I < J)
@@ -1062,19 +1116,23 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     const int kJ = min(kBb, d - J * kBb);
     GemmArgs g = {};
     g.job[0] = GemmJob{L + (int64_t)J * kBb * d, delta_w, J * kBb, d, d_out, 1};
+    g.job[0].la = ws;
+    g.job[0].lc = dws;
+    g.lb = dws;
     g.n_jobs = 1;
     g.B = delta_w + (int64_t)J * kBb * d_out;
     g.N = d_out;
     g.K = kJ;
     g.ldb = d_out;
-    const hipError_t e = launch_gemm(g, 1, stream);
+    const hipError_t e = launch_gemm(g, nl, stream);
     if (e != hipSuccess) return e;
   }
   // the P_I area is free once the forward sweep has run: it holds the partial sums
   const int64_t n = (int64_t)d * d_out;
-  hipLaunchKernelGGL(eps_partial_kernel, dim3(kEpsBlocks), dim3(kThreads), 0, stream, delta_w, C, n, (double*)pinv);
-  hipLaunchKernelGGL(eps_final_kernel, dim3(1), dim3(kThreads), 0, stream, (const double*)pinv, kEpsBlocks,
-                     w.scalars, (double)lambda, (const int*)w.status, w.eps_out, w.status_out);
+  hipLaunchKernelGGL(eps_partial_kernel, dim3(kEpsBlocks, nl), dim3(kThreads), 0, stream, delta_w, C, n,
+                     (double*)pinv, ws, dws);
+  hipLaunchKernelGGL(eps_final_kernel, dim3(1, nl), dim3(kThreads), 0, stream, (const double*)pinv, kEpsBlocks,
+                     w.scalars, (double)lambda, (const int*)w.status, w.eps_out, w.status_out, ws);
   return hipGetLastError();
 }
 

@@ -164,3 +164,14 @@ def test_async_solve_argument_errors(L):
     # checked before anything is enqueued (no handle: state error; bad pointers)
     p = lambda v: ctypes.c_void_p(v)
     assert L.ispa_solve_modulation_async(None, 1e-3, p(256), None, None) == ispa.ISPA_ERR_STATE
+
+
+def test_batch_solve_argument_errors(L):
+    # checked before anything is enqueued: no handle array, a count out of range,
+    # a null handle in the array
+    p = lambda v: ctypes.c_void_p(v)
+    hs = (ctypes.c_void_p * 2)(None, None)
+    assert L.ispa_solve_modulation_batch(None, 1, 1e-3, p(256), None, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_solve_modulation_batch(hs, 0, 1e-3, p(256), None, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_solve_modulation_batch(hs, 4097, 1e-3, p(256), None, None) == ispa.ISPA_ERR_INVALID_ARG
+    assert L.ispa_solve_modulation_batch(hs, 2, 1e-3, p(256), None, None) == ispa.ISPA_ERR_STATE

@@ -147,3 +147,80 @@ def test_async_solve_matches_sync():
     assert int(status0.item()) == 1
     with pytest.raises(ispa.NotSPDError):
         st0.solve(0.0)
+
+
+def _fill_batch(sb, wid, n):
+    """Accumulate different seeded rows into every layer of a StatsBatch."""
+    refs = []
+    for i, st in enumerate(sb.layers):
+        x = rows(wid, i, n, sb.d_in)
+        yf = synth.normal((n, sb.d_out), synth.seed_of(wid, i, synth.Y_FULL), DEV, dtype=torch.float32)
+        yl = synth.normal((n, sb.d_out), synth.seed_of(wid, i, synth.Y_LOCAL), DEV, dtype=torch.float32)
+        st.accum(x, yf, yl)
+        refs.append((x, yf, yl))
+    return refs
+
+
+@pytest.mark.parametrize("d_in,d_out,n,layers", [(200, 72, 700, 3), (776, 328, 1600, 4)])
+def test_batch_solve_matches_single(d_in, d_out, n, layers):
+    # the batched solve runs every layer's arithmetic unchanged: dW and eps bit
+    # for bit those of the single-layer solve, and within the oracle's bound
+    lam = 0.5
+    print(f"[solve] batch of {layers} at d_in={d_in} d_out={d_out}", flush=True)
+    sb = ispa.StatsBatch(layers, d_in, d_out, max_rows=n, device=DEV)
+    refs = _fill_batch(sb, 35, n)
+    dw_b, eps_b, status_b = sb.solve(lam)
+    torch.cuda.synchronize()
+    assert status_b.tolist() == [0] * layers
+    for i, st in enumerate(sb.layers):
+        dw_1, eps_1, status_1 = st.solve_async(lam)
+        torch.cuda.synchronize()
+        assert int(status_1.item()) == 0
+        assert torch.equal(dw_b[i].view(torch.int32), dw_1.view(torch.int32)), f"layer {i}: dW differs"
+        assert float(eps_b[i].item()) == float(eps_1.item()), f"layer {i}: eps differs"
+        x, yf, yl = refs[i]
+        ref = oracle.Stats(d_in, d_out)
+        ref.accumulate(f64(x), f64(yf).astype(np.float32), f64(yl).astype(np.float32))
+        dw_ref = oracle.solve_modulation(ref.G, ref.C, lam)
+        assert rel_fro(f64(dw_b[i]), dw_ref) <= DW_TOL
+        assert abs(float(eps_b[i].item()) - oracle.feasibility(ref.s, dw_ref, ref.C, lam)) <= 1e-4 * ref.s
+    # every layer's G and C are left intact: solving again gives the same bits
+    dw_again, _, _ = sb.solve(lam)
+    torch.cuda.synchronize()
+    assert torch.equal(dw_again.view(torch.int32), dw_b.view(torch.int32))
+
+
+def test_batch_solve_reports_each_layer():
+    # a zero column with lambda = 0 makes only layer 1 fail; the others solve
+    d, n = 64, 80
+    sb = ispa.StatsBatch(3, d, d, max_rows=n, device=DEV)
+    for i, st in enumerate(sb.layers):
+        x = rows(36, i, n, d)
+        if i == 1:
+            x[:, 5] = 0
+        y = synth.normal((n, d), synth.seed_of(36, i, synth.Y_FULL), DEV, dtype=torch.float32)
+        st.accum(x, y, torch.zeros_like(y))
+    dw, eps, status = sb.solve(0.0)
+    torch.cuda.synchronize()
+    assert status.tolist() == [0, 1, 0]
+    for i in (0, 2):
+        dw_1, eps_1, _ = sb.layers[i].solve_async(0.0)
+        torch.cuda.synchronize()
+        assert torch.equal(dw[i].view(torch.int32), dw_1.view(torch.int32))
+
+
+def test_batch_solve_wan13b_size():
+    # 4 layers of d = 1536 (the per-layer systems of the 1.3B absorption) from
+    # 4680 rows each plus lambda: bit for bit the single-layer solve
+    d, n, layers, lam = 1536, 4680, 4, 1e-1
+    print("[solve] batch of 4 at 1536", flush=True)
+    sb = ispa.StatsBatch(layers, d, d, max_rows=n, device=DEV)
+    _fill_batch(sb, 37, n)
+    dw_b, eps_b, status_b = sb.solve(lam)
+    torch.cuda.synchronize()
+    assert status_b.tolist() == [0] * layers
+    for i in (0, 3):
+        dw_1, eps_1, _ = sb.layers[i].solve_async(lam)
+        torch.cuda.synchronize()
+        assert torch.equal(dw_b[i].view(torch.int32), dw_1.view(torch.int32))
+        assert float(eps_b[i].item()) == float(eps_1.item())
