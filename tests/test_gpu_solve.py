@@ -8,7 +8,7 @@ import torch
 import oracle
 import synth
 import paper_2607_00712_amd as ispa
-from parity_util import DW_TOL, assert_attn, f64, lower_sym, rel_fro
+from parity_util import DW_TOL, assert_attn, assert_gram, f64, lower_sym, rel_fro
 
 pytestmark = pytest.mark.gpu
 
@@ -224,3 +224,34 @@ def test_batch_solve_wan13b_size():
         torch.cuda.synchronize()
         assert torch.equal(dw_b[i].view(torch.int32), dw_1.view(torch.int32))
         assert float(eps_b[i].item()) == float(eps_1.item())
+
+
+@pytest.mark.timeout(900)
+def test_14b_absorption():
+    # the 14B layer's absorption: G (5120 x 5120) and C from 4 warmup chunks of
+    # 4680 rows (bf16 X, fp32 y_full / y_local), then dW and eps; G and C on
+    # the Cauchy-Schwarz scale, dW within 1e-3 of the fp64 oracle
+    d, n, lam = 5120, 4680, 1e-3
+    print("[solve] 14B absorption: 5120 x 5120 from 4 x 4680 rows", flush=True)
+    st = ispa.Stats(d, d, max_rows=n, device=DEV)
+    ref = oracle.Stats(d, d)
+    s_cols = np.zeros(d)
+    for i in range(4):
+        x = rows(38, i, n, d)
+        yf = synth.normal((n, d), synth.seed_of(38, i, synth.Y_FULL), DEV, dtype=torch.float32)
+        yl = synth.normal((n, d), synth.seed_of(38, i, synth.Y_LOCAL), DEV, dtype=torch.float32)
+        st.accum(x, yf, yl)
+        r = ref.accumulate(f64(x), f64(yf).astype(np.float32), f64(yl).astype(np.float32))
+        s_cols += np.sum(r * r, axis=0)
+        del x, yf, yl, r
+    G, C, S, n_rows = st.views()
+    torch.cuda.synchronize()
+    assert n_rows == 4 * n
+    eg, ec = assert_gram(f64(G), f64(C), ref.G, ref.C, s_cols)
+    print(f"[solve] 14B Gram err {eg:.2e} / {ec:.2e}", flush=True)
+    dw, eps = st.solve(lam)
+    dw_ref = oracle.solve_modulation(ref.G, ref.C, lam)
+    e = rel_fro(f64(dw), dw_ref)
+    print(f"[solve] 14B dW rel err {e:.3e}", flush=True)
+    assert e <= DW_TOL
+    assert abs(eps - oracle.feasibility(ref.s, dw_ref, ref.C, lam)) <= 1e-4 * ref.s
