@@ -14,13 +14,13 @@
 //   fp64 atomic per workgroup.
 //
 // gram_kernel (bf16 MFMA 32x32x16, fp32 accumulation):
-//   G += X^T X on the lower block triangle of 256x256 tiles, C += X^T R.
+//   G += X^T X on the lower block triangle of 128x128 tiles, C += X^T R.
 //   The contraction runs over rows, the slow (strided) dimension of both
 //   operands: row-major stages of 32 rows go HBM -> LDS by buffer loads and both
 //   MFMA operands are read with the LDS transpose read (ds_read_b64_tr_b16), 4
-//   consecutive rows of one column per lane. Each wave owns a 128 x 128 quadrant
-//   of the tile. Rows are split over several workgroups when there are too few
-//   tiles to fill the 256 CUs, and partial sums are added with fp32 atomics.
+//   consecutive rows of one column per lane. Each wave owns a 32 x 64 piece of
+//   the tile. Rows are split in two when there are fewer tiles than CUs, and
+//   the halves are added with fp32 atomics.
 #include "ispa_internal.h"
 
 namespace ispa {
@@ -129,29 +129,33 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
 }
 
 // ---------------------------------------------------------------- Gram
-// Workgroup = 8 waves, tile 256 x 256 of G (lower block triangle of 256 x 256
-// blocks) or C. Wave w owns output rows 64 (w / 2) .. +63 (A side) and columns
-// 128 (w % 2) .. +127 (B side): 2 x 4 accumulator blocks of 32 x 32 (128
-// registers, two waves per SIMD). Rows are staged 32 at a time HBM -> LDS by
-// buffer loads (no register staging) into a ring of 4 stage buffers, 3 stages
-// ahead of the MFMAs. A stage holds the 32 rows of the tile's 256 X columns (A
-// side) and of its 256 X or R columns (B side), each as two 128-column halves
-// with 256-byte rows. Both MFMA operands need 8 consecutive rows of one column
-// per lane, which the LDS transpose read delivers; the 16-byte chunk index of
-// each row is XOR-swizzled with 4 (row mod 4) ^ 2 (row/4 mod 2) so that the 32
-// lanes of a transpose read hit 16 distinct chunk positions. The buffer
-// descriptor of a stage ends at the split's last row, so rows past it read as
-// zero; columns past d of a ragged last tile read neighbouring data that only
-// reaches output rows/columns >= d, which are never stored.
-constexpr int kGThreads = 512;
-constexpr int kGT = 256;                       // output tile (rows and columns)
+// Output tiles of 128 x 128 on the lower block triangle of G and all of C,
+// one workgroup of 8 waves per tile (two waves per SIMD), wave w owning rows
+// 32 (w / 2) .. +31 and columns 64 (w % 2) .. +63 (1 x 2 accumulator blocks of
+// 32 x 32). Rows are staged 32 at a time HBM -> LDS by buffer loads (no register
+// staging) into a ring of 4 stage buffers, 3 stages ahead of the MFMAs; a stage
+// holds the 32 rows of the tile's 128 X columns (A side) and of its 128 X or R
+// columns (B side) as 256-byte rows (16 KB). Both MFMA operands need 8
+// consecutive rows of one column per lane, which the LDS transpose read
+// delivers (two reads of 4 rows); the 16-byte chunk index of each row is
+// XOR-swizzled with 4 (row mod 4) ^ 2 (row/4 mod 2) so that the 32 lanes of a
+// transpose read hit 16 distinct chunk positions. The buffer descriptor of a
+// stage ends at the split's last row, so rows past it read as zero; columns
+// past d of a ragged last tile read neighbouring data that only reaches output
+// rows/columns >= d, which are never stored. When the tiles number fewer than
+// the 256 CUs, rows are split in two and the halves added with fp32 atomics
+// (two workgroups per CU hide each other's latencies); otherwise each tile is
+// added with plain read-modify-writes. Measured against 256 x 256 tiles of 8
+// waves of 64 x 128 (row splits and atomics to fill the chip): 0.081 vs 0.098 ms
+// per 4680-row chunk at d = 1536, 0.514 vs 0.531 ms at d = 5120.
 constexpr int kGK = 32;                        // rows per stage
 constexpr int kGRing = 4;                      // stage buffers
-constexpr int kHalfBytes = kGK * 256;          // one 32 x 128 half (bf16)
-constexpr int kSideBytes = 2 * kHalfBytes;     // 32 x 256
-constexpr int kStageBytes = 2 * kSideBytes;    // A side + B side
-constexpr int kLoadsPerStage = kStageBytes / (kGThreads * 16);  // direct loads per thread
-
+constexpr int kHalfBytes = kGK * 256;          // one 32 x 128 side (bf16)
+constexpr int kG2Threads = 512;
+constexpr int kG2Waves = kG2Threads / 64;
+constexpr int kG2T = 128;                                    // output tile (rows and columns)
+constexpr int kG2Stage = 2 * kHalfBytes;                     // A side + B side
+constexpr int kG2Loads = kG2Stage / (kG2Threads * 16);       // direct loads per thread per stage
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -184,27 +188,6 @@ struct GramArgs {
   int64_t rows_per_split;   // multiple of kGK
 };
 
-// Direct loads of one stage side: 32 rows x 256 columns starting at (row0, col0)
-// of a row-major bf16 matrix with leading dimension ld, rows >= row_end zero.
-// Thread slots: load q of wave w covers 16-byte slot (q * 8 + w) * 64 + lane of
-// the side: half = slot / 512, row = (slot / 16) % 32, stored chunk = slot % 16.
-__device__ __forceinline__ void stage_side(const uint16_t* src, int64_t ld, int64_t row0, int64_t row_end, int col0,
-                                           char* dst, int wave, int lane) {
-  int64_t nrec = ((row_end - row0) * ld - col0) * 2;
-  if (nrec < 0) nrec = 0;
-  if (nrec > 0x7fffffff) nrec = 0x7fffffff;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(src + row0 * ld + col0, (int)nrec);
-#pragma unroll
-  for (int q = 0; q < kSideBytes / (kGThreads * 16); ++q) {
-    const int slot = (q * 8 + wave) * 64 + lane;
-    const int half = slot >> 9;
-    const int row = (slot >> 4) & 31;
-    const int c = (slot & 15) ^ gswz(row);
-    const int voff = (int)((row * ld + half * 128 + c * 8) * 2);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * 8 + wave) * 1024), 16, voff, 0, 0, 0);
-  }
-}
-
 // Transpose-read addresses of one side for this lane, stage buffer 0, k-slice
 // 0: [blk][h] for column block blk0 + blk (32 columns of a 128-column half) and
 // row half h (rows +4). The swizzle of a row depends only on (row mod 4,
@@ -227,96 +210,12 @@ __device__ __forceinline__ void side_addr(SideAddr<NB>& s, uint32_t half_base, i
     }
 }
 
-// The 12 transpose reads (A side: 2 blocks, B side: 4 blocks, 2 row halves each)
-// of one 16-row k-slice, as inline asm: through the builtin the compiler would
-// wait for the direct loads filling the other stage buffers before reading this
-// one. IMM is the compile-time offset of the stage buffer and k-slice.
-template <int IMM>
-__device__ __forceinline__ void gram_issue(const SideAddr<2>& A, const SideAddr<4>& B, u32x2 (&ra)[2][2],
-                                           u32x2 (&rb)[4][2]) {
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(ra[b][h]) : "v"(A.a[b][h]), "i"(IMM));
-#pragma unroll
-  for (int b = 0; b < 4; ++b)
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(rb[b][h]) : "v"(B.a[b][h]), "i"(IMM));
-}
-
-// Wait until at most N LDS operations are outstanding (LDS operations complete
-// in order) and hand out the operands of that slice.
-template <int N>
-__device__ __forceinline__ void gram_wait(u32x2 (&ra)[2][2], u32x2 (&rb)[4][2], bf16x8* af, bf16x8* bf) {
-  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
-  asm volatile("s_waitcnt lgkmcnt(%12)"
-               : "+v"(ra[0][0]), "+v"(ra[0][1]), "+v"(ra[1][0]), "+v"(ra[1][1]), "+v"(rb[0][0]), "+v"(rb[0][1]),
-                 "+v"(rb[1][0]), "+v"(rb[1][1]), "+v"(rb[2][0]), "+v"(rb[2][1]), "+v"(rb[3][0]), "+v"(rb[3][1])
-               : "i"(N));
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-    af[b] = __builtin_bit_cast(bf16x8, u32x4{ra[b][0][0], ra[b][0][1], ra[b][1][0], ra[b][1][1]});
-#pragma unroll
-  for (int b = 0; b < 4; ++b)
-    bf[b] = __builtin_bit_cast(bf16x8, u32x4{rb[b][0][0], rb[b][0][1], rb[b][1][0], rb[b][1][1]});
-}
-
 struct GramTile {
   const uint16_t* bsrc;
   int64_t bld;
   int64_t r_begin, r_end;
   int row0, col0, steps, wave, lane;
 };
-
-__device__ __forceinline__ void stage_load(const GramArgs& a, const GramTile& t, char* smem, int s) {
-  const int64_t rr = t.r_begin + (int64_t)s * kGK;
-  char* d = smem + (s % kGRing) * kStageBytes;
-  stage_side(a.x, a.d_in, rr, t.r_end, t.row0, d, t.wave, t.lane);
-  stage_side(t.bsrc, t.bld, rr, t.r_end, t.col0, d + kSideBytes, t.wave, t.lane);
-}
-
-// Stage s from ring buffer BUF = s % 4: issue the loads of stage s + 3, run the
-// 16 MFMAs of this wave, then wait for stage s + 1 and synchronise.
-// A / B address the pair of stage buffers {BUF & ~1, BUF | 1} (LDS offsets are
-// 16-bit immediates, so buffers 2 and 3 use a second set of addresses).
-template <int BUF>
-__device__ __forceinline__ void gram_stage(const GramArgs& a, const GramTile& t, char* smem, const SideAddr<2>& A,
-                                           const SideAddr<4>& B, f32x16 (&acc)[2][4], int s) {
-  constexpr int kOff = (BUF & 1) * kStageBytes;
-  if (s + 3 < t.steps) stage_load(a, t, smem, s + 3);
-  // lgkmcnt counts at most 15 outstanding operations: the second slice's 12
-  // reads are issued once the first slice has landed, and overlap its MFMAs
-  u32x2 ra[2][2], rb[4][2];
-  bf16x8 af[2], bf[4];
-  gram_issue<kOff>(A, B, ra, rb);
-  gram_wait<0>(ra, rb, af, bf);
-  gram_issue<kOff + 16 * 256>(A, B, ra, rb);
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
-  gram_wait<0>(ra, rb, af, bf);
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
-  // stage s + 1 must have landed: younger stages still in flight are s + 2 and
-  // s + 3 when they exist (direct loads retire in order)
-  const int younger = t.steps - (s + 2);
-  if (younger >= 2) {
-    vm_wait<2 * kLoadsPerStage>();
-  } else if (younger == 1) {
-    vm_wait<kLoadsPerStage>();
-  } else {
-    vm_wait<0>();
-  }
-  // the direct loads of stage s + 1 have landed (vmcnt above) and every LDS
-  // read of this wave has completed (lgkmcnt(0) before the last MFMAs): a bare barrier
-  // suffices, where a fenced one would also wait for the younger stages
-  __builtin_amdgcn_s_barrier();
-}
 
 // Output tile k of one split in panel-group order: row panels (X columns) are
 // taken kGroup at a time; within a group the G tiles of the lower block
@@ -354,9 +253,91 @@ __device__ __forceinline__ bool gram_tile_of(int k, int tiles_in, int tiles_out,
   return false;
 }
 
-__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) void gram_kernel(GramArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kGRing * kStageBytes];
+// Direct loads of one 32-row x 128-column side: load q of wave w covers 16-byte
+// slot (q * 8 + w) * 64 + lane, row = (slot / 16) % 32, stored chunk = slot % 16.
+__device__ __forceinline__ void stage_half(const uint16_t* src, int64_t ld, int64_t row0, int64_t row_end, int col0,
+                                           char* dst, int wave, int lane) {
+  int64_t nrec = ((row_end - row0) * ld - col0) * 2;
+  if (nrec < 0) nrec = 0;
+  if (nrec > 0x7fffffff) nrec = 0x7fffffff;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(src + row0 * ld + col0, (int)nrec);
+#pragma unroll
+  for (int q = 0; q < kHalfBytes / (kG2Threads * 16); ++q) {
+    const int slot = (q * kG2Waves + wave) * 64 + lane;
+    const int row = (slot >> 4) & 31;
+    const int c = (slot & 15) ^ gswz(row);
+    const int voff = (int)((row * ld + c * 8) * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (ISPA_LDS void*)(dst + (q * kG2Waves + wave) * 1024), 16, voff, 0,
+                                             0, 0);
+  }
+}
 
+// The 8 transpose reads (2 A blocks, 2 B blocks, 2 row halves each) of one
+// 16-row slice and the wait for them.
+template <int IMM, int NA>
+__device__ __forceinline__ void gram2_issue(const SideAddr<NA>& A, const SideAddr<2>& B, u32x2 (&ra)[NA][2],
+                                            u32x2 (&rb)[2][2]) {
+#pragma unroll
+  for (int b = 0; b < NA; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(ra[b][h]) : "v"(A.a[b][h]), "i"(IMM));
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(rb[b][h]) : "v"(B.a[b][h]), "i"(IMM));
+}
+template <int N>
+__device__ __forceinline__ void gram2_wait(u32x2 (&ra)[1][2], u32x2 (&rb)[2][2], bf16x8* af, bf16x8* bf) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%6)"
+               : "+v"(ra[0][0]), "+v"(ra[0][1]), "+v"(rb[0][0]), "+v"(rb[0][1]), "+v"(rb[1][0]), "+v"(rb[1][1])
+               : "i"(N));
+  af[0] = __builtin_bit_cast(bf16x8, u32x4{ra[0][0][0], ra[0][0][1], ra[0][1][0], ra[0][1][1]});
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+    bf[b] = __builtin_bit_cast(bf16x8, u32x4{rb[b][0][0], rb[b][0][1], rb[b][1][0], rb[b][1][1]});
+}
+
+__device__ __forceinline__ void stage2_load(const GramArgs& a, const GramTile& t, char* smem, int s) {
+  const int64_t rr = t.r_begin + (int64_t)s * kGK;
+  char* d = smem + (s % kGRing) * kG2Stage;
+  stage_half(a.x, a.d_in, rr, t.r_end, t.row0, d, t.wave, t.lane);
+  stage_half(t.bsrc, t.bld, rr, t.r_end, t.col0, d + kHalfBytes, t.wave, t.lane);
+}
+
+// Stage s from ring buffer BUF = s % 4: loads of stage s + 3, the 8 MFMAs of
+// this wave (the second slice's reads in flight during the first slice's
+// MFMAs), then wait for stage s + 1 and synchronise.
+template <int BUF>
+__device__ __forceinline__ void gram2_stage(const GramArgs& a, const GramTile& t, char* smem, const SideAddr<1>& A,
+                                            const SideAddr<2>& B, f32x16 (&acc)[2], int s) {
+  constexpr int kOff = BUF * kG2Stage;
+  if (s + 3 < t.steps) stage2_load(a, t, smem, s + 3);
+  u32x2 ra[1][2], rb[2][2];
+  bf16x8 af[1], bf[2];
+  gram2_issue<kOff, 1>(A, B, ra, rb);
+  gram2_wait<0>(ra, rb, af, bf);
+  gram2_issue<kOff + 16 * 256, 1>(A, B, ra, rb);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) acc[j] = mfma32(af[0], bf[j], acc[j]);
+  gram2_wait<0>(ra, rb, af, bf);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) acc[j] = mfma32(af[0], bf[j], acc[j]);
+  const int younger = t.steps - (s + 2);
+  if (younger >= 2) {
+    vm_wait<2 * kG2Loads>();
+  } else if (younger == 1) {
+    vm_wait<kG2Loads>();
+  } else {
+    vm_wait<0>();
+  }
+  __builtin_amdgcn_s_barrier();
+}
+
+__global__ __launch_bounds__(kG2Threads) __attribute__((amdgpu_waves_per_eu(2))) void gram_kernel(GramArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kGRing * kG2Stage];
   // The work list (split-major, tiles in panel-group order within a split) is
   // cut into 8 contiguous ranges, one per XCD (workgroups are dealt to the XCDs
   // round robin), so that the workgroups resident on one XCD at a time work on
@@ -376,67 +357,57 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   } else {
     t.bsrc = a.r; t.bld = a.d_out; out = a.C; out_ld = a.d_out; out_cols = a.d_out;
   }
-  t.row0 = ti * kGT;  // output rows = X columns
-  t.col0 = tj * kGT;  // output cols = X or R columns
+  t.row0 = ti * kG2T;
+  t.col0 = tj * kG2T;
   t.r_begin = (int64_t)split * a.rows_per_split;
   t.r_end = t.r_begin + a.rows_per_split;
   if (t.r_end > a.rows) t.r_end = a.rows;
   t.lane = threadIdx.x & 63;
   t.wave = threadIdx.x >> 6;
   t.steps = t.r_end > t.r_begin ? (int)((t.r_end - t.r_begin + kGK - 1) / kGK) : 0;
-  const int wr = t.wave >> 1;  // output rows 64 wr .. +63: A half wr / 2, blocks 2 (wr % 2), +1
-  const int wc = t.wave & 1;   // output cols 128 wc .. +127: B half wc
+  const int wr = t.wave >> 1;  // output rows 32 wr .. +31: A block wr
+  const int wc = t.wave & 1;   // output cols 64 wc .. +63: B blocks 2 wc, +1
 
   const uint32_t lds0 = lds_addr(smem);
-  SideAddr<2> A, A2;
-  SideAddr<4> B, B2;
-  side_addr<2>(A, lds0 + (wr >> 1) * kHalfBytes, 2 * (wr & 1), t.lane);
-  side_addr<4>(B, lds0 + kSideBytes + wc * kHalfBytes, 0, t.lane);
-  side_addr<2>(A2, lds0 + 2 * kStageBytes + (wr >> 1) * kHalfBytes, 2 * (wr & 1), t.lane);
-  side_addr<4>(B2, lds0 + 2 * kStageBytes + kSideBytes + wc * kHalfBytes, 0, t.lane);
+  SideAddr<1> A;
+  SideAddr<2> B;
+  side_addr<1>(A, lds0, wr, t.lane);
+  side_addr<2>(B, lds0 + kHalfBytes, 2 * wc, t.lane);
 
-  f32x16 acc[2][4];
+  f32x16 acc[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+  for (int j = 0; j < 2; ++j) acc[j] = f32x16{};
 
-  // prologue: stages 0..2 in flight, wait for stage 0
-  for (int s = 0; s < 3 && s < t.steps; ++s) stage_load(a, t, smem, s);
+  for (int s = 0; s < 3 && s < t.steps; ++s) stage2_load(a, t, smem, s);
   if (t.steps >= 3) {
-    vm_wait<2 * kLoadsPerStage>();
+    vm_wait<2 * kG2Loads>();
   } else if (t.steps == 2) {
-    vm_wait<kLoadsPerStage>();
+    vm_wait<kG2Loads>();
   } else {
     vm_wait<0>();
   }
   __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
   for (int s = 0; s < t.steps; s += kGRing) {
-    gram_stage<0>(a, t, smem, A, B, acc, s);
-    if (s + 1 < t.steps) gram_stage<1>(a, t, smem, A, B, acc, s + 1);
-    if (s + 2 < t.steps) gram_stage<2>(a, t, smem, A2, B2, acc, s + 2);
-    if (s + 3 < t.steps) gram_stage<3>(a, t, smem, A2, B2, acc, s + 3);
+    gram2_stage<0>(a, t, smem, A, B, acc, s);
+    if (s + 1 < t.steps) gram2_stage<1>(a, t, smem, A, B, acc, s + 1);
+    if (s + 2 < t.steps) gram2_stage<2>(a, t, smem, A, B, acc, s + 2);
+    if (s + 3 < t.steps) gram2_stage<3>(a, t, smem, A, B, acc, s + 3);
   }
-
-  // accumulate into G / C: lane holds column (lane%32) and rows 8(r/4)+4(lane/32)+r%4
-  const bool atomic = a.splits > 1;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int orow = t.row0 + 64 * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
-        const int ocol = t.col0 + 128 * wc + 32 * j + (t.lane & 31);
-        if (orow < a.d_in && ocol < out_cols) {
-          float* p = out + (int64_t)orow * out_ld + ocol;
-          if (atomic) {
-            atomicAdd(p, acc[i][j][r]);
-          } else {
-            *p += acc[i][j][r];
-          }
+    for (int r = 0; r < 16; ++r) {
+      const int orow = t.row0 + 32 * wr + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
+      const int ocol = t.col0 + 64 * wc + 32 * j + (t.lane & 31);
+      if (orow < a.d_in && ocol < out_cols) {
+        float* p = out + (int64_t)orow * out_ld + ocol;
+        if (a.splits > 1) {
+          atomicAdd(p, acc[j][r]);
+        } else {
+          *p += acc[j][r];
         }
       }
+    }
 }
 
 __global__ void zero_kernel(uint32_t* p, int64_t n_words) {
@@ -488,30 +459,19 @@ hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d
   if (rows <= 0) return hipSuccess;
   GramArgs a;
   a.x = x; a.r = r; a.G = G; a.C = C; a.rows = rows; a.d_in = d_in; a.d_out = d_out;
-  a.tiles_in = (d_in + kGT - 1) / kGT;
-  a.tiles_out = (d_out + kGT - 1) / kGT;
+  a.tiles_in = (d_in + kG2T - 1) / kG2T;
+  a.tiles_out = (d_out + kG2T - 1) / kG2T;
   a.n_g_tiles = a.tiles_in * (a.tiles_in + 1) / 2;
   a.n_tiles = a.n_g_tiles + a.tiles_in * a.tiles_out;
-  // One workgroup per CU (128 KB of LDS). Rows are split so that the 256 CUs are
-  // used well: the split count s minimises rounds(n_tiles * s) / s, the smallest
-  // s winning ties (fewer atomics); every split keeps at least 8 stages of rows.
-  int splits = 1;
-  double best = 1e30;
-  for (int sc = 1; sc <= 4; ++sc) {
-    if (sc > 1 && rows < (int64_t)sc * 8 * kGK) break;
-    const int64_t wgs = (int64_t)a.n_tiles * sc;
-    const double cost = (double)((wgs + 255) / 256) / sc;
-    if (cost < best - 1e-12) {
-      best = cost;
-      splits = sc;
-    }
-  }
+  // fewer tiles than CUs: two row splits (each of at least 8 stages)
+  int splits = a.n_tiles < 256 && rows >= 2 * 8 * kGK ? 2 : 1;
   int64_t per = (rows + splits - 1) / splits;
   per = (per + kGK - 1) / kGK * kGK;
   splits = (int)((rows + per - 1) / per);
   a.splits = splits;
   a.rows_per_split = per;
-  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(8 * ((a.n_tiles * splits + 7) / 8))), dim3(kGThreads), 0, stream, a);
+  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(8 * ((a.n_tiles * splits + 7) / 8))), dim3(kG2Threads), 0, stream,
+                     a);
   return hipGetLastError();
 }
 
