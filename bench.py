@@ -98,7 +98,7 @@ def step_flops(w, f, only="all"):
     return total
 
 
-def gpu_run(w, steps, warmup, only="all"):
+def gpu_run(w, steps, warmup, only="all", extras=True):
     """Times `steps` layer warmups. Returns the wall-clock ms per step and the
     per-part averages: ms per call for the attention calls and the statistics
     (one per chunk), ms per solve."""
@@ -175,7 +175,7 @@ def gpu_run(w, steps, warmup, only="all"):
             raise RuntimeError("solve: G + lambda I not positive definite in the timed steps")
     avg = {k2: sum(v2) / len(v2) for k2, v2 in parts.items()}
     ms_step = (t1 - t0) * 1e3 / steps
-    if only == "all":
+    if only == "all" and extras:
         avg["absorb"] = absorb_run(ispa, w, chunks[0][1], chunks[0][2], dw, dev)
         avg["solve_all_layers"] = solve_all_run(ispa, w, stats, dev)
     return ms_step, avg
@@ -480,6 +480,9 @@ def main():
                     help="1.3b / 14b: one warmup step of one layer; rollout: the 60-chunk streaming "
                          "rollout of 30 layers (per-chunk attention time and KV bytes against all F-Layers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--step-only", action="store_true",
+                    help="skip the measurements after the timed steps (absorption kernels, the solve of all "
+                         "layers), e.g. for a kernel trace of the step alone")
     ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy"],
                     default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
@@ -496,7 +499,7 @@ def main():
         return
     w = WORKLOADS[args.workload]
     f = flops(w)
-    ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only)
+    ms_step, avg = gpu_run(w, args.steps, args.warmup, args.only, extras=not args.step_only)
     total = step_flops(w, f, args.only)
     value = total / (ms_step * 1e-3) / 1e12
     attn_ms = avg["attn_dual"]
