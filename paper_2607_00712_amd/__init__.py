@@ -261,20 +261,30 @@ class Stats:
     The device workspace is a torch uint8 tensor owned by this object.
     """
 
-    def __init__(self, d_in, d_out, max_rows=4680, device=None):
+    def __init__(self, d_in, d_out, max_rows=4680, device=None, workspace=None):
+        """``workspace`` optionally supplies the device workspace: a 256-byte
+        aligned uint8 tensor of at least ispa_stats_workspace_bytes (StatsBatch
+        passes equal slices of one buffer); by default this object allocates it."""
         L = lib()
         dev = torch.device("cuda") if device is None else torch.device(device)
         if dev.type != "cuda":
             raise ValueError("Stats lives on a HIP device")
         self.device = dev if dev.index is not None else torch.device("cuda", torch.cuda.current_device())
         self.d_in, self.d_out, self.max_rows = int(d_in), int(d_out), int(max_rows)
+        self._h = ctypes.c_void_p(0)
         nbytes = L.ispa_stats_workspace_bytes(self.d_in, self.d_out, self.max_rows)
         if nbytes == 0:
             raise IspaError(ISPA_ERR_INVALID_ARG, "ispa_stats_workspace_bytes")
-        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
-        pad = (-self.workspace.data_ptr()) % 256
-        self._ws = self.workspace[pad:pad + nbytes]
-        self._h = ctypes.c_void_p(0)
+        if workspace is None:
+            self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+            pad = (-self.workspace.data_ptr()) % 256
+            self._ws = self.workspace[pad:pad + nbytes]
+        else:
+            _require(workspace, "workspace", torch.uint8, self.device, ndim=1)
+            if workspace.numel() < nbytes or workspace.data_ptr() % 256:
+                raise ValueError(f"workspace must be 256-byte aligned and hold {nbytes} bytes")
+            self.workspace = workspace
+            self._ws = workspace[:nbytes]
         _check(L.ispa_stats_create(ctypes.byref(self._h), _ptr(self._ws), nbytes, self.d_in, self.d_out,
                                    self.max_rows, _stream(self.device)), "ispa_stats_create")
 
@@ -382,16 +392,9 @@ class StatsBatch:
         self.stride = (nbytes + 255) // 256 * 256
         self.workspace = torch.empty(self.stride * self.n_layers + 256, dtype=torch.uint8, device=self.device)
         pad = (-self.workspace.data_ptr()) % 256
-        self.layers = []
-        for i in range(self.n_layers):
-            st = Stats.__new__(Stats)
-            st.device, st.d_in, st.d_out, st.max_rows = self.device, self.d_in, self.d_out, self.max_rows
-            st.workspace = self.workspace
-            st._ws = self.workspace[pad + i * self.stride: pad + i * self.stride + nbytes]
-            st._h = ctypes.c_void_p(0)
-            _check(L.ispa_stats_create(ctypes.byref(st._h), _ptr(st._ws), nbytes, self.d_in, self.d_out,
-                                       self.max_rows, _stream(self.device)), "ispa_stats_create")
-            self.layers.append(st)
+        self.layers = [Stats(self.d_in, self.d_out, self.max_rows, self.device,
+                             workspace=self.workspace[pad + i * self.stride: pad + (i + 1) * self.stride])
+                       for i in range(self.n_layers)]
 
     def solve(self, lam=1e-3, delta_w=None, eps=None, status=None):
         """dW, eps and the status word of every layer (ispa_solve_modulation_batch),
