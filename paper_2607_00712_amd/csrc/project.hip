@@ -6,11 +6,12 @@
 // [d_out, d_in] (the layout ispa_inject_modulation updates with dW^T), so
 // Y = A W_lin^T and both operands have the contraction dimension contiguous.
 //
-// proj_kernel (bf16 MFMA 32x32x16, fp32 accumulation): output tile 256 rows x
-// TN columns (TN = 256 or 128, whichever fills the chip better), 8 waves (two
-// per SIMD); wave w owns rows 64 (w / 2) .. +63 and columns (TN / 2)(w % 2) ..
-// +TN/2 - 1. Stages of 32 k go HBM -> LDS by direct buffer loads into a ring of
-// 4 buffers, 3 stages ahead of the MFMAs, one barrier per stage. LDS rows are
+// proj_kernel (bf16 MFMA 32x32x16, fp32 accumulation): output tile 128 MB rows
+// x TN columns (256 x 256, 256 x 128, or 128 x 128 for the int8 form), 8 waves
+// (two per SIMD); wave w owns rows 32 MB (w / 2) .. +32 MB - 1 and columns
+// (TN / 2)(w % 2) .. +TN/2 - 1. Stages of 32 k go HBM -> LDS by direct buffer
+// loads into a ring of 4 buffers, 3 stages ahead of the MFMAs, one barrier per
+// stage. LDS rows are
 // 64 bytes (four 16-byte chunks of 8 k); the chunk index is XOR-swizzled with
 // (row / 4) mod 4 so that each 16-lane group of an operand read (16
 // consecutive rows, one chunk) covers all 64 banks. Rows past n_rows or d_out
@@ -28,13 +29,14 @@ namespace ispa {
 namespace {
 
 constexpr int kPThreads = 512;
-constexpr int kPM = 256;          // tile rows (rows of A)
 constexpr int kPRowBytes = 64;    // bytes of k per row per stage (32 bf16 or 64 int8)
 constexpr int kPRing = 4;         // stage buffers
 
-template <int TN>
+// TN tile columns; MB 32-row accumulator blocks per wave, so tiles of 128 MB rows
+template <int TN, int MB>
 struct PCfg {
-  static constexpr int sideA = kPM * kPRowBytes;
+  static constexpr int tm = 128 * MB;            // tile rows (rows of A)
+  static constexpr int sideA = tm * kPRowBytes;
   static constexpr int sideB = TN * kPRowBytes;
   static constexpr int stage = sideA + sideB;
   static constexpr int loadsA = sideA / (kPThreads * 16);
@@ -111,84 +113,92 @@ __device__ __forceinline__ void p_stage_side(const char* src, int64_t ld, int64_
 }
 
 // Operand read addresses of this lane for stage buffer 0: [block][k-slice].
-template <int TN>
+template <int TN, int MB>
 struct PAddr {
-  uint32_t a[2][2];
-  uint32_t b[PCfg<TN>::nb][2];
+  uint32_t a[MB][2];
+  uint32_t b[PCfg<TN, MB>::nb][2];
 };
-template <int TN>
-__device__ __forceinline__ void p_addr(PAddr<TN>& ad, uint32_t base, int wr, int wc, int lane) {
+template <int TN, int MB>
+__device__ __forceinline__ void p_addr(PAddr<TN, MB>& ad, uint32_t base, int wr, int wc, int lane) {
   const int r = lane & 31, h = lane >> 5;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int row = 64 * wr + 32 * i + r;
+    for (int i = 0; i < MB; ++i) {
+      const int row = 32 * MB * wr + 32 * i + r;
       ad.a[i][ks] = base + row * kPRowBytes + (((2 * ks + h) ^ pswz(row)) << 4);
     }
 #pragma unroll
-    for (int j = 0; j < PCfg<TN>::nb; ++j) {
+    for (int j = 0; j < PCfg<TN, MB>::nb; ++j) {
       const int row = (TN / 2) * wc + 32 * j + r;
-      ad.b[j][ks] = base + PCfg<TN>::sideA + row * kPRowBytes + (((2 * ks + h) ^ pswz(row)) << 4);
+      ad.b[j][ks] = base + PCfg<TN, MB>::sideA + row * kPRowBytes + (((2 * ks + h) ^ pswz(row)) << 4);
     }
   }
 }
 
 // The operand reads of one 32-byte k slice (inline asm: through the builtin the
 // compiler would also wait for the direct loads filling other buffers).
-template <int TN, int IMM>
-__device__ __forceinline__ void p_issue(const PAddr<TN>& ad, int ks, u32x4 (&ra)[2], u32x4 (&rb)[PCfg<TN>::nb]) {
+template <int TN, int MB, int IMM>
+__device__ __forceinline__ void p_issue(const PAddr<TN, MB>& ad, int ks, u32x4 (&ra)[MB],
+                                        u32x4 (&rb)[PCfg<TN, MB>::nb]) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(ra[i]) : "v"(ad.a[i][ks]), "i"(IMM));
+  for (int i = 0; i < MB; ++i)
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(ra[i]) : "v"(ad.a[i][ks]), "i"(IMM));
 #pragma unroll
-  for (int j = 0; j < PCfg<TN>::nb; ++j)
+  for (int j = 0; j < PCfg<TN, MB>::nb; ++j)
     asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(rb[j]) : "v"(ad.b[j][ks]), "i"(IMM));
 }
-__device__ __forceinline__ void p_wait0(u32x4 (&ra)[2], u32x4 (&rb)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(ra[0]), "+v"(ra[1]), "+v"(rb[0]), "+v"(rb[1]), "+v"(rb[2]), "+v"(rb[3]));
-}
-__device__ __forceinline__ void p_wait0(u32x4 (&ra)[2], u32x4 (&rb)[2]) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(ra[0]), "+v"(ra[1]), "+v"(rb[0]), "+v"(rb[1]));
+// Wait for every LDS read of this wave; each operand register is then tied to
+// the wait (an empty asm after it, in order), so no use moves above it.
+template <int MB, int NB>
+__device__ __forceinline__ void p_wait0(u32x4 (&ra)[MB], u32x4 (&rb)[NB]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < MB; ++i) asm volatile("" : "+v"(ra[i]));
+#pragma unroll
+  for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(rb[j]));
 }
 
-template <int TN>
+template <int TN, int MB>
 struct PTile {
   int64_t row0;  // rows of A / Y
   int col0;      // rows of W / columns of Y
   int steps, wave, lane;
 };
 
-template <int TN>
-__device__ __forceinline__ void p_load(const ProjArgs& a, const PTile<TN>& t, char* smem, int s) {
-  char* d = smem + (s % kPRing) * PCfg<TN>::stage;
-  p_stage_side<PCfg<TN>::loadsA>(a.a, a.ld, t.row0, a.n, s * kPRowBytes, d, t.wave, t.lane);
-  p_stage_side<PCfg<TN>::loadsB>(a.w, a.ld, t.col0, a.d_out, s * kPRowBytes, d + PCfg<TN>::sideA, t.wave, t.lane);
+template <int TN, int MB>
+__device__ __forceinline__ void p_load(const ProjArgs& a, const PTile<TN, MB>& t, char* smem, int s) {
+  using C = PCfg<TN, MB>;
+  char* d = smem + (s % kPRing) * C::stage;
+  p_stage_side<C::loadsA>(a.a, a.ld, t.row0, a.n, s * kPRowBytes, d, t.wave, t.lane);
+  p_stage_side<C::loadsB>(a.w, a.ld, t.col0, a.d_out, s * kPRowBytes, d + C::sideA, t.wave, t.lane);
 }
 
 // Stage s from ring buffer BUF: loads of stage s + 3, the 2 x nb x 2 MFMAs of
 // this wave, then wait for stage s + 1 and synchronise. Buffers 2 and 3 use
 // the second address set (LDS offsets are 16-bit immediates).
-template <int TN, bool I8, int BUF>
-__device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN>& t, char* smem, const PAddr<TN>& ad,
-                                        typename PMath<I8>::acc_t (&acc)[2][PCfg<TN>::nb], int s) {
-  using C = PCfg<TN>;
+template <int TN, int MB, bool I8, int BUF>
+__device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN, MB>& t, char* smem,
+                                        const PAddr<TN, MB>& ad,
+                                        typename PMath<I8>::acc_t (&acc)[MB][PCfg<TN, MB>::nb], int s) {
+  using C = PCfg<TN, MB>;
   constexpr int kOff = (BUF & 1) * C::stage;
-  if (s + 3 < t.steps) p_load<TN>(a, t, smem, s + 3);
-  u32x4 ra[2], rb[C::nb], fa[2], fb[C::nb];
-  p_issue<TN, kOff>(ad, 0, ra, rb);
-  p_wait0(ra, rb);
+  if (s + 3 < t.steps) p_load<TN, MB>(a, t, smem, s + 3);
+  u32x4 ra[MB], rb[C::nb], fa[MB], fb[C::nb];
+  p_issue<TN, MB, kOff>(ad, 0, ra, rb);
+  p_wait0<MB, C::nb>(ra, rb);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) fa[i] = ra[i];
+  for (int i = 0; i < MB; ++i) fa[i] = ra[i];
 #pragma unroll
   for (int j = 0; j < C::nb; ++j) fb[j] = rb[j];
-  p_issue<TN, kOff>(ad, 1, ra, rb);
+  p_issue<TN, MB, kOff>(ad, 1, ra, rb);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < C::nb; ++j) acc[i][j] = PMath<I8>::mma(fa[i], fb[j], acc[i][j]);
-  p_wait0(ra, rb);
+  p_wait0<MB, C::nb>(ra, rb);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < C::nb; ++j) acc[i][j] = PMath<I8>::mma(ra[i], rb[j], acc[i][j]);
   // stage s + 1 must have landed; stages s + 2 and s + 3 may still be in flight
@@ -203,9 +213,9 @@ __device__ __forceinline__ void p_stage(const ProjArgs& a, const PTile<TN>& t, c
   __builtin_amdgcn_s_barrier();
 }
 
-template <int TN, bool I8>
+template <int TN, int MB, bool I8>
 __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) void proj_kernel(ProjArgs a) {
-  using C = PCfg<TN>;
+  using C = PCfg<TN, MB>;
   __shared__ __attribute__((aligned(1024))) char smem[kPRing * C::stage];
   // XCD-aware order: each XCD takes a contiguous run of tiles (row panels of A
   // shared through its L2)
@@ -213,25 +223,25 @@ __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   const int per_xcd = (n_items + 7) / 8;
   const int item = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
   if (item >= n_items) return;
-  PTile<TN> t;
-  t.row0 = (int64_t)(item / a.tiles_n) * kPM;
+  PTile<TN, MB> t;
+  t.row0 = (int64_t)(item / a.tiles_n) * C::tm;
   t.col0 = (item % a.tiles_n) * TN;
   t.lane = threadIdx.x & 63;
   t.wave = threadIdx.x >> 6;
   t.steps = a.ld / kPRowBytes;
   const int wr = t.wave >> 1, wc = t.wave & 1;
   const uint32_t lds0 = p_lds_addr(smem);
-  PAddr<TN> ad, ad2;
-  p_addr<TN>(ad, lds0, wr, wc, t.lane);
-  p_addr<TN>(ad2, lds0 + 2 * C::stage, wr, wc, t.lane);
+  PAddr<TN, MB> ad, ad2;
+  p_addr<TN, MB>(ad, lds0, wr, wc, t.lane);
+  p_addr<TN, MB>(ad2, lds0 + 2 * C::stage, wr, wc, t.lane);
 
-  typename PMath<I8>::acc_t acc[2][C::nb];
+  typename PMath<I8>::acc_t acc[MB][C::nb];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < C::nb; ++j) acc[i][j] = typename PMath<I8>::acc_t{};
 
-  for (int s = 0; s < 3 && s < t.steps; ++s) p_load<TN>(a, t, smem, s);
+  for (int s = 0; s < 3 && s < t.steps; ++s) p_load<TN, MB>(a, t, smem, s);
   if (t.steps >= 3) {
     p_vm_wait<2 * C::loads>();
   } else if (t.steps == 2) {
@@ -241,10 +251,10 @@ __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   }
   __builtin_amdgcn_s_barrier();  // stage 0 has landed (vmcnt above)
   for (int s = 0; s < t.steps; s += kPRing) {
-    p_stage<TN, I8, 0>(a, t, smem, ad, acc, s);
-    if (s + 1 < t.steps) p_stage<TN, I8, 1>(a, t, smem, ad, acc, s + 1);
-    if (s + 2 < t.steps) p_stage<TN, I8, 2>(a, t, smem, ad2, acc, s + 2);
-    if (s + 3 < t.steps) p_stage<TN, I8, 3>(a, t, smem, ad2, acc, s + 3);
+    p_stage<TN, MB, I8, 0>(a, t, smem, ad, acc, s);
+    if (s + 1 < t.steps) p_stage<TN, MB, I8, 1>(a, t, smem, ad, acc, s + 1);
+    if (s + 2 < t.steps) p_stage<TN, MB, I8, 2>(a, t, smem, ad2, acc, s + 2);
+    if (s + 3 < t.steps) p_stage<TN, MB, I8, 3>(a, t, smem, ad2, acc, s + 3);
   }
 
   // lane holds column (lane % 32) and rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each block
@@ -254,10 +264,10 @@ __global__ __launch_bounds__(kPThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     if (ocol >= a.d_out) continue;
     const float scol = I8 ? a.sw[ocol] : 1.0f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t orow = t.row0 + 64 * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
+        const int64_t orow = t.row0 + 32 * MB * wr + 32 * i + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
         if (orow < a.n) {
           float v;
           if constexpr (I8)
@@ -332,25 +342,35 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const T* __restrict__ x
 
 }  // namespace
 
+template <int TN, int MB, bool I8>
+static void launch_proj_cfg(const ProjArgs& p, hipStream_t stream) {
+  const int grid = (p.tiles_m * p.tiles_n + 7) / 8 * 8;
+  hipLaunchKernelGGL((proj_kernel<TN, MB, I8>), dim3(grid), dim3(kPThreads), 0, stream, p);
+}
+
+static int64_t proj_items(int64_t n, int d_out, int tm, int tn) {
+  return ((n + tm - 1) / tm) * ((d_out + tn - 1) / tn);
+}
+
 static hipError_t launch_proj(ProjArgs p, bool i8, int d_out, int n_cu, hipStream_t stream) {
-  p.tiles_m = (int)((p.n + kPM - 1) / kPM);
-  // the tile width that leaves the fewest idle workgroup slots in the last round
-  const int n256 = p.tiles_m * ((d_out + 255) / 256), n128 = p.tiles_m * ((d_out + 127) / 128);
+  // 256-row tiles of 256 or 128 columns, whichever leaves fewer idle
+  // workgroup slots in the last round (ties to the wider tile); the int8 form
+  // takes 128 x 128 tiles when 256 x 128 ones would not fill one round, where
+  // two workgroups per CU hide its shorter stages better (measured at 4680 x
+  // 1536 x 1536: 0.026 ms against 0.030 ms; the bf16 form is slower there)
   const int cu = n_cu > 0 ? n_cu : 256;
-  const double f256 = (double)n256 / (cu * ((n256 + cu - 1) / cu));
-  const double f128 = (double)n128 / (cu * ((n128 + cu - 1) / cu));
-  const bool wide = f256 >= f128;
-  p.tiles_n = wide ? (d_out + 255) / 256 : (d_out + 127) / 128;
-  const int items = p.tiles_m * p.tiles_n;
-  const int grid = (items + 7) / 8 * 8;
-  if (wide && i8)
-    hipLaunchKernelGGL((proj_kernel<256, true>), dim3(grid), dim3(kPThreads), 0, stream, p);
-  else if (wide)
-    hipLaunchKernelGGL((proj_kernel<256, false>), dim3(grid), dim3(kPThreads), 0, stream, p);
-  else if (i8)
-    hipLaunchKernelGGL((proj_kernel<128, true>), dim3(grid), dim3(kPThreads), 0, stream, p);
+  auto fill = [&](int64_t items) { return (double)items / (double)(cu * ((items + cu - 1) / cu)); };
+  const int64_t wide = proj_items(p.n, d_out, 256, 256), narrow = proj_items(p.n, d_out, 256, 128);
+  int tm = 256, tn = fill(wide) >= fill(narrow) ? 256 : 128;
+  if (i8 && narrow < cu) tm = tn = 128;
+  p.tiles_m = (int)((p.n + tm - 1) / tm);
+  p.tiles_n = (d_out + tn - 1) / tn;
+  if (tm == 128)
+    launch_proj_cfg<128, 1, true>(p, stream);
+  else if (tn == 256)
+    i8 ? launch_proj_cfg<256, 2, true>(p, stream) : launch_proj_cfg<256, 2, false>(p, stream);
   else
-    hipLaunchKernelGGL((proj_kernel<128, false>), dim3(grid), dim3(kPThreads), 0, stream, p);
+    i8 ? launch_proj_cfg<128, 2, true>(p, stream) : launch_proj_cfg<128, 2, false>(p, stream);
   return hipGetLastError();
 }
 

@@ -106,7 +106,7 @@ def test_attention_over_the_ring():
 # the L-Layer's output projection y = a W^T (W in the linear-layer layout),
 # fp32 accumulation: compared with the fp64 oracle on the same bf16 operands
 @pytest.mark.parametrize("shape", [(64, 128, 64), (300, 256, 200), (4680, 1536, 1536), (777, 5120, 640),
-                                   (1, 32, 8)])
+                                   (1, 32, 8), (4000, 128, 4000)])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_projection(shape, out_dtype):
     n, d_in, d_out = shape

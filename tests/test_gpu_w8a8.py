@@ -121,18 +121,19 @@ def test_w8a8_chain_and_error_bound():
     assert np.all(err <= bound)
 
 
-@pytest.mark.parametrize("d", [1536, 5120])
-def test_w8a8_full_size_sampled_rows(d):
+@pytest.mark.parametrize("shape", [(4680, 1536, 1536), (4680, 5120, 5120), (4000, 128, 4000)])
+def test_w8a8_full_size_sampled_rows(shape):
     # the chunk's output projection at the sizes of the two workloads (4680 query
-    # rows, hidden d): the oracle recomputes 24 sampled rows exactly
-    n = 4680
-    g = torch.Generator().manual_seed(d)
-    qa, qw = codes(n, d, g), codes(d, d, g)
-    sa, sw = scales(n, g), scales(d, g)
-    print(f"project_w8a8 full size n={n} d={d}", flush=True)
+    # rows, hidden d; 128 x 128 and 256 x 128 tiles), and a shape of 256 x 256
+    # tiles: the oracle recomputes 24 sampled rows exactly
+    n, d_in, d_out = shape
+    g = torch.Generator().manual_seed(d_out)
+    qa, qw = codes(n, d_in, g), codes(d_out, d_in, g)
+    sa, sw = scales(n, g), scales(d_out, g)
+    print(f"project_w8a8 full size {shape}", flush=True)
     y = ispa.project_w8a8(qa.to(DEV), sa.to(DEV), qw.to(DEV), sw.to(DEV))
     torch.cuda.synchronize()
-    rows = np.sort(np.random.default_rng(d).choice(n, 24, replace=False))
+    rows = np.sort(np.random.default_rng(d_out).choice(n, 24, replace=False))
     rows[-1] = n - 1
     want = oracle.project_w8a8(qa.numpy()[rows], sa.numpy()[rows], qw.numpy(), sw.numpy())
     assert np.array_equal(f32_bits(y)[rows], want.view(np.int32))
