@@ -61,7 +61,7 @@ PEAK_HBM_GBS = 8000.0
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "56ebf55894cb74a1", "bytes_per_launch": 767.4e6},
+    "1.3b": {"attn_chunk_sha256_16": "e9996bf782375818", "bytes_per_launch": 779.8e6},
 }
 
 

@@ -590,11 +590,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // LSE = m + ln sum_p e^(LSE_p - m) and O = sum_p e^(LSE_p - LSE) O_p, for the
 // full result (all pieces) and the local result (pieces that start in the local
 // set). Items or sets covered by one piece were written by that piece.
+// floor(n / d) for 0 <= n < 2^53 and 0 < d in fp64: n and d are exact, and a
+// quotient q that is not an integer lies at least 1/d from one, farther than
+// the rounding of the division (at most q 2^-53 < 1/d) can move it, so the
+// floor is exact.
+__device__ __forceinline__ int64_t floor_div_exact(int64_t n, int64_t d) {
+  return (int64_t)__builtin_floor((double)n / (double)d);
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_split_kernel(AttnArgs a, int q_tiles, int n_tiles,
                                                                int n_tiles_local) {
   constexpr int kVec = D / 4;            // float4 per row
   constexpr int kRows = 256 / kVec;      // rows per block
+  constexpr int kBatch = 4;              // pieces whose loads are in flight together
   const AttnSplit& s = a.split;
   const int item = blockIdx.x;
   const int r = threadIdx.x / kVec, c = threadIdx.x % kVec;
@@ -602,27 +611,49 @@ __global__ __launch_bounds__(256) void attn_merge_split_kernel(AttnArgs a, int q
   const int head = item / q_tiles;
   const int qrow = (item - head * q_tiles) * kBq + qloc;
   if (qrow >= a.n_q) return;
+  // segments g_lo .. g_hi hold the pieces of this item: the same arithmetic as
+  // seg_of / seg_begin, exact in fp64 since units x segments < 2^52 (checked
+  // on the host)
   const int64_t i0 = (int64_t)item * n_tiles;
-  const int g_lo = seg_of(s, i0);
+  const int g_lo = (int)floor_div_exact((i0 + 1) * s.n_seg - 1, s.units);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
     if (which == 1 && a.out_local == nullptr) break;
-    const int g_hi = seg_of(s, i0 + (which == 0 ? n_tiles : n_tiles_local) - 1);
+    const int64_t u_last = i0 + (which == 0 ? n_tiles : n_tiles_local) - 1;
+    const int g_hi = (int)floor_div_exact((u_last + 1) * s.n_seg - 1, s.units);
     if (g_hi == g_lo) continue;
-    float m = -INFINITY;
-    for (int gg = g_lo; gg <= g_hi; ++gg) {
-      const int slot = gg * s.max_pieces + (item - (int)(seg_begin(s, gg) / n_tiles));
-      m = fmaxf(m, s.part_lse[((int64_t)slot * 2 + which) * kBq + qloc]);
-    }
-    float sum = 0.f;
+    // Eq. 11-12 over the pieces, kBatch at a time with a running maximum
+    float m = -INFINITY, sum = 0.f;
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int gg = g_lo; gg <= g_hi; ++gg) {
-      const int slot = gg * s.max_pieces + (item - (int)(seg_begin(s, gg) / n_tiles));
-      const int64_t base = ((int64_t)slot * 2 + which) * kBq + qloc;
-      const float e = expf(s.part_lse[base] - m);
-      const f32x4 v = *(const f32x4*)(s.part_o + base * D + 4 * c);
-      sum += e;
-      o += e * v;
+    for (int g0 = g_lo; g0 <= g_hi; g0 += kBatch) {
+      float l[kBatch];
+      f32x4 v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int gg = g0 + j;
+        l[j] = -INFINITY;
+        v[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (gg <= g_hi) {
+          const int64_t first = floor_div_exact(floor_div_exact((int64_t)gg * s.units, s.n_seg), n_tiles);
+          const int slot = gg * s.max_pieces + (item - (int)first);
+          const int64_t base = ((int64_t)slot * 2 + which) * kBq + qloc;
+          l[j] = s.part_lse[base];
+          v[j] = *(const f32x4*)(s.part_o + base * D + 4 * c);
+        }
+      }
+      float mm = m;
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) mm = fmaxf(mm, l[j]);
+      const float sc = m == -INFINITY ? 0.f : expf(m - mm);
+      sum *= sc;
+      o *= sc;
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const float e = l[j] == -INFINITY ? 0.f : expf(l[j] - mm);
+        sum += e;
+        o += e * v[j];
+      }
+      m = mm;
     }
     const float inv = 1.f / sum;
     float* out = which == 0 ? a.out : a.out_local;
@@ -715,6 +746,8 @@ size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit*
   }
   if (G > U) G = U;
   if (G > (1 << 20)) G = 1 << 20;
+  // the merge kernel's segment arithmetic is exact in fp64 below 2^52
+  while (G > 1 && (double)U * (double)G >= 4503599627370496.0) G /= 2;
   const int64_t seg_max = (U + G - 1) / G;
   s->units = U;
   s->n_seg = (int32_t)G;
