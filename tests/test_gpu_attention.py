@@ -119,6 +119,7 @@ def test_deterministic(shape):
     (600, 3000, 1000, 64, 2, 64, True, 11),    # d = 64
     (64, 640, 64, 0, 2, 64, True, 20),         # one tile per run
     (520, 2000, 300, 1, 1, 128, True, 2),      # fewer runs than work items
+    (300, 4000, 500, 3, 2, 128, True, 64),     # ~16 pieces per item, merged four at a time
 ])
 def test_split_parity(case):
     n_q, N, w, s, H, d, dual, seg = case
