@@ -62,6 +62,7 @@ PEAK_HBM_GBS = 8000.0
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
     "1.3b": {"attn_chunk_sha256_16": "e9996bf782375818", "bytes_per_launch": 779.8e6},
+    "14b": {"attn_chunk_sha256_16": "e9996bf782375818", "bytes_per_launch": 3059.8e6},
 }
 
 
