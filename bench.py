@@ -21,8 +21,12 @@ divided by the measured step time. The roofline object covers the dominant
 call (the dual-stream attention: its kernel and, when the work is split over
 the chip, the merge kernel), timed with HIP events on the stream it runs on.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same step.
-`--workload 14b` runs the 14B-like shape instead (40 heads, 98280 keys);
-`--workload rollout` the 60-chunk streaming rollout.
+The default run also times the same step at the 14B-like shape (40 heads x 128,
+98280 keys; `breakdown_14b`, with its own sampled CPU baseline on 4 of the 40
+heads) and, at both shapes, the dual-stream call against a single-stream call
+over the full cache (`dual_overhead`: the cost of also writing the local result,
+Sec. 3.4). `--workload 14b` runs the 14B-like shape alone; `--workload rollout`
+the 60-chunk streaming rollout.
 """
 
 import argparse
@@ -53,6 +57,7 @@ KV_BYTES_PER_KEY = 2 * 2  # one bf16 key and one bf16 value element per hidden u
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA
+PEAK_FP32_TFLOPS = 157.3   # MI355X fp32 matrix / vector (published)
 PEAK_HBM_GBS = 8000.0
 
 # HBM bytes of one dual-stream attention call (the attention kernel plus the
@@ -179,7 +184,44 @@ def gpu_run(w, steps, warmup, only="all", extras=True):
     if only == "all" and extras:
         avg["absorb"] = absorb_run(ispa, w, chunks[0][1], chunks[0][2], dw, dev)
         avg["solve_all_layers"] = solve_all_run(ispa, w, stats, dev)
+        avg["dual_overhead"] = dual_overhead_run(ispa, w, chunks[0], dev)
     return ms_step, avg
+
+
+def dual_overhead_run(ispa, w, qkv, dev, reps=20):
+    """The dual-stream call (full and local results from one pass) against a
+    single-stream call over the same full cache (an F-Layer), on the same
+    inputs: medians of `reps` HIP-event timings each. Sec. 3.4 states that the
+    LSE fusion costs under 1 % of execution time."""
+    q, k, v = qkv
+    H = w["heads"]
+    N = w["cache_len"]
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return sorted(ms)[len(ms) // 2]
+
+    out = torch.empty((w["n_q"], H * w["head_dim"]), dtype=torch.float32, device=dev)
+    out_l = torch.empty_like(out)
+    lse = torch.empty((H, w["n_q"]), dtype=torch.float32, device=dev)
+    lse_l = torch.empty_like(lse)
+    t_dual = timed(lambda: ispa.attn_chunk(q, k, v, N, w["window"], H, sink_len=w["sink"], dual=True,
+                                           out=out, lse=lse, out_local=out_l, lse_local=lse_l))
+    t_full = timed(lambda: ispa.attn_chunk(q, k, v, N, N, H, out=out, lse=lse))
+    return {"dual_ms": round(t_dual, 4), "full_single_ms": round(t_full, 4),
+            "overhead": round(t_dual / t_full - 1.0, 4),
+            "what": "dual-stream call (full + local outputs) / single-stream full-cache call - 1, same inputs, "
+                    "median of %d HIP-event timings each" % reps}
 
 
 def absorb_run(ispa, w, k, v, dw, dev, reps=10):
@@ -282,6 +324,38 @@ def solve_all_run(ispa, w, stats, dev, reps=3):
             "one_by_one_tflops": round(flop / t_1 / 1e9, 2)}
 
 
+def discrepancy_rotating(w, steps, warmup, sets=8):
+    """accum_stats over `sets` distinct (y_full, y_local) fp32 chunk pairs used
+    in rotation (8 x 57.5 MB = 460 MB at the 1.3B width, more than the 256 MB
+    last-level cache), so that the discrepancy kernel's reads come from HBM;
+    x aliases y_local as in the warmup chain. For a kernel trace of the
+    discrepancy and Gram kernels on an HBM-resident working set."""
+    import synth
+    import paper_2607_00712_amd as ispa
+    dev = torch.device("cuda", 0)
+    D = w["heads"] * w["head_dim"]
+    ys = [(synth.normal((w["n_q"], D), synth.seed_of(2607, i, synth.Y_FULL), dev, dtype=torch.float32),
+           synth.normal((w["n_q"], D), synth.seed_of(2607, i, synth.Y_LOCAL), dev, dtype=torch.float32))
+          for i in range(sets)]
+    st = ispa.Stats(D, D, max_rows=w["n_q"], device=dev)
+    for i in range(warmup):
+        yf, yl = ys[i % sets]
+        st.accum(yl, yf, yl)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        yf, yl = ys[i % sets]
+        st.accum(yl, yf, yl)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    per_call_bytes = w["n_q"] * D * (4 + 4 + 2 + 2)
+    return {"only": "discrepancy_rotating", "workload": w["name"], "sets": sets,
+            "working_set_mb": round(sets * 2 * w["n_q"] * D * 4 / 1e6, 1), "accum_stats_ms": round(ms, 4),
+            "discrepancy_bytes_per_call": per_call_bytes}
+
+
 def hbm_copy(steps, warmup, nbytes=1 << 30):
     """A plain 1 GiB device-to-device copy (torch's copy kernel), the yardstick
     for the HBM byte counters: FETCH_SIZE / WRITE_SIZE of this copy against the
@@ -301,51 +375,66 @@ def hbm_copy(steps, warmup, nbytes=1 << 30):
             "GB/s": round(2 * nbytes / ms / 1e6, 1)}
 
 
-def cpu_baseline(w, budget_rows=512):
-    """The oracle on a bounded sample of one step, scaled to TFLOP/s."""
+def cpu_baseline(w, budget_rows=512, heads=None):
+    """The oracle on a bounded sample of one step, scaled to TFLOP/s: attention
+    of `budget_rows` query rows over all keys for `heads` of the heads (all by
+    default), the statistics of those rows at the full width, and the full
+    D x D solve; the sampled times are scaled linearly to a whole step."""
     import numpy as np
     import oracle
     import synth
 
     H, d = w["heads"], w["head_dim"]
     D = H * d
+    hs = H if heads is None else heads
     cores = len(os.sched_getaffinity(0))
     q, k, v = synth.chunk_qkv(2607, 0, 0, w["n_q"], w["cache_len"], D, "cpu")
     rows = np.arange(budget_rows)
-    qn = q.double().numpy()
-    kn = k.double().numpy()
-    vn = v.double().numpy()
+    # the first hs heads (columns of the hidden layout), as their own tensors
+    qn = q[:, :hs * d].double().numpy()
+    kn = k[:, :hs * d].double().numpy()
+    vn = v[:, :hs * d].double().numpy()
+    del q, k, v
     f = flops(w)
-    frac = budget_rows / w["n_q"]
+    frac = budget_rows / w["n_q"] * hs / H
     t = time.perf_counter()
-    o = oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], H, sink_len=w["sink"],
+    o = oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], hs, sink_len=w["sink"],
                                branches=("full", "local"), query_rows=rows)
-    oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], H, sink_len=w["sink"],
+    oracle.chunk_attention(qn, kn, vn, w["cache_len"], w["window"], hs, sink_len=w["sink"],
                            branches=("local",), query_rows=rows)
     t_attn = time.perf_counter() - t
     del kn, vn
+    # statistics of the sampled rows at the full width D (the sampled heads'
+    # outputs tiled across the hidden dimension)
+    reps = H // hs
+    ol = np.tile(o["local"][0], (1, reps)).astype(np.float32)
+    of = np.tile(o["full"][0], (1, reps)).astype(np.float32)
     st = oracle.Stats(D, D)
-    xs = oracle.bf16_round(o["local"][0].astype(np.float32))
+    xs = oracle.bf16_round(ol)
     t = time.perf_counter()
-    st.accumulate(xs, o["full"][0].astype(np.float32), o["local"][0].astype(np.float32))
+    st.accumulate(xs, of, ol)
     t_stats = time.perf_counter() - t
     G = st.G + np.eye(D) * 10.0  # sample rows < D: keep the system well posed for timing
     t = time.perf_counter()
     oracle.solve_modulation(G, st.C, w["lam"])
     t_solve = time.perf_counter() - t
     # scale each sampled part to a whole step
-    t_step = w["t_warm_chunks"] * ((t_attn / frac) + (t_stats / frac)) + t_solve
+    frac_rows = budget_rows / w["n_q"]
+    t_step = w["t_warm_chunks"] * ((t_attn / frac) + (t_stats / frac_rows)) + t_solve
     total_flops = step_flops(w, f)
+    head_txt = f"all {H} heads" if hs == H else f"{hs} of {H} heads"
     return {
         "value": total_flops / t_step / 1e12,
         "unit": "TFLOP/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"fp64 numpy oracle: F-Layer dual + L-Layer attention and statistics for {budget_rows} "
-                   f"of {w['n_q']} query rows of one chunk (all {H} heads, all keys), full {D}x{D} Cholesky solve; "
-                   f"attention and statistics time scaled by {w['n_q']}/{budget_rows} and by the "
-                   f"{w['t_warm_chunks']} chunks of a step; measured "
+        "sample": (f"fp64 numpy oracle: F-Layer dual + L-Layer attention for {budget_rows} of {w['n_q']} query "
+                   f"rows of one chunk ({head_txt}, all {w['cache_len']} keys), statistics of those rows at "
+                   f"d = {D}, full {D}x{D} Cholesky solve; attention time scaled by {w['n_q']}/{budget_rows}"
+                   + ("" if hs == H else f" x {H}/{hs}") + f", statistics by {w['n_q']}/{budget_rows}, both by the "
+                   f"{w['t_warm_chunks']} chunks of a step (linear extrapolation); measured "
                    f"{t_attn:.2f}s + {t_stats:.2f}s + {t_solve:.2f}s"),
+        "extrapolated": True,
         "ms_per_step_extrapolated": t_step * 1e3,
     }
 
@@ -484,7 +573,10 @@ def main():
     ap.add_argument("--step-only", action="store_true",
                     help="skip the measurements after the timed steps (absorption kernels, the solve of all "
                          "layers), e.g. for a kernel trace of the step alone")
-    ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy"],
+    ap.add_argument("--no-14b", action="store_true",
+                    help="skip the 14B-shaped step that the default 1.3B run also times (breakdown_14b)")
+    ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy",
+                                       "discrepancy"],
                     default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
@@ -494,6 +586,9 @@ def main():
         sys.exit(2)
     if args.only == "hbm_copy":
         print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "discrepancy":
+        print(json.dumps(discrepancy_rotating(WORKLOADS[args.workload], args.steps, args.warmup)), flush=True)
         return
     if args.workload == "rollout":
         print(json.dumps(rollout_run(warmup=args.warmup)), flush=True)
@@ -555,12 +650,58 @@ def main():
             "absorb": avg.get("absorb"),
             "solve_all_layers": avg.get("solve_all_layers"),
         },
+        "dual_overhead": avg.get("dual_overhead"),
     }
     if args.only != "all":
         rec["only"] = args.only
-    if not args.no_cpu_baseline and args.workload == "1.3b" and args.only == "all":
-        rec["cpu_baseline"] = cpu_baseline(w)
+    if args.workload == "1.3b" and args.only == "all" and not args.no_14b:
+        print("[bench] 14B-shaped step", file=sys.stderr, flush=True)
+        w14 = WORKLOADS["14b"]
+        steps14 = max(3, min(args.steps, 8))
+        ms14, avg14 = gpu_run(w14, steps14, min(args.warmup, 2), "all", extras=not args.step_only)
+        rec["breakdown_14b"] = breakdown_14b(w14, ms14, avg14, steps14)
+        torch.cuda.empty_cache()
+    if not args.no_cpu_baseline and args.only == "all":
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(w, heads=4 if args.workload == "14b" else None)
+        if "breakdown_14b" in rec:
+            rec["breakdown_14b"]["cpu_baseline"] = cpu_baseline(WORKLOADS["14b"], heads=4)
     print(json.dumps(rec), flush=True)
+
+
+def breakdown_14b(w, ms_step, avg, steps):
+    """The 14B-shaped step's parts with their roofline fractions (attention and
+    Gram against the bf16 MFMA peak, the solve against the fp32 peak)."""
+    f = flops(w)
+    total = step_flops(w, f)
+
+    def frac(fl, ms, peak):
+        return round(fl / ms / 1e9 / peak, 4)
+
+    sa = avg.get("solve_all_layers")
+    return {
+        "workload": w["name"], "heads": w["heads"], "head_dim": w["head_dim"], "chunk_queries": w["n_q"],
+        "cache_len": w["cache_len"], "window": w["window"], "d": w["heads"] * w["head_dim"], "steps": steps,
+        "ms_per_step": round(ms_step, 4), "tflops_step": round(total / (ms_step * 1e-3) / 1e12, 2),
+        "attn_dual_ms": round(avg["attn_dual"], 4),
+        "attn_dual_tflops": round(f["attn_dual"] / avg["attn_dual"] / 1e9, 1),
+        "attn_dual_frac": frac(f["attn_dual"], avg["attn_dual"], PEAK_BF16_TFLOPS),
+        "attn_local_ms": round(avg["attn_local"], 4),
+        "attn_local_tflops": round(f["attn_local"] / avg["attn_local"] / 1e9, 1),
+        "attn_local_frac": frac(f["attn_local"], avg["attn_local"], PEAK_BF16_TFLOPS),
+        "accum_stats_ms": round(avg["accum_stats"], 4),
+        "gram_tflops": round(f["gram"] / avg["accum_stats"] / 1e9, 1),
+        "gram_frac": frac(f["gram"], avg["accum_stats"], PEAK_BF16_TFLOPS),
+        "solve_ms": round(avg["solve"], 4),
+        "solve_tflops": round(f["solve"] / avg["solve"] / 1e9, 2),
+        "solve_frac_fp32_peak": frac(f["solve"], avg["solve"], PEAK_FP32_TFLOPS),
+        "solve_all_layers": sa,
+        "absorb": avg.get("absorb"),
+        "dual_overhead": avg.get("dual_overhead"),
+        "per": "attention and accum_stats (discrepancy + Gram): ms per chunk call (4 per step); solve: ms per "
+               "layer; fractions against 2500 TFLOP/s bf16 and 157.3 TFLOP/s fp32",
+        "flop": f,
+    }
 
 
 if __name__ == "__main__":

@@ -28,7 +28,7 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Workspace layout of a statistics handle (offsets in bytes, 256-aligned).
 struct Layout {
-  size_t G, C, L, W, Dinv, X, R, scalars, status, total;
+  size_t G, C, L, W, Dinv, X, R, scalars, status, sqp, total;
 };
 
 bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
@@ -46,6 +46,8 @@ bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
   l.R = off; off = round_up(off + (size_t)max_rows * d_out * 2, kWsAlign);
   l.scalars = off; off = round_up(off + 4 * sizeof(double), kWsAlign);
   l.status = off; off = round_up(off + sizeof(int), kWsAlign);
+  // per-workgroup partials of ||R||^2 (added to s in a fixed order)
+  l.sqp = off; off = round_up(off + ispa::kDiscMaxGrid * sizeof(double), kWsAlign);
   l.total = off;
   *out = l;
   return true;
@@ -302,6 +304,7 @@ int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* 
   float* G = (float*)(h->ws + h->lay.G);
   float* C = (float*)(h->ws + h->lay.C);
   double* sq = (double*)(h->ws + h->lay.scalars);
+  double* sqp = (double*)(h->ws + h->lay.sqp);
   for (int64_t r0 = 0; r0 < n_rows; r0 += h->max_rows) {
     const int64_t rows = n_rows - r0 < h->max_rows ? n_rows - r0 : h->max_rows;
     const char* xp = (const char*)x + (size_t)r0 * h->d_in * xs;
@@ -309,11 +312,13 @@ int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* 
     const char* yl = (const char*)y_local + (size_t)r0 * h->d_out * ys;
     // keep the aliasing of x and y_local visible to the kernel for every block
     const void* xarg = (x == y_local) ? (const void*)yl : (const void*)xp;
-    if (ispa::launch_discrepancy(xarg, x_dtype, yf, yl, y_dtype, rows, h->d_in, h->d_out, xb, rb, sq,
+    if (ispa::launch_discrepancy(xarg, x_dtype, yf, yl, y_dtype, rows, h->d_in, h->d_out, xb, rb, sqp,
                                  h->stream) != hipSuccess)
       return ISPA_ERR_HIP;
     const uint16_t* xg = x_dtype == ISPA_DTYPE_BF16 ? (const uint16_t*)xp : xb;
-    if (ispa::launch_gram(xg, rb, rows, h->d_in, h->d_out, G, C, h->stream) != hipSuccess) return ISPA_ERR_HIP;
+    if (ispa::launch_gram(xg, rb, rows, h->d_in, h->d_out, G, C, sqp,
+                          ispa::discrepancy_grid(rows, h->d_in, h->d_out), sq, h->stream) != hipSuccess)
+      return ISPA_ERR_HIP;
   }
   h->n_rows += n_rows;
   return ISPA_OK;

@@ -82,12 +82,21 @@ hipError_t launch_attn_merge2(const float* o_a, const float* lse_a, const float*
                               hipStream_t stream);
 
 // ---- statistics (stats.hip) ----
+// The discrepancy kernel leaves one fp64 norm partial per workgroup in
+// sq_part (discrepancy_grid of them, at most kDiscMaxGrid); the Gram launch
+// that follows on the stream adds them to *sq_norm in workgroup order.
+constexpr int kDiscMaxGrid = 512;
+int discrepancy_grid(int64_t rows, int d_in, int d_out);
 hipError_t launch_discrepancy(const void* x, int x_dtype, const void* y_full, const void* y_local,
                               int y_dtype, int64_t rows, int d_in, int d_out,
-                              uint16_t* x_bf16, uint16_t* r_bf16, double* sq_norm,
-                              hipStream_t stream);
+                              uint16_t* x_bf16, uint16_t* r_bf16, double* sq_part, hipStream_t stream);
+// Gram tiles of (d_in, d_out); below kGramSplitTiles the rows are split in two
+// inside each workgroup.
+constexpr int kGramSplitTiles = 256;
+int gram_tiles(int d_in, int d_out);
 hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out,
-                       float* G, float* C, hipStream_t stream);
+                       float* G, float* C, const double* sq_part, int n_sq_part, double* sq_norm,
+                       hipStream_t stream);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
 
 // ---- absorption (absorb.hip) ----

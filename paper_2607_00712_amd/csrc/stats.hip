@@ -10,8 +10,11 @@
 //   as y_local (the attention output itself, the pre-projection reading) the
 //   y_local values already loaded are reused for X.
 //   8 elements per thread per step (all loads issued before use), a
-//   grid-stride loop over 2 workgroups per CU, wavefront shuffles then one
-//   fp64 atomic per workgroup.
+//   grid-stride loop over 2 workgroups per CU. Each step's 8 squares are
+//   summed in fp32 and added to a per-thread fp64 total; each workgroup leaves
+//   its fp64 partial in the caller's workspace, and the Gram kernel that
+//   follows on the stream adds the partials to s in workgroup order, so s does
+//   not depend on the order in which workgroups run.
 //
 // gram_kernel (bf16 MFMA 32x32x16, fp32 accumulation):
 //   G += X^T X on the lower block triangle of 128x128 tiles, C += X^T R.
@@ -19,8 +22,10 @@
 //   operands: row-major stages of 32 rows go HBM -> LDS by buffer loads and both
 //   MFMA operands are read with the LDS transpose read (ds_read_b64_tr_b16), 4
 //   consecutive rows of one column per lane. Each wave owns a 32 x 64 piece of
-//   the tile. Rows are split in two when there are fewer tiles than CUs, and
-//   the halves are added with fp32 atomics.
+//   the tile. When there are fewer tiles than CUs the rows are split in two
+//   inside one workgroup of 16 waves (8 per half); the second half's partial
+//   tile goes through LDS to the first half, which adds it to its own and then
+//   to G or C, so every sum is taken in a fixed order.
 #include "ispa_internal.h"
 
 namespace ispa {
@@ -64,10 +69,10 @@ __device__ __forceinline__ double wave_sum(double v) {
 template <int YT>
 __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
     const void* y_full, const void* y_local, int64_t n_r, uint16_t* r_out, const float* x_f32,
-    int64_t n_x, uint16_t* x_out, int x_from_y_local, double* sq_norm) {
+    int64_t n_x, uint16_t* x_out, int x_from_y_local, double* sq_part) {
   __shared__ double red[kThreads / 64];
   const int64_t stride = (int64_t)gridDim.x * kThreads * 8;
-  float part = 0.f;
+  double part = 0.0;
   const int64_t n_r8 = n_r & ~(int64_t)7;
   // 8 elements per thread and step: the four loads are in flight together
   for (int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 8; i < n_r8; i += stride) {
@@ -77,12 +82,14 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
     load4<YT>(y_local, i, l);
     load4<YT>(y_local, i + 4, l + 4);
     uint16_t r[8];
+    float step = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       r[j] = f2bf_rne(f[j] - l[j]);
       const float rv = bf2f(r[j]);
-      part = fmaf(rv, rv, part);
+      step = fmaf(rv, rv, step);
     }
+    part += (double)step;
     u32x4 rw;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rw[j] = (uint32_t)r[2 * j] | ((uint32_t)r[2 * j + 1] << 16);
@@ -101,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
     const uint16_t r = f2bf_rne(load1<YT>(y_full, i) - l);
     r_out[i] = r;
     const float rv = bf2f(r);
-    part = fmaf(rv, rv, part);
+    part += (double)rv * (double)rv;
     if (x_from_y_local) x_out[i] = f2bf_rne(l);
   }
   // separate fp32 -> bf16 conversion of x when it is its own buffer
@@ -117,14 +124,14 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
       x_out[i] = f2bf_rne(x_f32[i]);
     }
   }
-  double d = wave_sum((double)part);
+  double d = wave_sum(part);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = d;
   __syncthreads();
   if (threadIdx.x == 0) {
     double t = 0;
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) t += red[w];
-    if (t != 0.0) atomicAdd(sq_norm, t);
+    sq_part[blockIdx.x] = t;
   }
 }
 
@@ -143,9 +150,10 @@ __global__ __launch_bounds__(kThreads) void discrepancy_kernel(
 // stage ends at the split's last row, so rows past it read as zero; columns
 // past d of a ragged last tile read neighbouring data that only reaches output
 // rows/columns >= d, which are never stored. When the tiles number fewer than
-// the 256 CUs, rows are split in two and the halves added with fp32 atomics
-// (two workgroups per CU hide each other's latencies); otherwise each tile is
-// added with plain read-modify-writes. Measured against 256 x 256 tiles of 8
+// the 256 CUs, the rows are split in two inside a workgroup of 16 waves, each
+// half with its own ring (16 waves per CU hide each other's latencies as two
+// 8-wave workgroups would), and the halves are added through LDS in a fixed
+// order; every tile is then added to G or C with plain read-modify-writes. Measured against 256 x 256 tiles of 8
 // waves of 64 x 128 (row splits and atomics to fill the chip): 0.081 vs 0.098 ms
 // per 4680-row chunk at d = 1536, 0.514 vs 0.531 ms at d = 5120.
 constexpr int kGK = 32;                        // rows per stage
@@ -184,8 +192,10 @@ struct GramArgs {
   int tiles_in, tiles_out;  // output tiles along d_in / d_out
   int n_g_tiles;            // lower block triangle of G
   int n_tiles;              // G tiles + C tiles
-  int splits;               // row splits
-  int64_t rows_per_split;   // multiple of kGK
+  int64_t rows_per_split;   // rows of each half of a split workgroup (multiple of kGK)
+  const double* sq_part;    // norm partials of the discrepancy kernel, added to *sq_norm by workgroup 0
+  double* sq_norm;
+  int n_sq_part;
 };
 
 // Transpose-read addresses of one side for this lane, stage buffer 0, k-slice
@@ -336,20 +346,35 @@ __device__ __forceinline__ void gram2_stage(const GramArgs& a, const GramTile& t
   __builtin_amdgcn_s_barrier();
 }
 
-__global__ __launch_bounds__(kG2Threads) __attribute__((amdgpu_waves_per_eu(2))) void gram_kernel(GramArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kGRing * kG2Stage];
-  // The work list (split-major, tiles in panel-group order within a split) is
-  // cut into 8 contiguous ranges, one per XCD (workgroups are dealt to the XCDs
-  // round robin), so that the workgroups resident on one XCD at a time work on
-  // few distinct X / R panels and share them through that XCD's L2.
-  const int n_items = a.n_tiles * a.splits;
+// SPLIT = 2: 16 waves, waves 8..15 take the second half of the rows with
+// their own ring, and their partial tile reaches waves 0..7 through LDS.
+template <int SPLIT>
+__global__ __launch_bounds__(kG2Threads * SPLIT) __attribute__((amdgpu_waves_per_eu(2 * SPLIT))) void gram_kernel(
+    GramArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem_all[SPLIT * kGRing * kG2Stage];
+  // the norm partials of the discrepancy kernel that ran before this launch,
+  // in workgroup order (one wave: lane i takes partials i, i + 64, ..., then a
+  // fixed shuffle tree)
+  if (blockIdx.x == 0 && threadIdx.x < 64) {
+    double sq = 0.0;
+    for (int b = threadIdx.x; b < a.n_sq_part; b += 64) sq += a.sq_part[b];
+    sq = wave_sum(sq);
+    if (threadIdx.x == 0) *a.sq_norm += sq;
+  }
+  // The work list (tiles in panel-group order) is cut into 8 contiguous
+  // ranges, one per XCD (workgroups are dealt to the XCDs round robin), so
+  // that the workgroups resident on one XCD at a time work on few distinct
+  // X / R panels and share them through that XCD's L2.
+  const int n_items = a.n_tiles;
   const int per_xcd = (n_items + 7) / 8;
   const int item = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
   if (item >= n_items) return;
-  const int split = item / a.n_tiles;
+  const int half = SPLIT > 1 ? (int)(threadIdx.x / kG2Threads) : 0;
+  const int tid = (int)threadIdx.x - half * kG2Threads;
+  char* smem = smem_all + half * kGRing * kG2Stage;
   GramTile t;
   int ti, tj;
-  const bool is_g = gram_tile_of(item % a.n_tiles, a.tiles_in, a.tiles_out, ti, tj);
+  const bool is_g = gram_tile_of(item, a.tiles_in, a.tiles_out, ti, tj);
   float* out;
   int out_ld, out_cols;
   if (is_g) {
@@ -359,12 +384,14 @@ __global__ __launch_bounds__(kG2Threads) __attribute__((amdgpu_waves_per_eu(2)))
   }
   t.row0 = ti * kG2T;
   t.col0 = tj * kG2T;
-  t.r_begin = (int64_t)split * a.rows_per_split;
+  t.r_begin = (int64_t)half * a.rows_per_split;
   t.r_end = t.r_begin + a.rows_per_split;
   if (t.r_end > a.rows) t.r_end = a.rows;
-  t.lane = threadIdx.x & 63;
-  t.wave = threadIdx.x >> 6;
-  t.steps = t.r_end > t.r_begin ? (int)((t.r_end - t.r_begin + kGK - 1) / kGK) : 0;
+  t.lane = tid & 63;
+  t.wave = tid >> 6;
+  // both halves run the same number of stages (they share the barriers);
+  // stages past a half's last row read zeros
+  t.steps = (int)((a.rows_per_split + kGK - 1) / kGK);
   const int wr = t.wave >> 1;  // output rows 32 wr .. +31: A block wr
   const int wc = t.wave & 1;   // output cols 64 wc .. +63: B blocks 2 wc, +1
 
@@ -393,20 +420,37 @@ __global__ __launch_bounds__(kG2Threads) __attribute__((amdgpu_waves_per_eu(2)))
     if (s + 2 < t.steps) gram2_stage<2>(a, t, smem, A, B, acc, s + 2);
     if (s + 3 < t.steps) gram2_stage<3>(a, t, smem, A, B, acc, s + 3);
   }
+  if constexpr (SPLIT > 1) {
+    // the second half's tile through its (now idle) ring, 16 bytes per lane
+    // and store: [k][tid] for the 8 f32x4 pieces k of a thread's 32 values
+    f32x4* xch = (f32x4*)(smem_all + kGRing * kG2Stage);
+    __syncthreads();
+    if (half == 1) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          xch[(4 * j + i) * kG2Threads + tid] = f32x4{acc[j][4 * i], acc[j][4 * i + 1], acc[j][4 * i + 2],
+                                                      acc[j][4 * i + 3]};
+    }
+    __syncthreads();
+    if (half == 1) return;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 o = xch[(4 * j + i) * kG2Threads + tid];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[j][4 * i + e] += o[e];
+      }
+  }
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int orow = t.row0 + 32 * wr + 8 * (r >> 2) + 4 * (t.lane >> 5) + (r & 3);
       const int ocol = t.col0 + 64 * wc + 32 * j + (t.lane & 31);
-      if (orow < a.d_in && ocol < out_cols) {
-        float* p = out + (int64_t)orow * out_ld + ocol;
-        if (a.splits > 1) {
-          atomicAdd(p, acc[j][r]);
-        } else {
-          *p += acc[j][r];
-        }
-      }
+      if (orow < a.d_in && ocol < out_cols) out[(int64_t)orow * out_ld + ocol] += acc[j][r];
     }
 }
 
@@ -427,51 +471,69 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream) {
   return hipGetLastError();
 }
 
+int discrepancy_grid(int64_t rows, int d_in, int d_out) {
+  const int64_t n_r = rows * d_out;
+  const int64_t n_x = rows * d_in;
+  const int64_t n_max = n_r > n_x ? n_r : n_x;
+  int64_t grid = (n_max / 8 + kThreads - 1) / kThreads;
+  // 2 workgroups per CU, grid-stride beyond (measured: 256-512 workgroups
+  // best at the 1.3B chunk)
+  if (grid > kDiscMaxGrid) grid = kDiscMaxGrid;
+  if (grid < 1) grid = 1;
+  return (int)grid;
+}
+
 hipError_t launch_discrepancy(const void* x, int x_dtype, const void* y_full, const void* y_local,
                               int y_dtype, int64_t rows, int d_in, int d_out, uint16_t* x_bf16,
-                              uint16_t* r_bf16, double* sq_norm, hipStream_t stream) {
+                              uint16_t* r_bf16, double* sq_part, hipStream_t stream) {
   const int64_t n_r = rows * d_out;
   const int64_t n_x = rows * d_in;
   const bool x_from_y = x_dtype == ISPA_DTYPE_F32 && y_dtype == ISPA_DTYPE_F32 && x == y_local &&
                         d_in == d_out;
   const float* x_f32 = x_dtype == ISPA_DTYPE_F32 ? (const float*)x : nullptr;
-  const int64_t n_max = n_r > n_x ? n_r : n_x;
-  int64_t grid = (n_max / 8 + kThreads - 1) / kThreads;
-  // 2 workgroups per CU, grid-stride beyond: more workgroups only add fp64
-  // atomics on the one norm accumulator, which serialise (measured: 256-512
-  // workgroups best, 2048 +14 us at the 1.3B chunk)
-  if (grid > 512) grid = 512;
-  if (grid < 1) grid = 1;
+  const int grid = discrepancy_grid(rows, d_in, d_out);
   if (y_dtype == ISPA_DTYPE_F32) {
     hipLaunchKernelGGL(discrepancy_kernel<ISPA_DTYPE_F32>, dim3((unsigned)grid), dim3(kThreads), 0,
                        stream, y_full, y_local, n_r, r_bf16, x_f32, n_x, x_bf16, (int)x_from_y,
-                       sq_norm);
+                       sq_part);
   } else {
     hipLaunchKernelGGL(discrepancy_kernel<ISPA_DTYPE_BF16>, dim3((unsigned)grid), dim3(kThreads), 0,
                        stream, y_full, y_local, n_r, r_bf16, x_f32, n_x, x_bf16, (int)x_from_y,
-                       sq_norm);
+                       sq_part);
   }
   return hipGetLastError();
 }
 
+int gram_tiles(int d_in, int d_out) {
+  const int ti = (d_in + kG2T - 1) / kG2T, to = (d_out + kG2T - 1) / kG2T;
+  return ti * (ti + 1) / 2 + ti * to;
+}
+
 hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out,
-                       float* G, float* C, hipStream_t stream) {
+                       float* G, float* C, const double* sq_part, int n_sq_part, double* sq_norm,
+                       hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
   GramArgs a;
   a.x = x; a.r = r; a.G = G; a.C = C; a.rows = rows; a.d_in = d_in; a.d_out = d_out;
+  a.sq_part = sq_part;
+  a.n_sq_part = n_sq_part;
+  a.sq_norm = sq_norm;
   a.tiles_in = (d_in + kG2T - 1) / kG2T;
   a.tiles_out = (d_out + kG2T - 1) / kG2T;
   a.n_g_tiles = a.tiles_in * (a.tiles_in + 1) / 2;
   a.n_tiles = a.n_g_tiles + a.tiles_in * a.tiles_out;
-  // fewer tiles than CUs: two row splits (each of at least 8 stages)
-  int splits = a.n_tiles < 256 && rows >= 2 * 8 * kGK ? 2 : 1;
-  int64_t per = (rows + splits - 1) / splits;
+  // fewer tiles than CUs: the rows split in two inside each workgroup (each
+  // half of at least 8 stages)
+  const bool split = a.n_tiles < kGramSplitTiles && rows >= 2 * 8 * kGK;
+  int64_t per = split ? (rows + 1) / 2 : rows;
   per = (per + kGK - 1) / kGK * kGK;
-  splits = (int)((rows + per - 1) / per);
-  a.splits = splits;
   a.rows_per_split = per;
-  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(8 * ((a.n_tiles * splits + 7) / 8))), dim3(kG2Threads), 0, stream,
-                     a);
+  const dim3 grid((unsigned)(8 * ((a.n_tiles + 7) / 8)));
+  if (split) {
+    hipLaunchKernelGGL(gram_kernel<2>, grid, dim3(2 * kG2Threads), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(gram_kernel<1>, grid, dim3(kG2Threads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

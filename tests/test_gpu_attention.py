@@ -214,12 +214,20 @@ def test_binding_rejects_bad_tensors():
 
 # full-size shapes: sampled query rows checked one by one against the oracle
 SAMPLE_ROWS = [0, 1, 31, 32, 127, 128, 129, 1000, 2047, 2048, 4095, 4096, 4600, 4679]
+# plus one row inside every 256-query block (each block is one work item, and
+# every piece of a split work item covers all of its rows)
+BLOCK_ROWS = sorted(set(SAMPLE_ROWS) | {min(4679, 256 * b + (37 * b + 5) % 256) for b in range(19)})
 
 
-@pytest.mark.parametrize("sink", [0, 4680])
-def test_wan13b_chunk_sampled(sink):
-    # 12 heads x 128, chunk of 4680 queries, 7 chunks of cache, window of 2 chunks
-    run_and_check(4680, 32760, 9360, sink, 12, 128, True, wid=10, rows=SAMPLE_ROWS)
+def test_wan13b_chunk_all_rows():
+    # 12 heads x 128, chunk of 4680 queries, 7 chunks of cache, window of 2
+    # chunks: every query row of every head against the oracle
+    run_and_check(4680, 32760, 9360, 0, 12, 128, True, wid=10)
+
+
+def test_wan13b_chunk_sink_sampled():
+    # the same chunk with a one-chunk sink (the paper's local set of Eq. 7)
+    run_and_check(4680, 32760, 9360, 4680, 12, 128, True, wid=10, rows=BLOCK_ROWS)
 
 
 def test_14b_chunk_sampled_heads():
@@ -232,7 +240,8 @@ def test_14b_chunk_sampled_heads():
     for h in (0, 13, 26, 39):
         cols = slice(h * d, (h + 1) * d)
         ref = oracle.chunk_attention(f64(q[:, cols]), f64(k[:, cols]), f64(v[:, cols]), N, w, 1,
-                                     branches=("full", "local"), query_rows=SAMPLE_ROWS)
-        assert_attn(f64(out[:, cols])[SAMPLE_ROWS], ref["full"][0], f"head {h} full")
-        assert_attn(f64(out_l[:, cols])[SAMPLE_ROWS], ref["local"][0], f"head {h} local")
-        assert_lse(f64(lse[h])[SAMPLE_ROWS], ref["full"][1][0], f"head {h} lse")
+                                     branches=("full", "local"), query_rows=BLOCK_ROWS)
+        assert_attn(f64(out[:, cols])[BLOCK_ROWS], ref["full"][0], f"head {h} full")
+        assert_attn(f64(out_l[:, cols])[BLOCK_ROWS], ref["local"][0], f"head {h} local")
+        assert_lse(f64(lse[h])[BLOCK_ROWS], ref["full"][1][0], f"head {h} lse")
+        assert_lse(f64(lse_l[h])[BLOCK_ROWS], ref["local"][1][0], f"head {h} local lse")

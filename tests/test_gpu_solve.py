@@ -255,3 +255,28 @@ def test_14b_absorption():
     print(f"[solve] 14B dW rel err {e:.3e}", flush=True)
     assert e <= DW_TOL
     assert abs(eps - oracle.feasibility(ref.s, dw_ref, ref.C, lam)) <= 1e-4 * ref.s
+
+
+def test_eps_small_relative_to_s():
+    """A layer whose discrepancy is almost in the span of its inputs (R = X B
+    plus 3 % noise, eps / s ~ 1e-3): the layers the ranking of Sec. 3.3 keeps
+    are of this kind, and eps is then a small difference of large terms."""
+    d_in, d_out, n, lam = 1536, 128, 4680, 1e-3
+    print("[solve] eps << s at d = 1536", flush=True)
+    x = rows(36, 0, n, d_in)
+    g = torch.Generator(device="cpu").manual_seed(36)
+    B = (torch.randn(d_in, d_out, generator=g, dtype=torch.float64) / np.sqrt(d_in)).to(DEV)
+    noise = torch.randn(n, d_out, generator=g, dtype=torch.float64).to(DEV)
+    yf = (x.double() @ B + 0.03 * noise).float()
+    st = ispa.Stats(d_in, d_out, max_rows=n, device=DEV)
+    st.accum(x, yf, torch.zeros_like(yf))
+    dw, eps = st.solve(lam)
+    ref = oracle.Stats(d_in, d_out)
+    r = ref.accumulate(f64(x), f64(yf).astype(np.float32), np.zeros((n, d_out), dtype=np.float32))
+    dw_ref = oracle.solve_modulation(ref.G, ref.C, lam)
+    assert rel_fro(f64(dw), dw_ref) <= DW_TOL
+    eps_ref = oracle.feasibility(ref.s, dw_ref, ref.C, lam)
+    # the closed form against the direct residual of the same dW (Eq. 6)
+    assert eps_ref == pytest.approx(oracle.feasibility_direct(f64(x), r, dw_ref), rel=1e-6)
+    assert 1e-4 < eps_ref / ref.s < 1e-2
+    assert abs(eps - eps_ref) <= 0.02 * eps_ref, (eps, eps_ref, ref.s)
