@@ -48,6 +48,7 @@ extern "C" {
 #define ISPA_ERR_NOT_SPD     (-3) /* G + lambda I has a non-positive pivot      */
 #define ISPA_ERR_HIP         (-4) /* a HIP launch or runtime call failed        */
 #define ISPA_ERR_STATE       (-5) /* bad handle or workspace                    */
+#define ISPA_ERR_SCRATCH     (-6) /* needs more than the library's fixed scratch */
 
 /* element types of ispa_accum_stats inputs */
 #define ISPA_DTYPE_BF16 0
@@ -136,6 +137,29 @@ int ispa_attn_chunk_ws(const void* q, const void* k_cache, const void* v_cache,
 size_t ispa_attn_workspace_bytes(int64_t cache_len, int64_t window, int64_t sink_len,
                                  int32_t n_q, int32_t n_heads, int32_t head_dim,
                                  int32_t dual, int32_t segments);
+
+/*
+ * ispa_attn_chunk_ws with segments = 0 (the automatic split) for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation. The split's partial results go to a
+ * scratch array that the library holds in device memory, one per GPU, for the
+ * life of the process (ISPA_STATIC_SCRATCH_BYTES), instead of a caller
+ * workspace; the call itself allocates and frees nothing.
+ *   Arguments, outputs and results as for ispa_attn_chunk_ws (bitwise the same
+ *   outputs for the same inputs).
+ *   Returns ISPA_ERR_SCRATCH, before enqueueing anything, when the split needs
+ *   more than ISPA_STATIC_SCRATCH_BYTES (ispa_attn_workspace_bytes with
+ *   segments = 0 tells; the 1.3B-shaped dual-stream chunk needs 129 MiB).
+ * Every call on one GPU uses the same array: calls that overlap on one GPU
+ * (other streams, other threads) race and give undefined results. The array
+ * needs no clearing: every partial result is written before it is read.
+ */
+#define ISPA_STATIC_SCRATCH_BYTES ((size_t)160 << 20)
+int ispa_attn_chunk_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                            int64_t cache_len, int64_t window, int64_t sink_len,
+                            int32_t n_q, int32_t n_heads, int32_t head_dim, float scale,
+                            float* out, float* lse, float* out_local, float* lse_local,
+                            hipStream_t stream);
 
 /*
  * Attention over an explicit key set: one branch of the decomposable form of

@@ -21,11 +21,12 @@ import os
 
 import torch
 
-__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_ranges", "attn_merge", "Stats", "StatsBatch",
+__all__ = ["IspaError", "NotSPDError", "lib", "attn_chunk", "attn_chunk_noalloc", "attn_ranges", "attn_merge", "Stats", "StatsBatch",
            "status_string",
            "select_layers", "inject_modulation", "LocalKV", "project", "quantize_rows", "project_w8a8",
            "LIB_PATH", "ISPA_OK", "ISPA_ERR_INVALID_ARG", "ISPA_ERR_UNSUPPORTED",
-           "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE"]
+           "ISPA_ERR_NOT_SPD", "ISPA_ERR_HIP", "ISPA_ERR_STATE", "ISPA_ERR_SCRATCH",
+           "ISPA_STATIC_SCRATCH_BYTES"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libispa.so")
 
@@ -35,6 +36,8 @@ ISPA_ERR_UNSUPPORTED = -2
 ISPA_ERR_NOT_SPD = -3
 ISPA_ERR_HIP = -4
 ISPA_ERR_STATE = -5
+ISPA_ERR_SCRATCH = -6
+ISPA_STATIC_SCRATCH_BYTES = 160 << 20
 
 DTYPE_BF16 = 0
 DTYPE_F32 = 1
@@ -49,6 +52,8 @@ _SIGNATURES = {
     "ispa_attn_chunk_ws": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
                                           _c_f32, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p, _c_sz, _c_p]),
     "ispa_attn_workspace_bytes": (_c_sz, [_c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "ispa_attn_chunk_noalloc": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
+                                               _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "ispa_attn_ranges": (ctypes.c_int, [_c_p, _c_p, _c_p, ctypes.POINTER(_c_i64), _c_i32, _c_i32, _c_i32, _c_i32,
                                         _c_f32, _c_p, _c_p, _c_p]),
     "ispa_attn_merge": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
@@ -165,17 +170,7 @@ def _outputs(dev, n_q, hidden, n_heads, pairs):
                 raise ValueError(f"{name} must have shape {shape}")
 
 
-def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scale=0.0,
-               dual=False, out=None, lse=None, out_local=None, lse_local=None, need_lse=True, segments=0):
-    """Chunk attention (see ispa_attn_chunk / ispa_attn_chunk_ws in include/ispa.h).
-
-    q [n_q, H*d] bf16; k_cache, v_cache [>= cache_len, H*d] bf16 on one device.
-    Returns (out, lse), or (out, lse, out_local, lse_local) when dual: out is then
-    the full-cache result and out_local the sink + window result. ``segments``:
-    0 splits the work over the chip when whole work items fill it poorly, < 0
-    never splits, > 0 forces that many runs (the workspace is cached per device).
-    """
-    L = lib()
+def _chunk_outputs(q, k_cache, v_cache, cache_len, n_heads, dual, out, lse, out_local, lse_local, need_lse):
     dev, n_q, hidden, head_dim = _qkv(q, k_cache, v_cache, n_heads)
     if k_cache.shape[0] < cache_len or v_cache.shape[0] < cache_len:
         raise ValueError("cache tensors hold fewer than cache_len rows")
@@ -191,6 +186,22 @@ def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scal
     _outputs(dev, n_q, hidden, n_heads,
              (("out", out, (n_q, hidden)), ("out_local", out_local, (n_q, hidden)),
               ("lse", lse, (n_heads, n_q)), ("lse_local", lse_local, (n_heads, n_q))))
+    return dev, n_q, hidden, head_dim, out, lse, out_local, lse_local
+
+
+def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scale=0.0,
+               dual=False, out=None, lse=None, out_local=None, lse_local=None, need_lse=True, segments=0):
+    """Chunk attention (see ispa_attn_chunk / ispa_attn_chunk_ws in include/ispa.h).
+
+    q [n_q, H*d] bf16; k_cache, v_cache [>= cache_len, H*d] bf16 on one device.
+    Returns (out, lse), or (out, lse, out_local, lse_local) when dual: out is then
+    the full-cache result and out_local the sink + window result. ``segments``:
+    0 splits the work over the chip when whole work items fill it poorly, < 0
+    never splits, > 0 forces that many runs (the workspace is cached per device).
+    """
+    L = lib()
+    dev, n_q, hidden, head_dim, out, lse, out_local, lse_local = _chunk_outputs(
+        q, k_cache, v_cache, cache_len, n_heads, dual, out, lse, out_local, lse_local, need_lse)
     with torch.cuda.device(dev):
         nbytes = L.ispa_attn_workspace_bytes(int(cache_len), int(window), int(sink_len), int(n_q), int(n_heads),
                                              int(head_dim), int(bool(dual)), int(segments))
@@ -200,6 +211,23 @@ def attn_chunk(q, k_cache, v_cache, cache_len, window, n_heads, sink_len=0, scal
                               _ptr(out_local if dual else None), _ptr(lse_local if dual else None),
                               int(segments), _ptr(ws), int(ws.numel() if ws is not None else 0), _stream(dev))
     _check(st, "ispa_attn_chunk_ws")
+    return (out, lse, out_local, lse_local) if dual else (out, lse)
+
+
+def attn_chunk_noalloc(q, k_cache, v_cache, cache_len, window, n_heads, out, lse, out_local=None, lse_local=None,
+                       sink_len=0, scale=0.0):
+    """ispa_attn_chunk_noalloc: attn_chunk with the automatic split, its partial
+    results in the library's fixed per-GPU device scratch. The caller passes the
+    outputs (out_local given: the dual-stream form); nothing is allocated.
+    Returns (out, lse[, out_local, lse_local])."""
+    L = lib()
+    dual = out_local is not None
+    dev, n_q, hidden, head_dim, out, lse, out_local, lse_local = _chunk_outputs(
+        q, k_cache, v_cache, cache_len, n_heads, dual, out, lse, out_local, lse_local, False)
+    st = L.ispa_attn_chunk_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), int(cache_len), int(window),
+                                   int(sink_len), int(n_q), int(n_heads), int(head_dim), float(scale), _ptr(out),
+                                   _ptr(lse), _ptr(out_local), _ptr(lse_local), _stream(dev))
+    _check(st, "ispa_attn_chunk_noalloc")
     return (out, lse, out_local, lse_local) if dual else (out, lse)
 
 

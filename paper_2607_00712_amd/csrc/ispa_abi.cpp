@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <math.h>
+#include <mutex>
 #include <new>
 #include <stdint.h>
 #include <string.h>
@@ -80,11 +81,12 @@ const char* ispa_status_string(int status) {
     case ISPA_ERR_NOT_SPD: return "ISPA_ERR_NOT_SPD: G + lambda I is not positive definite";
     case ISPA_ERR_HIP: return "ISPA_ERR_HIP: HIP runtime or launch failure";
     case ISPA_ERR_STATE: return "ISPA_ERR_STATE: bad handle or workspace";
+    case ISPA_ERR_SCRATCH: return "ISPA_ERR_SCRATCH: needs more than the library's fixed device scratch";
     default: return "ISPA: unknown status";
   }
 }
 
-int ispa_abi_version(void) { return 103; }
+int ispa_abi_version(void) { return 104; }
 
 }  // extern "C"
 
@@ -186,6 +188,53 @@ int ispa_attn_chunk_ws(const void* q, const void* k_cache, const void* v_cache, 
     a.split.part_lse = (float*)((char*)workspace + round_up(slots * head_dim * 4, 256));
   }
   return ispa::launch_attn_chunk(a, head_dim, stream) == hipSuccess ? ISPA_OK : ISPA_ERR_HIP;
+}
+
+}  // extern "C"
+
+// Fixed device scratch of ispa_attn_chunk_noalloc (the split's partial
+// results), one copy per GPU. In host code `scratch` only stands for the
+// symbol: its device address, different on every GPU, comes from
+// hipGetSymbolAddress with that GPU current, once per device, and only that
+// address is passed to kernels.
+static __device__ __align__(256) char scratch[ISPA_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current GPU's scratch (nullptr on failure).
+void* device_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int ispa_attn_chunk_noalloc(const void* q, const void* k_cache, const void* v_cache, int64_t cache_len,
+                            int64_t window, int64_t sink_len, int32_t n_q, int32_t n_heads, int32_t head_dim,
+                            float scale, float* out, float* lse, float* out_local, float* lse_local,
+                            hipStream_t stream) {
+  // The plan of the automatic split; 0 also for invalid arguments, which
+  // ispa_attn_chunk_ws then rejects.
+  const size_t need = ispa_attn_workspace_bytes(cache_len, window, sink_len, n_q, n_heads, head_dim,
+                                                out_local != nullptr, 0);
+  if (need > ISPA_STATIC_SCRATCH_BYTES) return ISPA_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (need > 0 && (ws = device_scratch()) == nullptr) return ISPA_ERR_HIP;
+  return ispa_attn_chunk_ws(q, k_cache, v_cache, cache_len, window, sink_len, n_q, n_heads, head_dim, scale, out,
+                            lse, out_local, lse_local, 0, ws, ISPA_STATIC_SCRATCH_BYTES, stream);
 }
 
 int ispa_attn_ranges(const void* q, const void* k_cache, const void* v_cache, const int64_t* ranges,

@@ -35,10 +35,10 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_status_strings(L):
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert ispa.status_string(code).startswith("ISPA")
     assert "unknown" in ispa.status_string(7)
-    assert L.ispa_abi_version() == 103
+    assert L.ispa_abi_version() == 104
 
 
 def _attn(L, **kw):
@@ -69,6 +69,21 @@ def test_attention_argument_errors(L):
     assert _attn(L, heads=0) == E
     assert _attn(L, scale=float("nan")) == E
     assert _attn(L, scale=float("inf")) == E
+
+
+def test_noalloc_argument_errors(L):
+    # invalid arguments are rejected before the scratch is looked up
+    E, U = ispa.ISPA_ERR_INVALID_ARG, ispa.ISPA_ERR_UNSUPPORTED
+    p = ctypes.c_void_p
+    call = lambda hd=64, k=32, out=64, window=64: L.ispa_attn_chunk_noalloc(
+        p(16), p(k), p(48), 256, window, 0, 64, 2, hd, 0.0, p(out), p(128), p(0), p(0), p(0))
+    assert call(hd=96) == U
+    assert call(k=33) == E
+    assert call(out=0) == E
+    assert call(window=0) == E
+    hdr = open(HEADER).read()
+    m = re.search(r"#define ISPA_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == ispa.ISPA_STATIC_SCRATCH_BYTES
 
 
 def test_workspace_sizes(L):
