@@ -763,12 +763,17 @@ hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream
   const int n_log = a.split.n_seg > 0 ? a.split.n_seg : n_work;
   const int per_xcd = (n_log + kXcds - 1) / kXcds;
   const int grid = per_xcd * kXcds;
-  if (head_dim == 128) {
-    hipLaunchKernelGGL(attn_chunk_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
+  hipError_t e;
+  if (attn_fast_eligible(a, head_dim)) {
+    e = launch_attn_fast(a, stream);
   } else {
-    hipLaunchKernelGGL(attn_chunk_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
+    if (head_dim == 128) {
+      hipLaunchKernelGGL(attn_chunk_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
+    } else {
+      hipLaunchKernelGGL(attn_chunk_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, q_tiles);
+    }
+    e = hipGetLastError();
   }
-  hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.split.n_seg == 0) return e;
   int n_local = 0;
   const int T = attn_tiles(a.r, &n_local);

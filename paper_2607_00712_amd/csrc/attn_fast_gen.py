@@ -1,0 +1,809 @@
+"""Generates attn_fast.s: the gfx950 assembly of the head_dim-128 chunk
+attention kernel (Sec. 2 Eq. 3 over the key sets of Sec. 3.4 Eq. 7-8, with the
+dual-stream snapshot that gives the Eq. 11-12 fusion in one pass).
+
+Why assembly: with 64 queries per wave and one wave per SIMD, the K and V
+operands staged in LDS serve two 32-query blocks each (half the LDS operand
+traffic of 32 queries per wave), and the wave must hide its own softmax work
+behind its own matrix instructions. The loop is software-pipelined over
+32-key halves h: phase A(h) issues the score MFMAs of half h+1 for both query
+blocks while the VALU computes the softmax of half h for block 1; phase B(h)
+issues the P V MFMAs of half h for both blocks while the VALU computes the
+softmax of half h+1 for block 0. Every phase pairs 16 MFMAs with one block's
+softmax, interleaved instruction by instruction.
+
+Work decomposition, tile enumeration, LDS swizzles, the online softmax with a
+lazy reference (exp2 with the scale folded in, O normalised by the sum of the
+bf16-rounded weights, the LSE from the fp32 sum) and the partial-result layout
+of the split are those of the C++ kernel in attn_chunk.hip; the merge kernel
+there combines the partial results of either.
+
+Run as a script it prints the assembly; build.py assembles it into a code
+object that the library embeds and loads per device.
+"""
+
+import sys
+
+KNAME = "ispa_attn_fast_d128"
+ARGS_BYTES = 192
+
+# ---------------------------------------------------------------- registers
+# VGPRs
+V_TID, V_LANE = 0, 1
+V_KOFF = 2          # 8: K operand read addresses (buffer 0, half 0)
+V_VADDR = 10        # 8: V transpose-read addresses, [h2 * 4 + db] (include the V region base)
+V_STK = 18          # 4: staging voffsets of the K loads q = 0..3
+V_STV = 22          # 4: staging voffsets of the V loads
+V_QOFF = 26         # 2: Q load voffsets of query blocks 0 / 1
+V_ST = (28, 34)     # per block: m, thr, nmc, l, lr, alpha
+V_T = 40            # 16 temporaries v40..v55
+V_P1 = 56           # 8: P^T of block 1 (slice 0: +0..3, slice 1: +4..7)
+V_Y = 64            # 16: scores of block 0 (next half)
+V_Z = (80, 96)      # 16 each: scores of block 1, by half parity
+V_P0 = (112, 120)   # 8 each: P^T of block 0, by half parity
+V_O = (128, 192)    # 64 each: O^T of block 0 / 1, dBlock db at +16 db
+# AGPRs
+A_Q = (0, 32)       # Q^T operands of block 0 / 1, slice kk at +4 kk
+A_K = 64            # K operands of one half, slice kk at +4 kk
+A_V = 96            # V^T operands of one half, slice s and dBlock db at +16 s + 4 db
+
+# SGPRs
+S_ARG = 8           # kernel arguments s[8:55]
+S_RK, S_RV = 56, 60           # staging buffer resources
+S_RQ = 64                     # Q resource (piece start) / scratch
+S_RO, S_RL = 68, 72           # output O and LSE resources (write_state)
+S_G, S_U0, S_U1, S_ITEM, S_TA, S_TB, S_T, S_FL = 76, 77, 78, 79, 80, 81, 82, 83
+S_SLOT, S_HEAD, S_QTILE, S_HOFF2, S_WAVE, S_WAVE1K, S_QROWB, S_IFIRST = 84, 85, 86, 87, 88, 89, 90, 91
+S_NV = 92                     # 4: valid keys of the tiles in the LDS ring
+S_FLAG = (96, 97)             # deferred O rescale of block 0 / 1
+S_BUDGET = 98
+S_X, S_Y, S_W = 99, 100, 101  # scratch
+
+# kernel-argument SGPRs (byte offset / 4 + S_ARG)
+def arg(off):
+    return S_ARG + off // 4
+
+A_QPTR, A_KPTR, A_VPTR, A_OUT, A_LSE, A_OUTL, A_LSEL, A_PO, A_PL = (arg(o) for o in range(0, 72, 8))
+A_U, A_LD, A_NQ, A_QT, A_T, A_LT, A_NSEG, A_MAXP, A_PERXCD, A_NLOG = (arg(o) for o in range(72, 112, 4))
+A_B0, A_E0, A_B1, A_E1, A_B2, A_E2, A_TB1, A_TB2 = (arg(o) for o in range(112, 144, 4))
+A_SCALE, A_C, A_LAZY, A_DUAL, A_NEGC, A_LD2, A_LD4 = (arg(o) for o in range(144, 172, 4))
+
+K_REGION, V_REGION, BUF_BYTES, HALF_BYTES = 0, 65536, 16384, 8192
+LDS_BYTES = 131072
+
+
+def sp(r, n=1):
+    return f"s{r}" if n == 1 else f"s[{r}:{r + n - 1}]"
+
+
+def vp(r, n=1):
+    return f"v{r}" if n == 1 else f"v[{r}:{r + n - 1}]"
+
+
+def ap(r, n=1):
+    return f"a{r}" if n == 1 else f"a[{r}:{r + n - 1}]"
+
+
+class Gen:
+    def __init__(self):
+        self.lines = []
+        self.ool = []       # out-of-line blocks (rare paths), emitted after the kernel body
+        self.uid = 0
+
+    def new_uid(self):
+        self.uid += 1
+        return self.uid
+
+    def emit(self, *ins):
+        for i in ins:
+            self.lines.append("  " + i if not i.endswith(":") else i)
+
+    def label(self, name):
+        self.lines.append(name + ":")
+
+    # ---------------------------------------------------------------- helpers
+    def udiv(self, s_out, s_num, s_den):
+        """s_out = s_num / s_den (unsigned 32-bit; s_den > 0), through the VALU."""
+        t0, t1, t2, t3 = V_T, V_T + 1, V_T + 2, V_T + 3
+        self.emit(f"v_cvt_f32_u32_e32 {vp(t0)}, {sp(s_den)}",
+                  f"s_sub_i32 {sp(S_W)}, 0, {sp(s_den)}",
+                  f"v_rcp_iflag_f32_e32 {vp(t0)}, {vp(t0)}",
+                  "s_nop 0",
+                  f"v_mul_f32_e32 {vp(t0)}, 0x4f7ffffe, {vp(t0)}",
+                  f"v_cvt_u32_f32_e32 {vp(t0)}, {vp(t0)}",
+                  f"v_mul_lo_u32 {vp(t1)}, {sp(S_W)}, {vp(t0)}",
+                  f"v_mul_hi_u32 {vp(t1)}, {vp(t0)}, {vp(t1)}",
+                  f"v_add_u32_e32 {vp(t0)}, {vp(t0)}, {vp(t1)}",
+                  f"v_mov_b32_e32 {vp(t2)}, {sp(s_num)}",
+                  f"v_mul_hi_u32 {vp(t0)}, {vp(t2)}, {vp(t0)}",
+                  f"v_mul_lo_u32 {vp(t1)}, {vp(t0)}, {sp(s_den)}",
+                  f"v_sub_u32_e32 {vp(t2)}, {vp(t2)}, {vp(t1)}",
+                  f"v_add_u32_e32 {vp(t3)}, 1, {vp(t0)}",
+                  f"v_cmp_le_u32_e32 vcc, {sp(s_den)}, {vp(t2)}",
+                  f"v_subrev_u32_e32 {vp(t1)}, {sp(s_den)}, {vp(t2)}",
+                  "s_nop 1",
+                  f"v_cndmask_b32_e32 {vp(t0)}, {vp(t0)}, {vp(t3)}, vcc",
+                  f"v_cndmask_b32_e32 {vp(t2)}, {vp(t2)}, {vp(t1)}, vcc",
+                  f"v_add_u32_e32 {vp(t3)}, 1, {vp(t0)}",
+                  f"v_cmp_le_u32_e32 vcc, {sp(s_den)}, {vp(t2)}",
+                  "s_nop 1",
+                  f"v_cndmask_b32_e32 {vp(t0)}, {vp(t0)}, {vp(t3)}, vcc",
+                  "s_nop 1",
+                  f"v_readfirstlane_b32 {sp(s_out)}, {vp(t0)}",
+                  "s_nop 4")
+
+    def mul64(self, s_lo, s_hi, s_a, s_b):
+        """s_hi:s_lo = s_a * s_b (unsigned 32 x 32 -> 64)."""
+        self.emit(f"s_mul_hi_u32 {sp(s_hi)}, {sp(s_a)}, {sp(s_b)}",
+                  f"s_mul_i32 {sp(s_lo)}, {sp(s_a)}, {sp(s_b)}")
+
+    def add64_to(self, s_dst, s_base, s_lo, s_hi):
+        """s_dst:s_dst+1 = s_base:s_base+1 + s_hi:s_lo."""
+        self.emit(f"s_add_u32 {sp(s_dst)}, {sp(s_base)}, {sp(s_lo)}",
+                  f"s_addc_u32 {sp(s_dst + 1)}, {sp(s_base + 1)}, {sp(s_hi)}")
+
+    # ---------------------------------------------------------------- staging
+    def stage(self, s_tile, buf):
+        """Direct HBM -> LDS loads of key tile s_tile (K and V, 64 rows) into
+        ring buffer `buf`, and its valid-key count into s_nv[buf]."""
+        nv = S_NV + buf
+        b, e, f = S_RO, S_RO + 1, S_RO + 2   # (the output resource is only live inside write_state)
+        self.emit(f"s_mov_b32 {sp(b)}, {sp(A_B0)}", f"s_mov_b32 {sp(e)}, {sp(A_E0)}", f"s_mov_b32 {sp(f)}, 0",
+                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB1)}",
+                  f"s_cselect_b32 {sp(b)}, {sp(A_B1)}, {sp(b)}",
+                  f"s_cselect_b32 {sp(e)}, {sp(A_E1)}, {sp(e)}",
+                  f"s_cselect_b32 {sp(f)}, {sp(A_TB1)}, {sp(f)}",
+                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB2)}",
+                  f"s_cselect_b32 {sp(b)}, {sp(A_B2)}, {sp(b)}",
+                  f"s_cselect_b32 {sp(e)}, {sp(A_E2)}, {sp(e)}",
+                  f"s_cselect_b32 {sp(f)}, {sp(A_TB2)}, {sp(f)}",
+                  f"s_sub_i32 {sp(S_X)}, {sp(s_tile)}, {sp(f)}",
+                  f"s_lshl_b32 {sp(S_X)}, {sp(S_X)}, 6",
+                  f"s_add_i32 {sp(S_X)}, {sp(b)}, {sp(S_X)}",          # key0
+                  f"s_sub_i32 {sp(nv)}, {sp(e)}, {sp(S_X)}",
+                  f"s_min_i32 {sp(nv)}, {sp(nv)}, 64")
+        # byte offset of the tile's first row in this head: key0 * ld * 2 + hoff * 2
+        self.mul64(S_Y, S_W, S_X, A_LD2)
+        self.emit(f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_HOFF2)}", f"s_addc_u32 {sp(S_W)}, {sp(S_W)}, 0")
+        self.add64_to(S_RK, A_KPTR, S_Y, S_W)
+        self.add64_to(S_RV, A_VPTR, S_Y, S_W)
+        # records: the tile's valid rows (rows past them read as zero)
+        self.emit(f"s_sub_i32 {sp(S_X)}, {sp(nv)}, 1",
+                  f"s_mul_i32 {sp(S_X)}, {sp(S_X)}, {sp(A_LD2)}",
+                  f"s_add_u32 {sp(S_RK + 2)}, {sp(S_X)}, 0x100",
+                  f"s_mov_b32 {sp(S_RV + 2)}, {sp(S_RK + 2)}",
+                  f"s_mov_b32 {sp(S_RK + 3)}, 0x20000",
+                  f"s_mov_b32 {sp(S_RV + 3)}, 0x20000")
+        kb = K_REGION + buf * BUF_BYTES
+        vb = V_REGION + buf * BUF_BYTES
+        for q in range(4):
+            self.emit(f"s_add_u32 m0, {sp(S_WAVE1K)}, {kb + q * 4096}",
+                      "s_nop 0",
+                      f"buffer_load_dwordx4 {vp(V_STK + q)}, {sp(S_RK, 4)}, 0 offen lds",
+                      f"s_add_u32 m0, {sp(S_WAVE1K)}, {vb + q * 4096}",
+                      "s_nop 0",
+                      f"buffer_load_dwordx4 {vp(V_STV + q)}, {sp(S_RV, 4)}, 0 offen lds")
+
+    def stage_if(self, s_tile, buf):
+        """stage(s_tile) when s_tile < tb."""
+        u = self.new_uid()
+        self.emit(f"s_cmp_lt_i32 {sp(s_tile)}, {sp(S_TB)}", f"s_cbranch_scc0 .Lnost{u}")
+        self.stage(s_tile, buf)
+        self.label(f".Lnost{u}")
+
+    # ---------------------------------------------------------------- softmax
+    def softmax(self, qb, s_base, p_base, nv_reg, half):
+        """The online-softmax step of query block qb over one 32-key half
+        whose scores are in v[s_base:+15]; writes the bf16 weights to
+        v[p_base:+7] and updates the block's m / thr / nmc / l / lr (and alpha
+        and the deferred-rescale flag when the reference moves). Returns the
+        instruction list (to be interleaved with matrix instructions)."""
+        m, thr, nmc, l, lr, alpha = (V_ST[qb] + i for i in range(6))
+        flag = S_FLAG[qb]
+        u = self.new_uid()
+        T = V_T
+        S = [s_base + r for r in range(16)]
+        ins = []
+        # keys past the end of a range (only in the last tile of each range)
+        # (a rare-path branch and the label it returns to stay adjacent: the
+        # interleaver must not move matrix or LDS instructions between them)
+        ins += [f"s_cmp_lt_u32 {sp(nv_reg)}, {32 * (half + 1)}\n  s_cbranch_scc1 .Lmask{u}\n.Lmback{u}:"]
+        mask = [f".Lmask{u}:",
+                f"s_sub_i32 {sp(S_W)}, {sp(nv_reg)}, {32 * half}",
+                f"v_lshrrev_b32_e32 {vp(T)}, 5, {vp(V_LANE)}",
+                f"v_lshlrev_b32_e32 {vp(T)}, 2, {vp(T)}",
+                f"v_sub_u32_e32 {vp(T)}, {sp(S_W)}, {vp(T)}",        # lim = nv - 32 half - 4 hh
+                f"v_mov_b32_e32 {vp(T + 1)}, 0xff800000"]
+        for r in range(16):
+            c = 8 * (r >> 2) + (r & 3)    # key of register r within the half, less 4 hh
+            mask += [f"v_cmp_ge_i32_e32 vcc, {c}, {vp(T)}", "s_nop 1",
+                     f"v_cndmask_b32_e32 {vp(S[r])}, {vp(S[r])}, {vp(T + 1)}, vcc"]
+        mask += [f"s_branch .Lmback{u}"]
+        self.ool.append(mask)
+        # row max over the 16 scores and the lane pair
+        ins += [f"v_maximum3_f32 {vp(T)}, {vp(S[0])}, {vp(S[1])}, {vp(S[2])}"]
+        for r in range(3, 15, 2):
+            ins += [f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(S[r])}, {vp(S[r + 1])}"]
+        ins += [f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(S[15])}, {vp(S[15])}",
+                f"v_mov_b32_e32 {vp(T + 1)}, {vp(T)}",
+                "s_nop 1",
+                f"v_permlane32_swap_b32 {vp(T)}, {vp(T + 1)}",
+                "s_nop 1",
+                f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(T + 1)}, {vp(T + 1)}",
+                f"v_cmp_gt_f32_e32 vcc, {vp(T)}, {vp(thr)}",
+                f"s_cbranch_vccnz .Lresc{u}\n.Lrback{u}:"]
+        # reference update: m = max(m, tmax) for every lane of the wave; the
+        # factor alpha rescales l and lr here and O later (deferred)
+        self.ool.append([f".Lresc{u}:",
+                         f"v_maximum3_f32 {vp(T + 1)}, {vp(m)}, {vp(T)}, {vp(T)}",
+                         f"v_sub_f32_e32 {vp(T + 2)}, {vp(m)}, {vp(T + 1)}",
+                         f"v_mul_f32_e32 {vp(T + 2)}, {sp(A_C)}, {vp(T + 2)}",
+                         f"v_exp_f32_e32 {vp(alpha)}, {vp(T + 2)}",
+                         f"v_mov_b32_e32 {vp(m)}, {vp(T + 1)}",
+                         f"v_add_f32_e32 {vp(thr)}, {sp(A_LAZY)}, {vp(T + 1)}",
+                         f"v_mul_f32_e32 {vp(nmc)}, {sp(A_NEGC)}, {vp(T + 1)}",
+                         "s_nop 0",
+                         f"v_mul_f32_e32 {vp(l)}, {vp(alpha)}, {vp(l)}",
+                         f"v_mul_f32_e32 {vp(lr)}, {vp(alpha)}, {vp(lr)}",
+                         f"s_mov_b32 {sp(flag)}, 1",
+                         f"s_branch .Lrback{u}"])
+        # weights p = 2^(s c - m c), pairwise sums, bf16 pairs and their sum
+        P = [p_base + i for i in range(8)]
+        pending = []
+        for p in range(8):
+            a, b = S[2 * p], S[2 * p + 1]
+            ins += [f"v_fma_f32 {vp(a)}, {vp(a)}, {sp(A_C)}, {vp(nmc)}", f"v_exp_f32_e32 {vp(a)}, {vp(a)}",
+                    f"v_fma_f32 {vp(b)}, {vp(b)}, {sp(A_C)}, {vp(nmc)}", f"v_exp_f32_e32 {vp(b)}, {vp(b)}"]
+            ins += pending
+            pending = [f"v_add_f32_e32 {vp(T + 2 + p)}, {vp(a)}, {vp(b)}",
+                       f"v_cvt_pk_bf16_f32 {vp(P[p])}, {vp(a)}, {vp(b)}",
+                       f"v_dot2c_f32_bf16_e32 {vp(lr)}, 0x3f803f80, {vp(P[p])}"]
+        ins += ["s_nop 0"] + pending
+        t = [T + 2 + p for p in range(8)]
+        ins += [f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[1])}",
+                f"v_add_f32_e32 {vp(t[2])}, {vp(t[2])}, {vp(t[3])}",
+                f"v_add_f32_e32 {vp(t[4])}, {vp(t[4])}, {vp(t[5])}",
+                f"v_add_f32_e32 {vp(t[6])}, {vp(t[6])}, {vp(t[7])}",
+                f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[2])}",
+                f"v_add_f32_e32 {vp(t[4])}, {vp(t[4])}, {vp(t[6])}",
+                f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[4])}",
+                f"v_add_f32_e32 {vp(l)}, {vp(l)}, {vp(t[0])}"]
+        return ins
+
+    def deferred_rescale(self, qb):
+        """O of block qb *= alpha if the block's reference moved (its P V
+        MFMAs issued so far have completed by then)."""
+        flag, alpha = S_FLAG[qb], V_ST[qb] + 5
+        u = self.new_uid()
+        self.emit(f"s_cmp_eq_u32 {sp(flag)}, 0", f"s_cbranch_scc1 .Ldskip{u}", "s_nop 7", "s_nop 7", "s_nop 7")
+        for i in range(64):
+            self.emit(f"v_mul_f32_e32 {vp(V_O[qb] + i)}, {vp(alpha)}, {vp(V_O[qb] + i)}")
+        self.emit(f"s_mov_b32 {sp(flag)}, 0")
+        self.label(f".Ldskip{u}")
+
+    # ---------------------------------------------------------------- matrix work
+    @staticmethod
+    def mfma_scores(y_reg, z_reg):
+        """S^T = K Q^T of both blocks for the half whose K operands are in A_K."""
+        # the two blocks' accumulation chains alternate, so that consecutive
+        # MFMAs are independent
+        out = []
+        for kk in range(8):
+            for qb, dst in ((0, y_reg), (1, z_reg)):
+                c = "0" if kk == 0 else vp(dst, 16)
+                out.append(f"v_mfma_f32_32x32x16_bf16 {vp(dst, 16)}, {ap(A_K + 4 * kk, 4)}, "
+                           f"{ap(A_Q[qb] + 4 * kk, 4)}, {c}")
+        return out
+
+    @staticmethod
+    def mfma_pv(p0_reg):
+        """O^T += V^T P^T of both blocks for the half whose V operands are in A_V."""
+        out = []
+        for qb, p in ((0, p0_reg), (1, V_P1)):
+            for s in range(2):
+                for db in range(4):
+                    o = vp(V_O[qb] + 16 * db, 16)
+                    out.append(f"v_mfma_f32_32x32x16_bf16 {o}, {ap(A_V + 16 * s + 4 * db, 4)}, "
+                               f"{vp(p + 4 * s, 4)}, {o}")
+        return out
+
+    @staticmethod
+    def lds_k(buf, half):
+        base = K_REGION + buf * BUF_BYTES + half * HALF_BYTES
+        return [f"ds_read_b128 {ap(A_K + 4 * kk, 4)}, {vp(V_KOFF + kk)} offset:{base}" for kk in range(8)]
+
+    @staticmethod
+    def lds_v(buf, half):
+        out = []
+        for s in range(2):
+            imm = buf * BUF_BYTES + 16 * (2 * half + s) * 256
+            for db in range(4):
+                a = A_V + 16 * s + 4 * db
+                out.append(f"ds_read_b64_tr_b16 {ap(a, 2)}, {vp(V_VADDR + db)} offset:{imm}")
+                out.append(f"ds_read_b64_tr_b16 {ap(a + 2, 2)}, {vp(V_VADDR + 4 + db)} offset:{imm}")
+        return out
+
+    def phase(self, mfma, lds, valu, lds_start=2):
+        """Interleave 16 (or 0) MFMAs with LDS reads and a VALU list."""
+        self.emit("s_waitcnt lgkmcnt(0)")
+        if not mfma:
+            for i in lds:
+                self.emit(i)
+            for i in valu:
+                self.emit(i)
+            return
+        n = len(mfma)
+        lds_slots = [[] for _ in range(n)]
+        if lds:
+            span = max(1, min(n - lds_start, 8))
+            per = -(-len(lds) // span)
+            for k, i in enumerate(lds):
+                lds_slots[lds_start + k // per].append(i)
+        per_v = -(-len(valu) // n)
+        vi = 0
+        for s in range(n):
+            self.emit(mfma[s])
+            for i in lds_slots[s]:
+                self.emit(i)
+            for i in valu[vi:vi + per_v]:
+                self.emit(i)
+            vi += per_v
+        for i in valu[vi:]:
+            self.emit(i)
+
+    # ---------------------------------------------------------------- output
+    def write_state(self, rows, which):
+        """Normalised O and LSE of both blocks. rows: to the output rows
+        (out / lse, or out_local / lse_local when which = 1); else to partial
+        slot S_SLOT (part `which`)."""
+        u = self.new_uid()
+        T = V_T
+        if rows:
+            optr, lptr = (A_OUT, A_LSE) if which == 0 else (A_OUTL, A_LSEL)
+            # O: base = out + (qrow_b * ld + hoff) * 4; this wave's rows that exist
+            self.mul64(S_X, S_Y, S_QROWB, A_LD4)
+            self.emit(f"s_lshl_b32 {sp(S_W)}, {sp(S_HOFF2)}, 1",
+                      f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_W)}", f"s_addc_u32 {sp(S_Y)}, {sp(S_Y)}, 0")
+            self.add64_to(S_RO, optr, S_X, S_Y)
+            self.emit(f"s_sub_i32 {sp(S_W)}, {sp(A_NQ)}, {sp(S_QROWB)}",
+                      f"s_min_i32 {sp(S_W)}, {sp(S_W)}, 64",
+                      f"s_max_i32 {sp(S_W)}, {sp(S_W)}, 0",
+                      f"s_mul_i32 {sp(S_RO + 2)}, {sp(S_W)}, {sp(A_LD4)}",     # (covers the rows' head slices)
+                      f"s_mov_b32 {sp(S_RO + 3)}, 0x20000",
+                      f"s_mov_b32 {sp(S_X)}, {sp(A_LD4)}")                    # lane stride
+            # LSE: base = lse + (head * n_q + qrow_b) * 4; none when the pointer is null
+            self.emit(f"s_mul_i32 {sp(S_Y)}, {sp(S_HEAD)}, {sp(A_NQ)}",
+                      f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_QROWB)}",
+                      f"s_mul_hi_u32 {sp(S_RL + 3)}, {sp(S_Y)}, 4",
+                      f"s_mul_i32 {sp(S_Y)}, {sp(S_Y)}, 4")
+            self.emit(f"s_add_u32 {sp(S_RL)}, {sp(lptr)}, {sp(S_Y)}",
+                      f"s_addc_u32 {sp(S_RL + 1)}, {sp(lptr + 1)}, {sp(S_RL + 3)}",
+                      f"s_lshl_b32 {sp(S_RL + 2)}, {sp(S_W)}, 2",
+                      f"s_cmp_eq_u64 {sp(lptr, 2)}, 0",
+                      f"s_cselect_b32 {sp(S_RL + 2)}, 0, {sp(S_RL + 2)}",
+                      f"s_mov_b32 {sp(S_RL + 3)}, 0x20000")
+        else:
+            # O: part_o + ((slot * 2 + which) * 256 + wave * 64) * 512
+            self.emit(f"s_lshl_b32 {sp(S_Y)}, {sp(S_SLOT)}, 1")
+            if which:
+                self.emit(f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, 1")
+            self.emit(f"s_lshl_b32 {sp(S_Y)}, {sp(S_Y)}, 8",
+                      f"s_lshl_b32 {sp(S_W)}, {sp(S_WAVE)}, 6",
+                      f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_W)}",           # first query of this wave's rows
+                      f"s_mov_b32 {sp(S_RO + 2)}, 512")
+            self.mul64(S_X, S_W, S_Y, S_RO + 2)
+            self.add64_to(S_RO, A_PO, S_X, S_W)
+            self.emit(f"s_mov_b32 {sp(S_RO + 2)}, 32768", f"s_mov_b32 {sp(S_RO + 3)}, 0x20000")
+            self.emit(f"s_mov_b32 {sp(S_RL + 2)}, 4")
+            self.mul64(S_X, S_W, S_Y, S_RL + 2)
+            self.add64_to(S_RL, A_PL, S_X, S_W)
+            self.emit(f"s_mov_b32 {sp(S_RL + 2)}, 256", f"s_mov_b32 {sp(S_RL + 3)}, 0x20000",
+                      f"s_mov_b32 {sp(S_X)}, 512")
+        # every P V MFMA has completed (the O registers are read below)
+        self.emit("s_nop 7", "s_nop 7", "s_nop 7",
+                  f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",              # ql
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}",         # 16 hh
+                  f"v_mov_b32_e32 {vp(V_Y)}, 0x40000000")                   # an offset past every record (the scores are dead here)
+        for qb in range(2):
+            m, l, lr = V_ST[qb], V_ST[qb] + 3, V_ST[qb] + 4
+            self.emit(f"v_mov_b32_e32 {vp(T + 2)}, {vp(l)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(l)}",
+                      f"v_mov_b32_e32 {vp(T + 4)}, {vp(lr)}", f"v_mov_b32_e32 {vp(T + 5)}, {vp(lr)}",
+                      "s_nop 1",
+                      f"v_permlane32_swap_b32 {vp(T + 2)}, {vp(T + 3)}",
+                      f"v_permlane32_swap_b32 {vp(T + 4)}, {vp(T + 5)}",
+                      "s_nop 1",
+                      f"v_add_f32_e32 {vp(T + 2)}, {vp(T + 2)}, {vp(T + 3)}",   # l total
+                      f"v_add_f32_e32 {vp(T + 4)}, {vp(T + 4)}, {vp(T + 5)}",   # lr total
+                      f"v_rcp_f32_e32 {vp(T + 4)}, {vp(T + 4)}",
+                      f"v_add_u32_e32 {vp(T + 6)}, {32 * qb}, {vp(T)}",
+                      f"v_mul_lo_u32 {vp(T + 7)}, {vp(T + 6)}, {sp(S_X)}",
+                      f"v_add_u32_e32 {vp(T + 7)}, {vp(T + 7)}, {vp(T + 1)}")  # O voffset
+            for db in range(4):
+                for j in range(4):
+                    d = T + 8 + 4 * (j & 1)
+                    src = V_O[qb] + 16 * db + 4 * j
+                    for i in range(4):
+                        self.emit(f"v_mul_f32_e32 {vp(d + i)}, {vp(T + 4)}, {vp(src + i)}")
+                    self.emit(f"buffer_store_dwordx4 {vp(d, 4)}, {vp(T + 7)}, {sp(S_RO, 4)}, 0 offen "
+                              f"offset:{128 * db + 32 * j}")
+            # LSE = m scale + ln(l total), from the lanes of the lower half
+            self.emit(f"v_log_f32_e32 {vp(T + 2)}, {vp(T + 2)}",
+                      f"v_lshlrev_b32_e32 {vp(T + 6)}, 2, {vp(T + 6)}",
+                      f"v_cmp_ne_u32_e32 vcc, 0, {vp(T + 1)}",
+                      f"v_mul_f32_e32 {vp(T + 2)}, 0x3f317218, {vp(T + 2)}",
+                      f"v_fma_f32 {vp(T + 3)}, {vp(m)}, {sp(A_SCALE)}, {vp(T + 2)}",
+                      f"v_cndmask_b32_e32 {vp(T + 6)}, {vp(T + 6)}, {vp(V_Y)}, vcc",
+                      "s_nop 1",
+                      f"buffer_store_dword {vp(T + 3)}, {vp(T + 6)}, {sp(S_RL, 4)}, 0 offen")
+        self.emit("s_waitcnt vmcnt(0)")
+        del u
+
+    # ---------------------------------------------------------------- tile loop
+    def prologue(self, b):
+        """Restart of the compute pipeline at tile t (ring buffer b): the K
+        operands of its first half are in registers."""
+        self.label(f".Lpro{b}")
+        self.emit("s_waitcnt lgkmcnt(0)")
+        for i in self.mfma_scores(V_Y, V_Z[0]):
+            self.emit(i)
+        self.emit("s_nop 7")
+        for i in self.lds_k(b, 1):
+            self.emit(i)
+        self.emit("s_nop 7", "s_nop 7", "s_nop 7")
+        for i in self.softmax(0, V_Y, V_P0[0], S_NV + b, 0):
+            self.emit(i)
+        self.deferred_rescale(0)
+        self.emit(f"s_branch .Ltile{b}")
+
+    def tile_body(self, B):
+        nb = (B + 1) & 3
+        self.label(f".Ltile{B}")
+        self.emit(f"s_sub_i32 {sp(S_BUDGET)}, {sp(S_BUDGET)}, 1",
+                  f"s_cmp_lt_i32 {sp(S_BUDGET)}, 0",
+                  "s_cbranch_scc1 .Lend")
+        # A(2t): scores of half 2t+1 | softmax of half 2t, block 1 | V of half 2t
+        self.phase(self.mfma_scores(V_Y, V_Z[1]), self.lds_v(B, 0),
+                   self.softmax(1, V_Z[0], V_P1, S_NV + B, 0))
+        self.deferred_rescale(1)
+        # barrier: tile t+1 resident everywhere; tile t-1's buffer is free
+        u = self.new_uid()
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2",
+                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
+                  f"s_cbranch_scc0 .Lw0_{u}",
+                  "s_waitcnt vmcnt(8)",
+                  f"s_branch .Lw1_{u}",
+                  f".Lw0_{u}:",
+                  "s_waitcnt vmcnt(0)",
+                  f".Lw1_{u}:",
+                  "s_barrier")
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 3")
+        self.stage_if(S_X, (B + 3) & 3)
+        # B(2t): P V of half 2t | softmax of half 2t+1, block 0 | K of half 2t+2
+        self.phase(self.mfma_pv(V_P0[0]), self.lds_k(nb, 0),
+                   self.softmax(0, V_Y, V_P0[1], S_NV + B, 1))
+        self.deferred_rescale(0)
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1",
+                  f"s_cmp_eq_u32 {sp(S_X)}, {sp(S_FL)}",
+                  f"s_cbranch_scc1 .Ltail{B}")
+        # A(2t+1): scores of half 2t+2 | softmax of half 2t+1, block 1 | V of half 2t+1
+        self.phase(self.mfma_scores(V_Y, V_Z[0]), self.lds_v(B, 1),
+                   self.softmax(1, V_Z[1], V_P1, S_NV + B, 1))
+        self.deferred_rescale(1)
+        # B(2t+1): P V of half 2t+1 | softmax of half 2t+2, block 0 | K of half 2t+3
+        self.phase(self.mfma_pv(V_P0[1]), self.lds_k(nb, 1),
+                   self.softmax(0, V_Y, V_P0[0], S_NV + nb, 0))
+        self.deferred_rescale(0)
+        self.emit(f"s_add_u32 {sp(S_T)}, {sp(S_T)}, 1")
+        if B == 3:
+            self.emit(".Ltile_wrap:", "s_branch .Ltile0")
+
+    def tail(self, B):
+        """Last half of tile t before a flush point: no scores of the next
+        half, no softmax of the next half."""
+        nb = (B + 1) & 3
+        self.label(f".Ltail{B}")
+        self.phase([], self.lds_v(B, 1), self.softmax(1, V_Z[1], V_P1, S_NV + B, 1))
+        self.deferred_rescale(1)
+        self.phase(self.mfma_pv(V_P0[1]), [], [])
+        self.emit(f"s_add_u32 {sp(S_T)}, {sp(S_T)}, 1",
+                  f"s_cmp_eq_u32 {sp(S_T)}, {sp(S_TB)}",
+                  "s_cbranch_scc1 .Lpiece_end")
+        # dual-stream snapshot at the end of the local set: O, LSE of the
+        # local keys, to the local output (piece from tile 0) or the slot
+        u = self.new_uid()
+        self.emit(f"s_cmp_eq_u32 {sp(S_TA)}, 0", f"s_cbranch_scc0 .Lsnap_slot{u}")
+        self.write_state(True, 1)
+        self.emit(f"s_branch .Lsnap_done{u}", f".Lsnap_slot{u}:")
+        self.write_state(False, 1)
+        self.emit(f".Lsnap_done{u}:",
+                  f"s_mov_b32 {sp(S_FL)}, {sp(S_TB)}",
+                  f"s_branch .Lpro{nb}")
+
+    # ---------------------------------------------------------------- kernel
+    def lane_constants(self):
+        T = V_T
+        self.emit(f"v_and_b32_e32 {vp(V_LANE)}, 63, {vp(V_TID)}")
+        # K operand addresses: row ql, chunk (2 kk + hh) ^ (ql & 15)
+        self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",            # ql
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",      # hh
+                  f"v_and_b32_e32 {vp(T + 2)}, 15, {vp(V_LANE)}")        # ql & 15
+        for kk in range(8):
+            self.emit(f"v_add_u32_e32 {vp(T + 3)}, {2 * kk}, {vp(T + 1)}",
+                      f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 2)}",
+                      f"v_lshlrev_b32_e32 {vp(T + 3)}, 4, {vp(T + 3)}",
+                      f"v_lshl_add_u32 {vp(V_KOFF + kk)}, {vp(T)}, 8, {vp(T + 3)}")
+        # V transpose-read addresses: with sl = lane & 15, g1 = (lane >> 4) & 1:
+        # row = 8 h2 + 4 hh + (sl >> 2), chunk = 4 db + 2 g1 + ((sl & 3) >> 1),
+        # swizzle = 4 (sl >> 2) ^ 2 hh, plus 8 bytes for odd sl
+        self.emit(f"v_and_b32_e32 {vp(T + 2)}, 15, {vp(V_LANE)}",        # sl
+                  f"v_lshrrev_b32_e32 {vp(T + 3)}, 2, {vp(T + 2)}",      # sl >> 2
+                  f"v_bfe_u32 {vp(T + 4)}, {vp(V_LANE)}, 4, 1",          # g1
+                  f"v_bfe_u32 {vp(T + 5)}, {vp(T + 2)}, 1, 1",           # (sl & 3) >> 1
+                  f"v_and_b32_e32 {vp(T + 6)}, 1, {vp(T + 2)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 6)}, 3, {vp(T + 6)}",      # 8 (sl & 1)
+                  f"v_lshlrev_b32_e32 {vp(T + 7)}, 2, {vp(T + 3)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 8)}, 1, {vp(T + 1)}",
+                  f"v_xor_b32_e32 {vp(T + 7)}, {vp(T + 7)}, {vp(T + 8)}",  # swizzle
+                  f"v_lshlrev_b32_e32 {vp(T + 8)}, 2, {vp(T + 1)}",
+                  f"v_add_u32_e32 {vp(T + 8)}, {vp(T + 8)}, {vp(T + 3)}",   # 4 hh + (sl >> 2)
+                  f"v_lshlrev_b32_e32 {vp(T + 9)}, 1, {vp(T + 4)}",
+                  f"v_add_u32_e32 {vp(T + 9)}, {vp(T + 9)}, {vp(T + 5)}")   # 2 g1 + ((sl & 3) >> 1)
+        for h2 in range(2):
+            for db in range(4):
+                r = V_VADDR + 4 * h2 + db
+                self.emit(f"v_add_u32_e32 {vp(T + 10)}, {8 * h2}, {vp(T + 8)}",          # row
+                          f"v_add_u32_e32 {vp(T + 11)}, {4 * db}, {vp(T + 9)}",          # chunk
+                          f"v_xor_b32_e32 {vp(T + 11)}, {vp(T + 11)}, {vp(T + 7)}",
+                          f"v_lshlrev_b32_e32 {vp(T + 11)}, 4, {vp(T + 11)}",
+                          f"v_lshl_add_u32 {vp(r)}, {vp(T + 10)}, 8, {vp(T + 11)}",
+                          f"v_add_u32_e32 {vp(r)}, {vp(r)}, {vp(T + 6)}",
+                          f"v_add_u32_e32 {vp(r)}, 0x{V_REGION:x}, {vp(r)}")
+        # staging voffsets of thread tid: row = tid >> 4, stored chunk st = tid & 15;
+        # K: chunk st ^ row, V: st ^ (4 (row & 3) ^ 2 ((row >> 2) & 1)); load q adds 16 q rows
+        self.emit(f"v_lshrrev_b32_e32 {vp(T)}, 4, {vp(V_TID)}",          # row
+                  f"v_and_b32_e32 {vp(T + 1)}, 15, {vp(V_TID)}",         # st
+                  f"v_xor_b32_e32 {vp(T + 2)}, {vp(T + 1)}, {vp(T)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 2)}, 4, {vp(T + 2)}",      # K chunk bytes
+                  f"v_and_b32_e32 {vp(T + 3)}, 3, {vp(T)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 3)}, 2, {vp(T + 3)}",
+                  f"v_bfe_u32 {vp(T + 4)}, {vp(T)}, 2, 1",
+                  f"v_lshlrev_b32_e32 {vp(T + 4)}, 1, {vp(T + 4)}",
+                  f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 4)}",
+                  f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 1)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 3)}, 4, {vp(T + 3)}")      # V chunk bytes
+        for q in range(4):
+            self.emit(f"v_add_u32_e32 {vp(T + 5)}, {16 * q}, {vp(T)}",
+                      f"v_mul_lo_u32 {vp(T + 5)}, {vp(T + 5)}, {sp(A_LD2)}",
+                      f"v_add_u32_e32 {vp(V_STK + q)}, {vp(T + 5)}, {vp(T + 2)}",
+                      f"v_add_u32_e32 {vp(V_STV + q)}, {vp(T + 5)}, {vp(T + 3)}")
+        # Q load voffsets: row (32 qb + ql), bytes 16 hh within the head's slice
+        self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}")
+        for qb in range(2):
+            self.emit(f"v_add_u32_e32 {vp(T + 2)}, {32 * qb}, {vp(T)}",
+                      f"v_mul_lo_u32 {vp(T + 2)}, {vp(T + 2)}, {sp(A_LD2)}",
+                      f"v_add_u32_e32 {vp(V_QOFF + qb)}, {vp(T + 2)}, {vp(T + 1)}")
+
+    def piece_start(self):
+        """Set up a piece: slot, head, Q operands, fresh state, the first
+        three tiles staged, the K operands of the first half read."""
+        T = V_T
+        self.label(".Lpiece")
+        # ta, tb, slot, head, qtile, hoff
+        self.emit(f"s_mul_i32 {sp(S_X)}, {sp(S_ITEM)}, {sp(A_T)}",
+                  f"s_sub_i32 {sp(S_TA)}, {sp(S_U0)}, {sp(S_X)}",
+                  f"s_max_i32 {sp(S_TA)}, {sp(S_TA)}, 0",
+                  f"s_sub_i32 {sp(S_TB)}, {sp(S_U1)}, {sp(S_X)}",
+                  f"s_min_i32 {sp(S_TB)}, {sp(S_TB)}, {sp(A_T)}",
+                  f"s_cmp_ge_i32 {sp(S_TA)}, {sp(S_TB)}",
+                  "s_cbranch_scc1 .Lnext_item",
+                  f"s_mul_i32 {sp(S_SLOT)}, {sp(S_G)}, {sp(A_MAXP)}",
+                  f"s_add_u32 {sp(S_SLOT)}, {sp(S_SLOT)}, {sp(S_ITEM)}",
+                  f"s_sub_u32 {sp(S_SLOT)}, {sp(S_SLOT)}, {sp(S_IFIRST)}")
+        self.udiv(S_HEAD, S_ITEM, A_QT)
+        self.emit(f"s_mul_i32 {sp(S_X)}, {sp(S_HEAD)}, {sp(A_QT)}",
+                  f"s_sub_u32 {sp(S_QTILE)}, {sp(S_ITEM)}, {sp(S_X)}",
+                  f"s_lshl_b32 {sp(S_HOFF2)}, {sp(S_HEAD)}, 8",               # head * 128 * 2 bytes
+                  f"s_lshl_b32 {sp(S_QROWB)}, {sp(S_QTILE)}, 8",
+                  f"s_lshl_b32 {sp(S_X)}, {sp(S_WAVE)}, 6",
+                  f"s_add_u32 {sp(S_QROWB)}, {sp(S_QROWB)}, {sp(S_X)}")        # first query row of this wave
+        # flush point: the end of the local set when it falls inside the piece
+        self.emit(f"s_mov_b32 {sp(S_FL)}, {sp(S_TB)}",
+                  f"s_cmp_eq_u32 {sp(A_DUAL)}, 0",
+                  "s_cbranch_scc1 .Lfl_done",
+                  f"s_cmp_lt_i32 {sp(S_TA)}, {sp(A_LT)}",
+                  "s_cbranch_scc0 .Lfl_done",
+                  f"s_cmp_lt_i32 {sp(A_LT)}, {sp(S_TB)}",
+                  f"s_cselect_b32 {sp(S_FL)}, {sp(A_LT)}, {sp(S_FL)}",
+                  ".Lfl_done:")
+        # every wave is done with the previous piece's LDS tiles
+        self.emit("s_barrier")
+        self.emit(f"s_mov_b32 {sp(S_T)}, {sp(S_TA)}")
+        self.stage(S_T, 0)
+        # Q resource: rows of this wave that exist; the head's 256 bytes of each
+        self.mul64(S_X, S_Y, S_QROWB, A_LD2)
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_HOFF2)}", f"s_addc_u32 {sp(S_Y)}, {sp(S_Y)}, 0")
+        self.add64_to(S_RQ, A_QPTR, S_X, S_Y)
+        self.emit(f"s_sub_i32 {sp(S_W)}, {sp(A_NQ)}, {sp(S_QROWB)}",
+                  f"s_min_i32 {sp(S_W)}, {sp(S_W)}, 64",
+                  f"s_max_i32 {sp(S_W)}, {sp(S_W)}, 0",
+                  f"s_mul_i32 {sp(S_RQ + 2)}, {sp(S_W)}, {sp(A_LD2)}",
+                  f"s_mov_b32 {sp(S_RQ + 3)}, 0x20000")
+        for qb in range(2):
+            for kk in range(8):
+                self.emit(f"buffer_load_dwordx4 {ap(A_Q[qb] + 4 * kk, 4)}, {vp(V_QOFF + qb)}, {sp(S_RQ, 4)}, 0 "
+                          f"offen offset:{32 * kk}")
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1")
+        self.stage_if(S_X, 1)
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2")
+        self.stage_if(S_X, 2)
+        # fresh softmax state and O
+        for qb in range(2):
+            m, thr, nmc, l, lr, alpha = (V_ST[qb] + i for i in range(6))
+            self.emit(f"v_mov_b32_e32 {vp(m)}, 0xff800000", f"v_mov_b32_e32 {vp(thr)}, 0xff800000",
+                      f"v_mov_b32_e32 {vp(nmc)}, 0", f"v_mov_b32_e32 {vp(l)}, 0", f"v_mov_b32_e32 {vp(lr)}, 0",
+                      f"v_mov_b32_e32 {vp(alpha)}, 1.0")
+            for i in range(64):
+                self.emit(f"v_mov_b32_e32 {vp(V_O[qb] + i)}, 0")
+        self.emit(f"s_mov_b32 {sp(S_FLAG[0])}, 0", f"s_mov_b32 {sp(S_FLAG[1])}, 0")
+        # wait for tile ta and Q (the loads of tiles ta+1, ta+2 may stay in flight)
+        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2",
+                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
+                  "s_cbranch_scc1 .Lps_w16",
+                  f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1",
+                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
+                  "s_cbranch_scc1 .Lps_w8",
+                  "s_waitcnt vmcnt(0)",
+                  "s_branch .Lps_wd",
+                  ".Lps_w16:",
+                  "s_waitcnt vmcnt(16)",
+                  "s_branch .Lps_wd",
+                  ".Lps_w8:",
+                  "s_waitcnt vmcnt(8)",
+                  ".Lps_wd:",
+                  "s_barrier")
+        for i in self.lds_k(0, 0):
+            self.emit(i)
+        self.emit("s_branch .Lpro0")
+
+    def piece_end(self):
+        self.label(".Lpiece_end")
+        # end state: to the output rows when the piece is the whole item
+        self.emit(f"s_cmp_eq_u32 {sp(S_TA)}, 0", "s_cbranch_scc0 .Lpe_slot",
+                  f"s_cmp_eq_u32 {sp(S_TB)}, {sp(A_T)}", "s_cbranch_scc0 .Lpe_slot")
+        self.write_state(True, 0)
+        self.emit("s_branch .Lpe_local", ".Lpe_slot:")
+        self.write_state(False, 0)
+        self.label(".Lpe_local")
+        # a piece that ends inside (or at the end of) the local set also holds
+        # its local result
+        self.emit(f"s_cmp_eq_u32 {sp(A_DUAL)}, 0", "s_cbranch_scc1 .Lnext_item",
+                  f"s_cmp_le_i32 {sp(S_TB)}, {sp(A_LT)}", "s_cbranch_scc0 .Lnext_item",
+                  f"s_cmp_eq_u32 {sp(S_TA)}, 0", "s_cbranch_scc0 .Lpl_slot",
+                  f"s_cmp_eq_u32 {sp(S_TB)}, {sp(A_LT)}", "s_cbranch_scc0 .Lpl_slot")
+        self.write_state(True, 1)
+        self.emit("s_branch .Lnext_item", ".Lpl_slot:")
+        self.write_state(False, 1)
+        self.label(".Lnext_item")
+        self.emit(f"s_sub_i32 {sp(S_ITEM)}, {sp(S_ITEM)}, 1",
+                  f"s_cmp_ge_i32 {sp(S_ITEM)}, {sp(S_IFIRST)}",
+                  "s_cbranch_scc1 .Lpiece",
+                  "s_branch .Lend")
+
+    def kernel(self):
+        self.emit(f"s_load_dwordx16 {sp(S_ARG, 16)}, s[0:1], 0x0",
+                  f"s_load_dwordx16 {sp(S_ARG + 16, 16)}, s[0:1], 0x40",
+                  f"s_load_dwordx16 {sp(S_ARG + 32, 16)}, s[0:1], 0x80",
+                  f"v_lshrrev_b32_e32 {vp(V_T)}, 6, {vp(V_TID)}",
+                  "s_nop 1",
+                  f"v_readfirstlane_b32 {sp(S_WAVE)}, {vp(V_T)}",
+                  "s_waitcnt lgkmcnt(0)",
+                  f"s_lshl_b32 {sp(S_WAVE1K)}, {sp(S_WAVE)}, 10",
+                  # XCD-aware workgroup index
+                  f"s_and_b32 {sp(S_X)}, s2, 7",
+                  f"s_mul_i32 {sp(S_X)}, {sp(S_X)}, {sp(A_PERXCD)}",
+                  f"s_lshr_b32 {sp(S_Y)}, s2, 3",
+                  f"s_add_u32 {sp(S_G)}, {sp(S_X)}, {sp(S_Y)}",
+                  f"s_cmp_ge_u32 {sp(S_G)}, {sp(A_NLOG)}",
+                  "s_cbranch_scc1 .Lend",
+                  f"s_cmp_eq_u32 {sp(A_NSEG)}, 0",
+                  "s_cbranch_scc1 .Lnosplit",
+                  f"s_mul_i32 {sp(S_Y)}, {sp(S_G)}, {sp(A_U)}")
+        self.udiv(S_U0, S_Y, A_NSEG)
+        self.emit(f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(A_U)}")
+        self.udiv(S_U1, S_Y, A_NSEG)
+        self.emit("s_branch .Lhave_u", ".Lnosplit:",
+                  f"s_mul_i32 {sp(S_U0)}, {sp(S_G)}, {sp(A_T)}",
+                  f"s_add_u32 {sp(S_U1)}, {sp(S_U0)}, {sp(A_T)}",
+                  ".Lhave_u:")
+        self.udiv(S_IFIRST, S_U0, A_T)
+        self.emit(f"s_sub_u32 {sp(S_Y)}, {sp(S_U1)}, 1")
+        self.udiv(S_ITEM, S_Y, A_T)
+        self.emit(f"s_sub_u32 {sp(S_BUDGET)}, {sp(S_U1)}, {sp(S_U0)}",
+                  f"s_add_u32 {sp(S_BUDGET)}, {sp(S_BUDGET)}, 16",
+                  f"s_mov_b32 {sp(S_SLOT)}, 0")
+        self.lane_constants()
+        self.piece_start()
+        for b in range(4):
+            self.prologue(b)
+        for B in range(4):
+            self.tile_body(B)
+        for B in range(4):
+            self.tail(B)
+        self.piece_end()
+        self.label(".Lend")
+        self.emit("s_endpgm")
+        for blk in self.ool:
+            for i in blk:
+                self.emit(i)
+
+    def text(self):
+        self.kernel()
+        head = f"""\t.amdgcn_target "amdgcn-amd-amdhsa--gfx950"
+\t.amdhsa_code_object_version 5
+\t.text
+\t.globl {KNAME}
+\t.p2align 8
+\t.type {KNAME},@function
+{KNAME}:
+"""
+        body = "\n".join(self.lines)
+        tail = f"""
+\t.section .rodata,"a",@progbits
+\t.p2align 6, 0x0
+\t.amdhsa_kernel {KNAME}
+\t\t.amdhsa_group_segment_fixed_size {LDS_BYTES}
+\t\t.amdhsa_private_segment_fixed_size 0
+\t\t.amdhsa_kernarg_size {ARGS_BYTES}
+\t\t.amdhsa_user_sgpr_count 2
+\t\t.amdhsa_user_sgpr_kernarg_segment_ptr 1
+\t\t.amdhsa_system_sgpr_workgroup_id_x 1
+\t\t.amdhsa_system_vgpr_workitem_id 0
+\t\t.amdhsa_next_free_vgpr 384
+\t\t.amdhsa_next_free_sgpr 102
+\t\t.amdhsa_accum_offset 256
+\t\t.amdhsa_reserve_vcc 1
+\t\t.amdhsa_float_denorm_mode_32 3
+\t\t.amdhsa_float_denorm_mode_16_64 3
+\t\t.amdhsa_dx10_clamp 1
+\t\t.amdhsa_ieee_mode 1
+\t.end_amdhsa_kernel
+\t.amdgpu_metadata
+---
+amdhsa.kernels:
+  - .agpr_count:     128
+    .args:
+      - .offset:         0
+        .size:           {ARGS_BYTES}
+        .value_kind:     by_value
+    .group_segment_fixed_size: {LDS_BYTES}
+    .kernarg_segment_align: 8
+    .kernarg_segment_size: {ARGS_BYTES}
+    .max_flat_workgroup_size: 256
+    .name:           {KNAME}
+    .private_segment_fixed_size: 0
+    .sgpr_count:     104
+    .sgpr_spill_count: 0
+    .symbol:         {KNAME}.kd
+    .uniform_work_group_size: 1
+    .vgpr_count:     384
+    .vgpr_spill_count: 0
+    .wavefront_size: 64
+amdhsa.target:   amdgcn-amd-amdhsa--gfx950
+amdhsa.version:
+  - 1
+  - 2
+...
+\t.end_amdgpu_metadata
+"""
+        return head + body + "\n" + tail
+
+
+def generate():
+    return Gen().text()
+
+
+if __name__ == "__main__":
+    sys.stdout.write(generate())

@@ -73,6 +73,11 @@ int attn_cu_count();
 // units/n_seg/max_pieces (n_seg = 0: no split) and returns the workspace bytes.
 size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit* s);
 hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream);
+// The hand-scheduled head_dim-128 kernel (attn_fast.cpp): whether it takes
+// this launch (its 32-bit work arithmetic fits and its code object loaded on
+// the current device), and the launch itself (the split's merge excluded).
+bool attn_fast_eligible(const AttnArgs& a, int head_dim);
+hipError_t launch_attn_fast(const AttnArgs& a, hipStream_t stream);
 // out = 0, lse = -inf (attention over an empty key set)
 hipError_t launch_attn_empty(float* out, float* lse, int64_t n_q, int64_t n_heads, int head_dim,
                              hipStream_t stream);
