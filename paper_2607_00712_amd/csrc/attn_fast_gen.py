@@ -46,6 +46,9 @@ V_O = (128, 192)    # 64 each: O^T of block 0 / 1, dBlock db at +16 db
 A_Q = (0, 32)       # Q^T operands of block 0 / 1, slice kk at +4 kk
 A_K = 64            # K operands of one half, slice kk at +4 kk
 A_V = 96            # V^T operands of one half, slice s and dBlock db at +16 s + 4 db
+A_ONES = 128        # an all-ones bf16 operand: (ones) P^T sums the bf16 weights of each query
+A_LR = (132, 148)   # 16 each: those sums (every row of the 32 x 32 block holds them), per block
+N_AGPR = 164
 
 # SGPRs
 S_ARG = 8           # kernel arguments s[8:55]
@@ -143,53 +146,61 @@ class Gen:
                   f"s_addc_u32 {sp(s_dst + 1)}, {sp(s_base + 1)}, {sp(s_hi)}")
 
     # ---------------------------------------------------------------- staging
-    def stage(self, s_tile, buf):
+    def stage_list(self, s_tile, buf):
         """Direct HBM -> LDS loads of key tile s_tile (K and V, 64 rows) into
-        ring buffer `buf`, and its valid-key count into s_nv[buf]."""
+        ring buffer `buf`, and its valid-key count into s_nv[buf], as an
+        instruction list. A tile at or past the piece end (s_tile >= tb) gets
+        a resource with no records: its loads fetch nothing and fill the (then
+        unused) buffer with zeros, so the launch needs no branch and every
+        tile step issues the same number of loads."""
         nv = S_NV + buf
-        b, e, f = S_RO, S_RO + 1, S_RO + 2   # (the output resource is only live inside write_state)
-        self.emit(f"s_mov_b32 {sp(b)}, {sp(A_B0)}", f"s_mov_b32 {sp(e)}, {sp(A_E0)}", f"s_mov_b32 {sp(f)}, 0",
-                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB1)}",
-                  f"s_cselect_b32 {sp(b)}, {sp(A_B1)}, {sp(b)}",
-                  f"s_cselect_b32 {sp(e)}, {sp(A_E1)}, {sp(e)}",
-                  f"s_cselect_b32 {sp(f)}, {sp(A_TB1)}, {sp(f)}",
-                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB2)}",
-                  f"s_cselect_b32 {sp(b)}, {sp(A_B2)}, {sp(b)}",
-                  f"s_cselect_b32 {sp(e)}, {sp(A_E2)}, {sp(e)}",
-                  f"s_cselect_b32 {sp(f)}, {sp(A_TB2)}, {sp(f)}",
-                  f"s_sub_i32 {sp(S_X)}, {sp(s_tile)}, {sp(f)}",
-                  f"s_lshl_b32 {sp(S_X)}, {sp(S_X)}, 6",
-                  f"s_add_i32 {sp(S_X)}, {sp(b)}, {sp(S_X)}",          # key0
-                  f"s_sub_i32 {sp(nv)}, {sp(e)}, {sp(S_X)}",
-                  f"s_min_i32 {sp(nv)}, {sp(nv)}, 64")
-        # byte offset of the tile's first row in this head: key0 * ld * 2 + hoff * 2
-        self.mul64(S_Y, S_W, S_X, A_LD2)
-        self.emit(f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_HOFF2)}", f"s_addc_u32 {sp(S_W)}, {sp(S_W)}, 0")
-        self.add64_to(S_RK, A_KPTR, S_Y, S_W)
-        self.add64_to(S_RV, A_VPTR, S_Y, S_W)
-        # records: the tile's valid rows (rows past them read as zero)
-        self.emit(f"s_sub_i32 {sp(S_X)}, {sp(nv)}, 1",
-                  f"s_mul_i32 {sp(S_X)}, {sp(S_X)}, {sp(A_LD2)}",
-                  f"s_add_u32 {sp(S_RK + 2)}, {sp(S_X)}, 0x100",
-                  f"s_mov_b32 {sp(S_RV + 2)}, {sp(S_RK + 2)}",
-                  f"s_mov_b32 {sp(S_RK + 3)}, 0x20000",
-                  f"s_mov_b32 {sp(S_RV + 3)}, 0x20000")
+        b, e, f, t = S_RO, S_RO + 1, S_RO + 2, S_RO + 3   # (free outside write_state)
+        ins = [f"s_add_i32 {sp(t)}, {sp(A_T)}, -1",
+               f"s_min_i32 {sp(t)}, {sp(s_tile)}, {sp(t)}",                # a valid tile index
+               f"s_mov_b32 {sp(b)}, {sp(A_B0)}", f"s_mov_b32 {sp(e)}, {sp(A_E0)}", f"s_mov_b32 {sp(f)}, 0",
+               f"s_cmp_ge_i32 {sp(t)}, {sp(A_TB1)}",
+               f"s_cselect_b32 {sp(b)}, {sp(A_B1)}, {sp(b)}",
+               f"s_cselect_b32 {sp(e)}, {sp(A_E1)}, {sp(e)}",
+               f"s_cselect_b32 {sp(f)}, {sp(A_TB1)}, {sp(f)}",
+               f"s_cmp_ge_i32 {sp(t)}, {sp(A_TB2)}",
+               f"s_cselect_b32 {sp(b)}, {sp(A_B2)}, {sp(b)}",
+               f"s_cselect_b32 {sp(e)}, {sp(A_E2)}, {sp(e)}",
+               f"s_cselect_b32 {sp(f)}, {sp(A_TB2)}, {sp(f)}",
+               f"s_sub_i32 {sp(f)}, {sp(t)}, {sp(f)}",
+               f"s_lshl_b32 {sp(f)}, {sp(f)}, 6",
+               f"s_add_i32 {sp(f)}, {sp(b)}, {sp(f)}",                     # key0
+               f"s_sub_i32 {sp(nv)}, {sp(e)}, {sp(f)}",
+               f"s_min_i32 {sp(nv)}, {sp(nv)}, 64",
+               # byte offset of the tile's first row in this head: key0 * ld * 2 + hoff * 2
+               f"s_mul_hi_u32 {sp(e)}, {sp(f)}, {sp(A_LD2)}",
+               f"s_mul_i32 {sp(b)}, {sp(f)}, {sp(A_LD2)}",
+               f"s_add_u32 {sp(b)}, {sp(b)}, {sp(S_HOFF2)}",
+               f"s_addc_u32 {sp(e)}, {sp(e)}, 0",
+               f"s_add_u32 {sp(S_RK)}, {sp(A_KPTR)}, {sp(b)}",
+               f"s_addc_u32 {sp(S_RK + 1)}, {sp(A_KPTR + 1)}, {sp(e)}",
+               f"s_add_u32 {sp(S_RV)}, {sp(A_VPTR)}, {sp(b)}",
+               f"s_addc_u32 {sp(S_RV + 1)}, {sp(A_VPTR + 1)}, {sp(e)}",
+               # records: the tile's valid rows (rows past them read as zero); none past the piece
+               f"s_sub_i32 {sp(f)}, {sp(nv)}, 1",
+               f"s_mul_i32 {sp(f)}, {sp(f)}, {sp(A_LD2)}",
+               f"s_add_u32 {sp(f)}, {sp(f)}, 0x100",
+               f"s_cmp_lt_i32 {sp(s_tile)}, {sp(S_TB)}",
+               f"s_cselect_b32 {sp(S_RK + 2)}, {sp(f)}, 0",
+               f"s_mov_b32 {sp(S_RV + 2)}, {sp(S_RK + 2)}",
+               f"s_mov_b32 {sp(S_RK + 3)}, 0x20000",
+               f"s_mov_b32 {sp(S_RV + 3)}, 0x20000"]
         kb = K_REGION + buf * BUF_BYTES
         vb = V_REGION + buf * BUF_BYTES
         for q in range(4):
-            self.emit(f"s_add_u32 m0, {sp(S_WAVE1K)}, {kb + q * 4096}",
-                      "s_nop 0",
-                      f"buffer_load_dwordx4 {vp(V_STK + q)}, {sp(S_RK, 4)}, 0 offen lds",
-                      f"s_add_u32 m0, {sp(S_WAVE1K)}, {vb + q * 4096}",
-                      "s_nop 0",
-                      f"buffer_load_dwordx4 {vp(V_STV + q)}, {sp(S_RV, 4)}, 0 offen lds")
+            ins += [f"s_add_u32 m0, {sp(S_WAVE1K)}, {kb + q * 4096}\n  s_nop 0\n"
+                    f"  buffer_load_dwordx4 {vp(V_STK + q)}, {sp(S_RK, 4)}, 0 offen lds",
+                    f"s_add_u32 m0, {sp(S_WAVE1K)}, {vb + q * 4096}\n  s_nop 0\n"
+                    f"  buffer_load_dwordx4 {vp(V_STV + q)}, {sp(S_RV, 4)}, 0 offen lds"]
+        return ins
 
-    def stage_if(self, s_tile, buf):
-        """stage(s_tile) when s_tile < tb."""
-        u = self.new_uid()
-        self.emit(f"s_cmp_lt_i32 {sp(s_tile)}, {sp(S_TB)}", f"s_cbranch_scc0 .Lnost{u}")
-        self.stage(s_tile, buf)
-        self.label(f".Lnost{u}")
+    def stage(self, s_tile, buf):
+        for i in self.stage_list(s_tile, buf):
+            self.emit(i)
 
     # ---------------------------------------------------------------- softmax
     def softmax(self, qb, s_base, p_base, nv_reg, half):
@@ -220,11 +231,15 @@ class Gen:
                      f"v_cndmask_b32_e32 {vp(S[r])}, {vp(S[r])}, {vp(T + 1)}, vcc"]
         mask += [f"s_branch .Lmback{u}"]
         self.ool.append(mask)
-        # row max over the 16 scores and the lane pair
-        ins += [f"v_maximum3_f32 {vp(T)}, {vp(S[0])}, {vp(S[1])}, {vp(S[2])}"]
-        for r in range(3, 15, 2):
-            ins += [f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(S[r])}, {vp(S[r + 1])}"]
-        ins += [f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(S[15])}, {vp(S[15])}",
+        # row max over the 16 scores (a tree of depth three) and the lane pair
+        ins += [f"v_maximum3_f32 {vp(T)}, {vp(S[0])}, {vp(S[1])}, {vp(S[2])}",
+                f"v_maximum3_f32 {vp(T + 1)}, {vp(S[3])}, {vp(S[4])}, {vp(S[5])}",
+                f"v_maximum3_f32 {vp(T + 2)}, {vp(S[6])}, {vp(S[7])}, {vp(S[8])}",
+                f"v_maximum3_f32 {vp(T + 3)}, {vp(S[9])}, {vp(S[10])}, {vp(S[11])}",
+                f"v_maximum3_f32 {vp(T + 4)}, {vp(S[12])}, {vp(S[13])}, {vp(S[14])}",
+                f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(T + 1)}, {vp(T + 2)}",
+                f"v_maximum3_f32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 4)}, {vp(S[15])}",
+                f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(T + 3)}, {vp(T + 3)}",
                 f"v_mov_b32_e32 {vp(T + 1)}, {vp(T)}",
                 "s_nop 1",
                 f"v_permlane32_swap_b32 {vp(T)}, {vp(T + 1)}",
@@ -244,21 +259,26 @@ class Gen:
                          f"v_mul_f32_e32 {vp(nmc)}, {sp(A_NEGC)}, {vp(T + 1)}",
                          "s_nop 0",
                          f"v_mul_f32_e32 {vp(l)}, {vp(alpha)}, {vp(l)}",
-                         f"v_mul_f32_e32 {vp(lr)}, {vp(alpha)}, {vp(lr)}",
                          f"s_mov_b32 {sp(flag)}, 1",
                          f"s_branch .Lrback{u}"])
-        # weights p = 2^(s c - m c), pairwise sums, bf16 pairs and their sum
+        # weights p = 2^(s c - m c) in groups of four (each exponential four
+        # instructions after its argument), then per pair of keys the fp32 sum
+        # and the bf16 pair (the bf16 weights are summed by the matrix cores)
         P = [p_base + i for i in range(8)]
-        pending = []
-        for p in range(8):
-            a, b = S[2 * p], S[2 * p + 1]
-            ins += [f"v_fma_f32 {vp(a)}, {vp(a)}, {sp(A_C)}, {vp(nmc)}", f"v_exp_f32_e32 {vp(a)}, {vp(a)}",
-                    f"v_fma_f32 {vp(b)}, {vp(b)}, {sp(A_C)}, {vp(nmc)}", f"v_exp_f32_e32 {vp(b)}, {vp(b)}"]
-            ins += pending
-            pending = [f"v_add_f32_e32 {vp(T + 2 + p)}, {vp(a)}, {vp(b)}",
-                       f"v_cvt_pk_bf16_f32 {vp(P[p])}, {vp(a)}, {vp(b)}",
-                       f"v_dot2c_f32_bf16_e32 {vp(lr)}, 0x3f803f80, {vp(P[p])}"]
-        ins += ["s_nop 0"] + pending
+        pend = []
+        for g in range(4):
+            idx = [4 * g + i for i in range(4)]
+            ins += [f"v_fma_f32 {vp(S[i])}, {vp(S[i])}, {sp(A_C)}, {vp(nmc)}" for i in idx]
+            ins += pend[:4]
+            ins += [f"v_exp_f32_e32 {vp(S[i])}, {vp(S[i])}" for i in idx]
+            ins += pend[4:]
+            pend = []
+            for pp in (2 * g, 2 * g + 1):
+                a_, b_ = S[2 * pp], S[2 * pp + 1]
+                pend += [f"v_add_f32_e32 {vp(T + 2 + pp)}, {vp(a_)}, {vp(b_)}",
+                         f"v_cvt_pk_bf16_f32 {vp(P[pp])}, {vp(a_)}, {vp(b_)}"]
+
+        ins += ["s_nop 0"] + pend
         t = [T + 2 + p for p in range(8)]
         ins += [f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[1])}",
                 f"v_add_f32_e32 {vp(t[2])}, {vp(t[2])}, {vp(t[3])}",
@@ -278,6 +298,11 @@ class Gen:
         self.emit(f"s_cmp_eq_u32 {sp(flag)}, 0", f"s_cbranch_scc1 .Ldskip{u}", "s_nop 7", "s_nop 7", "s_nop 7")
         for i in range(64):
             self.emit(f"v_mul_f32_e32 {vp(V_O[qb] + i)}, {vp(alpha)}, {vp(V_O[qb] + i)}")
+        for i in range(16):
+            t = V_T + (i & 7)
+            self.emit(f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb] + i)}",
+                      f"v_mul_f32_e32 {vp(t)}, {vp(alpha)}, {vp(t)}",
+                      f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(t)}")
         self.emit(f"s_mov_b32 {sp(flag)}, 0")
         self.label(f".Ldskip{u}")
 
@@ -305,6 +330,9 @@ class Gen:
                     o = vp(V_O[qb] + 16 * db, 16)
                     out.append(f"v_mfma_f32_32x32x16_bf16 {o}, {ap(A_V + 16 * s + 4 * db, 4)}, "
                                f"{vp(p + 4 * s, 4)}, {o}")
+            for s in range(2):
+                acc = ap(A_LR[qb], 16)
+                out.append(f"v_mfma_f32_32x32x16_bf16 {acc}, {ap(A_ONES, 4)}, {vp(p + 4 * s, 4)}, {acc}")
         return out
 
     @staticmethod
@@ -406,15 +434,13 @@ class Gen:
                   f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}",         # 16 hh
                   f"v_mov_b32_e32 {vp(V_Y)}, 0x40000000")                   # an offset past every record (the scores are dead here)
         for qb in range(2):
-            m, l, lr = V_ST[qb], V_ST[qb] + 3, V_ST[qb] + 4
+            m, l = V_ST[qb], V_ST[qb] + 3
             self.emit(f"v_mov_b32_e32 {vp(T + 2)}, {vp(l)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(l)}",
-                      f"v_mov_b32_e32 {vp(T + 4)}, {vp(lr)}", f"v_mov_b32_e32 {vp(T + 5)}, {vp(lr)}",
+                      f"v_accvgpr_read_b32 {vp(T + 4)}, {ap(A_LR[qb])}",          # lr total
                       "s_nop 1",
                       f"v_permlane32_swap_b32 {vp(T + 2)}, {vp(T + 3)}",
-                      f"v_permlane32_swap_b32 {vp(T + 4)}, {vp(T + 5)}",
                       "s_nop 1",
                       f"v_add_f32_e32 {vp(T + 2)}, {vp(T + 2)}, {vp(T + 3)}",   # l total
-                      f"v_add_f32_e32 {vp(T + 4)}, {vp(T + 4)}, {vp(T + 5)}",   # lr total
                       f"v_rcp_f32_e32 {vp(T + 4)}, {vp(T + 4)}",
                       f"v_add_u32_e32 {vp(T + 6)}, {32 * qb}, {vp(T)}",
                       f"v_mul_lo_u32 {vp(T + 7)}, {vp(T + 6)}, {sp(S_X)}",
@@ -468,20 +494,14 @@ class Gen:
         self.deferred_rescale(1)
         # barrier: tile t+1 resident everywhere; tile t-1's buffer is free
         u = self.new_uid()
-        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2",
-                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
-                  f"s_cbranch_scc0 .Lw0_{u}",
-                  "s_waitcnt vmcnt(8)",
-                  f"s_branch .Lw1_{u}",
-                  f".Lw0_{u}:",
-                  "s_waitcnt vmcnt(0)",
-                  f".Lw1_{u}:",
-                  "s_barrier")
-        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 3")
-        self.stage_if(S_X, (B + 3) & 3)
-        # B(2t): P V of half 2t | softmax of half 2t+1, block 0 | K of half 2t+2
+        # (every tile step issues the loads of one tile, so the loads of tile
+        # t+2 are the only ones that may still be in flight)
+        self.emit("s_waitcnt vmcnt(8)", "s_barrier", f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 3")
+        del u
+        # B(2t): P V of half 2t | softmax of half 2t+1, block 0 | K of half 2t+2,
+        # with the loads of tile t+3 into the buffer tile t-1 has left
         self.phase(self.mfma_pv(V_P0[0]), self.lds_k(nb, 0),
-                   self.softmax(0, V_Y, V_P0[1], S_NV + B, 1))
+                   self.stage_list(S_X, (B + 3) & 3) + self.softmax(0, V_Y, V_P0[1], S_NV + B, 1))
         self.deferred_rescale(0)
         self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1",
                   f"s_cmp_eq_u32 {sp(S_X)}, {sp(S_FL)}",
@@ -636,9 +656,9 @@ class Gen:
                 self.emit(f"buffer_load_dwordx4 {ap(A_Q[qb] + 4 * kk, 4)}, {vp(V_QOFF + qb)}, {sp(S_RQ, 4)}, 0 "
                           f"offen offset:{32 * kk}")
         self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1")
-        self.stage_if(S_X, 1)
+        self.stage(S_X, 1)
         self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2")
-        self.stage_if(S_X, 2)
+        self.stage(S_X, 2)
         # fresh softmax state and O
         for qb in range(2):
             m, thr, nmc, l, lr, alpha = (V_ST[qb] + i for i in range(6))
@@ -647,23 +667,13 @@ class Gen:
                       f"v_mov_b32_e32 {vp(alpha)}, 1.0")
             for i in range(64):
                 self.emit(f"v_mov_b32_e32 {vp(V_O[qb] + i)}, 0")
+        self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0")
+        for qb in range(2):
+            for i in range(16):
+                self.emit(f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(V_T)}")
         self.emit(f"s_mov_b32 {sp(S_FLAG[0])}, 0", f"s_mov_b32 {sp(S_FLAG[1])}, 0")
         # wait for tile ta and Q (the loads of tiles ta+1, ta+2 may stay in flight)
-        self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2",
-                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
-                  "s_cbranch_scc1 .Lps_w16",
-                  f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1",
-                  f"s_cmp_lt_i32 {sp(S_X)}, {sp(S_TB)}",
-                  "s_cbranch_scc1 .Lps_w8",
-                  "s_waitcnt vmcnt(0)",
-                  "s_branch .Lps_wd",
-                  ".Lps_w16:",
-                  "s_waitcnt vmcnt(16)",
-                  "s_branch .Lps_wd",
-                  ".Lps_w8:",
-                  "s_waitcnt vmcnt(8)",
-                  ".Lps_wd:",
-                  "s_barrier")
+        self.emit("s_waitcnt vmcnt(16)", "s_barrier")
         for i in self.lds_k(0, 0):
             self.emit(i)
         self.emit("s_branch .Lpro0")
@@ -725,6 +735,9 @@ class Gen:
                   f"s_add_u32 {sp(S_BUDGET)}, {sp(S_BUDGET)}, 16",
                   f"s_mov_b32 {sp(S_SLOT)}, 0")
         self.lane_constants()
+        self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0x3f803f80")
+        for i in range(4):
+            self.emit(f"v_accvgpr_write_b32 {ap(A_ONES + i)}, {vp(V_T)}")
         self.piece_start()
         for b in range(4):
             self.prologue(b)
@@ -761,7 +774,7 @@ class Gen:
 \t\t.amdhsa_user_sgpr_kernarg_segment_ptr 1
 \t\t.amdhsa_system_sgpr_workgroup_id_x 1
 \t\t.amdhsa_system_vgpr_workitem_id 0
-\t\t.amdhsa_next_free_vgpr 384
+\t\t.amdhsa_next_free_vgpr {256 + (N_AGPR + 7) // 8 * 8}
 \t\t.amdhsa_next_free_sgpr 102
 \t\t.amdhsa_accum_offset 256
 \t\t.amdhsa_reserve_vcc 1
@@ -773,7 +786,7 @@ class Gen:
 \t.amdgpu_metadata
 ---
 amdhsa.kernels:
-  - .agpr_count:     128
+  - .agpr_count:     {N_AGPR}
     .args:
       - .offset:         0
         .size:           {ARGS_BYTES}
@@ -788,7 +801,7 @@ amdhsa.kernels:
     .sgpr_spill_count: 0
     .symbol:         {KNAME}.kd
     .uniform_work_group_size: 1
-    .vgpr_count:     384
+    .vgpr_count:     {256 + (N_AGPR + 7) // 8 * 8}
     .vgpr_spill_count: 0
     .wavefront_size: 64
 amdhsa.target:   amdgcn-amd-amdhsa--gfx950
