@@ -72,10 +72,14 @@ MEASURED_TRAFFIC = {
 
 
 def attn_source_hash():
+    """sha256[:16] over the sources of the attention launch (the C++ kernels and
+    merge, the generator of the head_dim-128 assembly kernel and its host side)."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2607_00712_amd", "csrc", "attn_chunk.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in ("attn_chunk.hip", "attn_fast_gen.py", "attn_fast.cpp"):
+        with open(os.path.join(ROOT, "paper_2607_00712_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def flops(w):
@@ -546,7 +550,7 @@ def rollout_run(reps=3, warmup=2):
                    "layers": n_layers, "l_layers": n_l, "window": win, "sink": sink, "chunks": w["chunks"],
                    "step": "one chunk: attention of every layer (F-Layers over the whole cache, L-Layers over "
                            "their ring); median of %d timings per chunk" % reps},
-        "roofline": {"kernel": "attn_chunk_kernel<128> (F-Layer, full cache of 280800 keys, chunk 60)",
+        "roofline": {"kernel": "ispa_attn_fast_d128 (F-Layer, full cache of 280800 keys, chunk 60)",
                      "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
         "summary": {
@@ -626,7 +630,7 @@ def main():
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
-            "kernel": "attn_chunk_kernel<128> + attn_merge_split_kernel<128> (F-Layer, dual stream; one call)",
+            "kernel": "ispa_attn_fast_d128 + attn_merge_split_kernel<128> (F-Layer, dual stream; one call)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,
