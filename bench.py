@@ -66,8 +66,8 @@ PEAK_HBM_GBS = 8000.0
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "e9996bf782375818", "bytes_per_launch": 779.8e6},
-    "14b": {"attn_chunk_sha256_16": "e9996bf782375818", "bytes_per_launch": 3059.8e6},
+    "1.3b": {"attn_chunk_sha256_16": "60624b284a1a0c75", "bytes_per_launch": 767.3e6},
+    "14b": {"attn_chunk_sha256_16": "60624b284a1a0c75", "bytes_per_launch": 3059.8e6},
 }
 
 
