@@ -13,7 +13,7 @@ import numpy as np
 import torch
 
 ATTN_TOL = 2e-2
-LSE_TOL = 2e-3
+LSE_TOL = 1e-3
 GRAM_TOL = 1e-4
 DW_TOL = 1e-3
 
