@@ -35,7 +35,7 @@ V_VADDR = 10        # 8: V transpose-read addresses, [h2 * 4 + db] (include the 
 V_STK = 18          # 4: staging voffsets of the K loads q = 0..3
 V_STV = 22          # 4: staging voffsets of the V loads
 V_QOFF = 26         # 2: Q load voffsets of query blocks 0 / 1
-V_ST = (28, 34)     # per block: m, thr, nmc, l, lr, alpha
+V_ST = (28, 34)     # per block: m, lr, -m c, l, lr of the current half, alpha (lr: VALU weight sums)
 V_T = 40            # 16 temporaries v40..v55
 V_P1 = 56           # 8: P^T of block 1 (slice 0: +0..3, slice 1: +4..7)
 V_Y = 64            # 16: scores of block 0 (next half)
@@ -46,9 +46,15 @@ V_O = (128, 192)    # 64 each: O^T of block 0 / 1, dBlock db at +16 db
 A_Q = (0, 32)       # Q^T operands of block 0 / 1, slice kk at +4 kk
 A_K = 64            # K operands of one half, slice kk at +4 kk
 A_V = 96            # V^T operands of one half, slice s and dBlock db at +16 s + 4 db
+# the sum of the bf16-rounded weights (the normaliser of O): on the matrix
+# cores (an all-ones operand times P^T) or on the VALU (v_dot2c per pair)
+SUMS_ON_MFMA = True
 A_ONES = 128        # an all-ones bf16 operand: (ones) P^T sums the bf16 weights of each query
 A_LR = (132, 148)   # 16 each: those sums (every row of the 32 x 32 block holds them), per block
-N_AGPR = 164
+N_AGPR = 164 if SUMS_ON_MFMA else 128
+BF16_ONES = "0x3f803f80"
+# phase schedule: spread the non-matrix instructions by estimated issue cost
+BALANCED = True
 
 # SGPRs
 S_ARG = 8           # kernel arguments s[8:55]
@@ -56,10 +62,15 @@ S_RK, S_RV = 56, 60           # staging buffer resources
 S_RQ = 64                     # Q resource (piece start) / scratch
 S_RO, S_RL = 68, 72           # output O and LSE resources (write_state)
 S_G, S_U0, S_U1, S_ITEM, S_TA, S_TB, S_T, S_FL = 76, 77, 78, 79, 80, 81, 82, 83
-S_SLOT, S_HEAD, S_QTILE, S_HOFF2, S_WAVE, S_WAVE1K, S_QROWB, S_IFIRST = 84, 85, 86, 87, 88, 89, 90, 91
+S_SLOT, S_HEAD, S_QTILE, S_HOFF2, S_WAVE, S_WAVE4K, S_QROWB, S_IFIRST = 84, 85, 86, 87, 88, 89, 90, 91
 S_NV = 92                     # 4: valid keys of the tiles in the LDS ring
-S_FLAG = (96, 97)             # deferred O rescale of block 0 / 1
+S_REC0 = 96                   # 256 - 2 ld: buffer records of a tile are nv * 2 ld + S_REC0
+S_LD128 = 97                  # 128 ld: bytes of 64 rows
 S_BUDGET = 98
+# staging cursor: the next tile to load starts at key S_SKEY of range S_SRNG,
+# which ends at key S_SEND; S_SOFF (64-bit) is the byte offset of that key's
+# row slice of this head
+S_SKEY, S_SEND, S_SOFF, S_SRNG = 3, 4, 5, 7
 S_X, S_Y, S_W = 99, 100, 101  # scratch
 
 # kernel-argument SGPRs (byte offset / 4 + S_ARG)
@@ -146,56 +157,91 @@ class Gen:
                   f"s_addc_u32 {sp(s_dst + 1)}, {sp(s_base + 1)}, {sp(s_hi)}")
 
     # ---------------------------------------------------------------- staging
+    def stage_init(self, s_tile):
+        """Points the staging cursor at tile s_tile (a tile of the piece, so
+        below the item's tile count): its range, first key and row offset."""
+        b, e, f = S_RO, S_RO + 1, S_RO + 2   # (free outside write_state)
+        self.emit(f"s_mov_b32 {sp(b)}, {sp(A_B0)}", f"s_mov_b32 {sp(e)}, {sp(A_E0)}", f"s_mov_b32 {sp(f)}, 0",
+                  f"s_mov_b32 {sp(S_SRNG)}, 0",
+                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB1)}",
+                  f"s_cselect_b32 {sp(b)}, {sp(A_B1)}, {sp(b)}",
+                  f"s_cselect_b32 {sp(e)}, {sp(A_E1)}, {sp(e)}",
+                  f"s_cselect_b32 {sp(f)}, {sp(A_TB1)}, {sp(f)}",
+                  f"s_cselect_b32 {sp(S_SRNG)}, 1, {sp(S_SRNG)}",
+                  f"s_cmp_ge_i32 {sp(s_tile)}, {sp(A_TB2)}",
+                  f"s_cselect_b32 {sp(b)}, {sp(A_B2)}, {sp(b)}",
+                  f"s_cselect_b32 {sp(e)}, {sp(A_E2)}, {sp(e)}",
+                  f"s_cselect_b32 {sp(f)}, {sp(A_TB2)}, {sp(f)}",
+                  f"s_cselect_b32 {sp(S_SRNG)}, 2, {sp(S_SRNG)}",
+                  f"s_sub_i32 {sp(f)}, {sp(s_tile)}, {sp(f)}",
+                  f"s_lshl_b32 {sp(f)}, {sp(f)}, 6",
+                  f"s_add_i32 {sp(S_SKEY)}, {sp(b)}, {sp(f)}",
+                  f"s_mov_b32 {sp(S_SEND)}, {sp(e)}")
+        self.emit(*self.cursor_offset())
+
+    @staticmethod
+    def cursor_offset():
+        """S_SOFF = S_SKEY * 2 ld + 2 head_offset (64-bit)."""
+        return [f"s_mul_hi_u32 {sp(S_SOFF + 1)}, {sp(S_SKEY)}, {sp(A_LD2)}",
+                f"s_mul_i32 {sp(S_SOFF)}, {sp(S_SKEY)}, {sp(A_LD2)}",
+                f"s_add_u32 {sp(S_SOFF)}, {sp(S_SOFF)}, {sp(S_HOFF2)}",
+                f"s_addc_u32 {sp(S_SOFF + 1)}, {sp(S_SOFF + 1)}, 0"]
+
     def stage_list(self, s_tile, buf):
-        """Direct HBM -> LDS loads of key tile s_tile (K and V, 64 rows) into
-        ring buffer `buf`, and its valid-key count into s_nv[buf], as an
+        """Direct HBM -> LDS loads of key tile s_tile (K and V, 64 rows, the
+        tile under the staging cursor) into ring buffer `buf`, its valid-key
+        count into s_nv[buf], and the cursor moved to the next tile, as an
         instruction list. A tile at or past the piece end (s_tile >= tb) gets
         a resource with no records: its loads fetch nothing and fill the (then
         unused) buffer with zeros, so the launch needs no branch and every
-        tile step issues the same number of loads."""
+        tile step issues the same number of loads. The cursor walks the key
+        ranges in order (a rare branch moves it to the next non-empty range;
+        past the last one it stays put with no valid keys)."""
         nv = S_NV + buf
-        b, e, f, t = S_RO, S_RO + 1, S_RO + 2, S_RO + 3   # (free outside write_state)
-        ins = [f"s_add_i32 {sp(t)}, {sp(A_T)}, -1",
-               f"s_min_i32 {sp(t)}, {sp(s_tile)}, {sp(t)}",                # a valid tile index
-               f"s_mov_b32 {sp(b)}, {sp(A_B0)}", f"s_mov_b32 {sp(e)}, {sp(A_E0)}", f"s_mov_b32 {sp(f)}, 0",
-               f"s_cmp_ge_i32 {sp(t)}, {sp(A_TB1)}",
-               f"s_cselect_b32 {sp(b)}, {sp(A_B1)}, {sp(b)}",
-               f"s_cselect_b32 {sp(e)}, {sp(A_E1)}, {sp(e)}",
-               f"s_cselect_b32 {sp(f)}, {sp(A_TB1)}, {sp(f)}",
-               f"s_cmp_ge_i32 {sp(t)}, {sp(A_TB2)}",
-               f"s_cselect_b32 {sp(b)}, {sp(A_B2)}, {sp(b)}",
-               f"s_cselect_b32 {sp(e)}, {sp(A_E2)}, {sp(e)}",
-               f"s_cselect_b32 {sp(f)}, {sp(A_TB2)}, {sp(f)}",
-               f"s_sub_i32 {sp(f)}, {sp(t)}, {sp(f)}",
-               f"s_lshl_b32 {sp(f)}, {sp(f)}, 6",
-               f"s_add_i32 {sp(f)}, {sp(b)}, {sp(f)}",                     # key0
-               f"s_sub_i32 {sp(nv)}, {sp(e)}, {sp(f)}",
+        f = S_RO + 2
+        u = self.new_uid()
+        ins = [f"s_sub_i32 {sp(nv)}, {sp(S_SEND)}, {sp(S_SKEY)}",
                f"s_min_i32 {sp(nv)}, {sp(nv)}, 64",
-               # byte offset of the tile's first row in this head: key0 * ld * 2 + hoff * 2
-               f"s_mul_hi_u32 {sp(e)}, {sp(f)}, {sp(A_LD2)}",
-               f"s_mul_i32 {sp(b)}, {sp(f)}, {sp(A_LD2)}",
-               f"s_add_u32 {sp(b)}, {sp(b)}, {sp(S_HOFF2)}",
-               f"s_addc_u32 {sp(e)}, {sp(e)}, 0",
-               f"s_add_u32 {sp(S_RK)}, {sp(A_KPTR)}, {sp(b)}",
-               f"s_addc_u32 {sp(S_RK + 1)}, {sp(A_KPTR + 1)}, {sp(e)}",
-               f"s_add_u32 {sp(S_RV)}, {sp(A_VPTR)}, {sp(b)}",
-               f"s_addc_u32 {sp(S_RV + 1)}, {sp(A_VPTR + 1)}, {sp(e)}",
+               f"s_add_u32 {sp(S_RK)}, {sp(A_KPTR)}, {sp(S_SOFF)}\n"
+               f"  s_addc_u32 {sp(S_RK + 1)}, {sp(A_KPTR + 1)}, {sp(S_SOFF + 1)}",
+               f"s_add_u32 {sp(S_RV)}, {sp(A_VPTR)}, {sp(S_SOFF)}\n"
+               f"  s_addc_u32 {sp(S_RV + 1)}, {sp(A_VPTR + 1)}, {sp(S_SOFF + 1)}",
                # records: the tile's valid rows (rows past them read as zero); none past the piece
-               f"s_sub_i32 {sp(f)}, {sp(nv)}, 1",
-               f"s_mul_i32 {sp(f)}, {sp(f)}, {sp(A_LD2)}",
-               f"s_add_u32 {sp(f)}, {sp(f)}, 0x100",
-               f"s_cmp_lt_i32 {sp(s_tile)}, {sp(S_TB)}",
-               f"s_cselect_b32 {sp(S_RK + 2)}, {sp(f)}, 0",
-               f"s_mov_b32 {sp(S_RV + 2)}, {sp(S_RK + 2)}",
-               f"s_mov_b32 {sp(S_RK + 3)}, 0x20000",
-               f"s_mov_b32 {sp(S_RV + 3)}, 0x20000"]
+               f"s_mul_i32 {sp(f)}, {sp(nv)}, {sp(A_LD2)}",
+               f"s_add_u32 {sp(f)}, {sp(f)}, {sp(S_REC0)}",
+               f"s_cmp_lt_i32 {sp(s_tile)}, {sp(S_TB)}\n"
+               f"  s_cselect_b32 {sp(S_RK + 2)}, {sp(f)}, 0",
+               f"s_mov_b32 {sp(S_RV + 2)}, {sp(S_RK + 2)}"]
+        # each wave loads 16 consecutive rows, 4 per instruction: one M0 per
+        # operand, the instruction offset (applied to both the memory and the
+        # LDS address; the voffsets take it back out) selects the 4 rows
         kb = K_REGION + buf * BUF_BYTES
         vb = V_REGION + buf * BUF_BYTES
-        for q in range(4):
-            ins += [f"s_add_u32 m0, {sp(S_WAVE1K)}, {kb + q * 4096}\n  s_nop 0\n"
-                    f"  buffer_load_dwordx4 {vp(V_STK + q)}, {sp(S_RK, 4)}, 0 offen lds",
-                    f"s_add_u32 m0, {sp(S_WAVE1K)}, {vb + q * 4096}\n  s_nop 0\n"
-                    f"  buffer_load_dwordx4 {vp(V_STV + q)}, {sp(S_RV, 4)}, 0 offen lds"]
+        ins += [f"s_add_u32 m0, {sp(S_WAVE4K)}, {kb}\n  s_nop 0"]
+        ins += [f"buffer_load_dwordx4 {vp(V_STK + q)}, {sp(S_RK, 4)}, 0 offen offset:{1024 * q} lds"
+                for q in range(4)]
+        ins += [f"s_add_u32 m0, {sp(S_WAVE4K)}, {vb}\n  s_nop 0"]
+        ins += [f"buffer_load_dwordx4 {vp(V_STV + q)}, {sp(S_RV, 4)}, 0 offen offset:{1024 * q} lds"
+                for q in range(4)]
+        ins += [f"s_add_u32 {sp(S_SKEY)}, {sp(S_SKEY)}, 64",
+                f"s_add_u32 {sp(S_SOFF)}, {sp(S_SOFF)}, {sp(S_LD128)}\n"
+                f"  s_addc_u32 {sp(S_SOFF + 1)}, {sp(S_SOFF + 1)}, 0",
+                f"s_cmp_ge_i32 {sp(S_SKEY)}, {sp(S_SEND)}\n  s_cbranch_scc1 .Lnr{u}\n.Lnrback{u}:"]
+        self.ool.append([f".Lnr{u}:",
+                         f"s_add_u32 {sp(S_SRNG)}, {sp(S_SRNG)}, 1",
+                         f"s_cmp_eq_u32 {sp(S_SRNG)}, 1",
+                         f"s_cselect_b32 {sp(S_SKEY)}, {sp(A_B1)}, {sp(S_SKEY)}",
+                         f"s_cselect_b32 {sp(S_SEND)}, {sp(A_E1)}, {sp(S_SEND)}",
+                         f"s_cmp_eq_u32 {sp(S_SRNG)}, 2",
+                         f"s_cselect_b32 {sp(S_SKEY)}, {sp(A_B2)}, {sp(S_SKEY)}",
+                         f"s_cselect_b32 {sp(S_SEND)}, {sp(A_E2)}, {sp(S_SEND)}",
+                         f"s_cmp_lt_u32 {sp(S_SRNG)}, 3",
+                         f"s_cselect_b32 {sp(S_SEND)}, {sp(S_SEND)}, {sp(S_SKEY)}",
+                         f"s_cbranch_scc0 .Lnrback{u}",
+                         f"s_cmp_ge_i32 {sp(S_SKEY)}, {sp(S_SEND)}",
+                         f"s_cbranch_scc1 .Lnr{u}"]
+                        + self.cursor_offset()
+                        + [f"s_branch .Lnrback{u}"])
         return ins
 
     def stage(self, s_tile, buf):
@@ -203,17 +249,66 @@ class Gen:
             self.emit(i)
 
     # ---------------------------------------------------------------- softmax
+    @staticmethod
+    def weights(S, nmc, P, dot=None):
+        """Weights p = 2^(s c - m c) of the 16 scores S into the temporaries
+        (exponentials in groups of four, each four instructions after its
+        argument), the bf16 pairs into P, and the fp32 sum of the 16 unrounded
+        weights into the first temporary (by pairs, then a tree)."""
+        T = [V_T + i for i in range(16)]
+        ins = []
+        pend = []
+        for g in range(4):
+            idx = [4 * g + i for i in range(4)]
+            ins += [f"v_fma_f32 {vp(T[i])}, {vp(S[i])}, {sp(A_C)}, {vp(nmc)}" for i in idx]
+            ins += pend[:4]
+            ins += [f"v_exp_f32_e32 {vp(T[i])}, {vp(T[i])}" for i in idx]
+            ins += pend[4:]
+            pend = []
+            for pp in (2 * g, 2 * g + 1):
+                a_, b_ = T[2 * pp], T[2 * pp + 1]
+                pend += [f"v_cvt_pk_bf16_f32 {vp(P[pp])}, {vp(a_)}, {vp(b_)}",
+                         f"v_add_f32_e32 {vp(a_)}, {vp(a_)}, {vp(b_)}"]
+                if dot is not None and pp > 0:
+                    pend += [f"v_dot2c_f32_bf16_e32 {vp(dot)}, {BF16_ONES}, {vp(P[pp - 1])}"]
+        if dot is not None:
+            ins = [f"v_mov_b32_e32 {vp(dot)}, 0"] + ins
+        ins += ["s_nop 0"] + pend
+        if dot is not None:
+            ins += [f"v_dot2c_f32_bf16_e32 {vp(dot)}, {BF16_ONES}, {vp(P[7])}"]
+        ins += [f"v_add_f32_e32 {vp(T[0])}, {vp(T[0])}, {vp(T[2])}",
+                f"v_add_f32_e32 {vp(T[4])}, {vp(T[4])}, {vp(T[6])}",
+                f"v_add_f32_e32 {vp(T[8])}, {vp(T[8])}, {vp(T[10])}",
+                f"v_add_f32_e32 {vp(T[12])}, {vp(T[12])}, {vp(T[14])}",
+                f"v_add_f32_e32 {vp(T[0])}, {vp(T[0])}, {vp(T[4])}",
+                f"v_add_f32_e32 {vp(T[8])}, {vp(T[8])}, {vp(T[12])}",
+                f"v_add_f32_e32 {vp(T[0])}, {vp(T[0])}, {vp(T[8])}"]
+        return ins
+
     def softmax(self, qb, s_base, p_base, nv_reg, half):
         """The online-softmax step of query block qb over one 32-key half
-        whose scores are in v[s_base:+15]; writes the bf16 weights to
-        v[p_base:+7] and updates the block's m / thr / nmc / l / lr (and alpha
-        and the deferred-rescale flag when the reference moves). Returns the
-        instruction list (to be interleaved with matrix instructions)."""
-        m, thr, nmc, l, lr, alpha = (V_ST[qb] + i for i in range(6))
-        flag = S_FLAG[qb]
+        whose scores are in v[s_base:+15]: the bf16 weights into
+        v[p_base:+7] and the fp32 sum of this lane's 16 weights into the first
+        temporary. Returns (body, check): the body is interleaved with matrix
+        instructions, the check (the trigger compare into VCC) ends the phase,
+        and resolve() takes the branch and adds the sum to l.
+
+        The reference m moves lazily: the weights are computed against the
+        current m, and only when some lane's 16 weights sum to more than 2^8
+        (or to inf / NaN: the first half of a piece starts from m = -inf with
+        -m c = +inf) does a rare path raise m to the row maximum, recompute
+        the weights and rescale l, O and the bf16 weight sums by
+        alpha = 2^((m_old - m_new) c). Every weight therefore stays at or
+        below 2^8, as with an explicit maximum test, without the maximum on
+        the common path. The branch is taken after the phase's P V matrix
+        instructions (those still apply weights of the old reference) have
+        been issued; the rare path waits for them before it rescales O."""
+        m, nmc, l, alpha = V_ST[qb], V_ST[qb] + 2, V_ST[qb] + 3, V_ST[qb] + 5
+        lr, dot = V_ST[qb] + 1, (None if SUMS_ON_MFMA else V_ST[qb] + 4)
         u = self.new_uid()
         T = V_T
         S = [s_base + r for r in range(16)]
+        P = [p_base + i for i in range(8)]
         ins = []
         # keys past the end of a range (only in the last tile of each range)
         # (a rare-path branch and the label it returns to stay adjacent: the
@@ -231,8 +326,31 @@ class Gen:
                      f"v_cndmask_b32_e32 {vp(S[r])}, {vp(S[r])}, {vp(T + 1)}, vcc"]
         mask += [f"s_branch .Lmback{u}"]
         self.ool.append(mask)
-        # row max over the 16 scores (a tree of depth three) and the lane pair
-        ins += [f"v_maximum3_f32 {vp(T)}, {vp(S[0])}, {vp(S[1])}, {vp(S[2])}",
+        ins += self.weights(S, nmc, P, dot)
+        # trigger: !(2^8 >= lane sum), true for a sum above 2^8, inf or NaN
+        return ins, [f"v_cmp_nge_f32_e32 vcc, 0x43800000, {vp(T)}"]
+
+    def resolve(self, qb, s_base, p_base):
+        """The branch on a softmax step's trigger (in VCC) and the addition of
+        its weight sums to l: placed after the first matrix instruction of the
+        next phase (so the compare has completed when the branch reads VCC),
+        before anything there overwrites the temporaries or, for block 0, the
+        scores. The rare path (emitted out of line): the row maximum over the
+        16 scores (a tree of depth three) and the lane pair, the new
+        reference, the weights again, and the rescale of l, O and the weight
+        sums."""
+        m, nmc, l, alpha = V_ST[qb], V_ST[qb] + 2, V_ST[qb] + 3, V_ST[qb] + 5
+        lr, dot = V_ST[qb] + 1, (None if SUMS_ON_MFMA else V_ST[qb] + 4)
+        u = self.new_uid()
+        T = V_T
+        S = [s_base + r for r in range(16)]
+        P = [p_base + i for i in range(8)]
+        out = [f"s_cbranch_vccnz .Lresc{u}\n.Lrback{u}:",
+               f"v_add_f32_e32 {vp(l)}, {vp(l)}, {vp(T)}"]
+        if dot is not None:
+            out += [f"v_add_f32_e32 {vp(lr)}, {vp(lr)}, {vp(dot)}"]
+        resc = [f".Lresc{u}:",
+                f"v_maximum3_f32 {vp(T)}, {vp(S[0])}, {vp(S[1])}, {vp(S[2])}",
                 f"v_maximum3_f32 {vp(T + 1)}, {vp(S[3])}, {vp(S[4])}, {vp(S[5])}",
                 f"v_maximum3_f32 {vp(T + 2)}, {vp(S[6])}, {vp(S[7])}, {vp(S[8])}",
                 f"v_maximum3_f32 {vp(T + 3)}, {vp(S[9])}, {vp(S[10])}, {vp(S[11])}",
@@ -244,67 +362,29 @@ class Gen:
                 "s_nop 1",
                 f"v_permlane32_swap_b32 {vp(T)}, {vp(T + 1)}",
                 "s_nop 1",
-                f"v_maximum3_f32 {vp(T)}, {vp(T)}, {vp(T + 1)}, {vp(T + 1)}",
-                f"v_cmp_gt_f32_e32 vcc, {vp(T)}, {vp(thr)}",
-                f"s_cbranch_vccnz .Lresc{u}\n.Lrback{u}:"]
-        # reference update: m = max(m, tmax) for every lane of the wave; the
-        # factor alpha rescales l and lr here and O later (deferred)
-        self.ool.append([f".Lresc{u}:",
-                         f"v_maximum3_f32 {vp(T + 1)}, {vp(m)}, {vp(T)}, {vp(T)}",
-                         f"v_sub_f32_e32 {vp(T + 2)}, {vp(m)}, {vp(T + 1)}",
-                         f"v_mul_f32_e32 {vp(T + 2)}, {sp(A_C)}, {vp(T + 2)}",
-                         f"v_exp_f32_e32 {vp(alpha)}, {vp(T + 2)}",
-                         f"v_mov_b32_e32 {vp(m)}, {vp(T + 1)}",
-                         f"v_add_f32_e32 {vp(thr)}, {sp(A_LAZY)}, {vp(T + 1)}",
-                         f"v_mul_f32_e32 {vp(nmc)}, {sp(A_NEGC)}, {vp(T + 1)}",
-                         "s_nop 0",
-                         f"v_mul_f32_e32 {vp(l)}, {vp(alpha)}, {vp(l)}",
-                         f"s_mov_b32 {sp(flag)}, 1",
-                         f"s_branch .Lrback{u}"])
-        # weights p = 2^(s c - m c) in groups of four (each exponential four
-        # instructions after its argument), then per pair of keys the fp32 sum
-        # and the bf16 pair (the bf16 weights are summed by the matrix cores)
-        P = [p_base + i for i in range(8)]
-        pend = []
-        for g in range(4):
-            idx = [4 * g + i for i in range(4)]
-            ins += [f"v_fma_f32 {vp(S[i])}, {vp(S[i])}, {sp(A_C)}, {vp(nmc)}" for i in idx]
-            ins += pend[:4]
-            ins += [f"v_exp_f32_e32 {vp(S[i])}, {vp(S[i])}" for i in idx]
-            ins += pend[4:]
-            pend = []
-            for pp in (2 * g, 2 * g + 1):
-                a_, b_ = S[2 * pp], S[2 * pp + 1]
-                pend += [f"v_add_f32_e32 {vp(T + 2 + pp)}, {vp(a_)}, {vp(b_)}",
-                         f"v_cvt_pk_bf16_f32 {vp(P[pp])}, {vp(a_)}, {vp(b_)}"]
-
-        ins += ["s_nop 0"] + pend
-        t = [T + 2 + p for p in range(8)]
-        ins += [f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[1])}",
-                f"v_add_f32_e32 {vp(t[2])}, {vp(t[2])}, {vp(t[3])}",
-                f"v_add_f32_e32 {vp(t[4])}, {vp(t[4])}, {vp(t[5])}",
-                f"v_add_f32_e32 {vp(t[6])}, {vp(t[6])}, {vp(t[7])}",
-                f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[2])}",
-                f"v_add_f32_e32 {vp(t[4])}, {vp(t[4])}, {vp(t[6])}",
-                f"v_add_f32_e32 {vp(t[0])}, {vp(t[0])}, {vp(t[4])}",
-                f"v_add_f32_e32 {vp(l)}, {vp(l)}, {vp(t[0])}"]
-        return ins
-
-    def deferred_rescale(self, qb):
-        """O of block qb *= alpha if the block's reference moved (its P V
-        MFMAs issued so far have completed by then)."""
-        flag, alpha = S_FLAG[qb], V_ST[qb] + 5
-        u = self.new_uid()
-        self.emit(f"s_cmp_eq_u32 {sp(flag)}, 0", f"s_cbranch_scc1 .Ldskip{u}", "s_nop 7", "s_nop 7", "s_nop 7")
-        for i in range(64):
-            self.emit(f"v_mul_f32_e32 {vp(V_O[qb] + i)}, {vp(alpha)}, {vp(V_O[qb] + i)}")
-        for i in range(16):
-            t = V_T + (i & 7)
-            self.emit(f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb] + i)}",
-                      f"v_mul_f32_e32 {vp(t)}, {vp(alpha)}, {vp(t)}",
-                      f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(t)}")
-        self.emit(f"s_mov_b32 {sp(flag)}, 0")
-        self.label(f".Ldskip{u}")
+                f"v_maximum3_f32 {vp(T + 1)}, {vp(m)}, {vp(T)}, {vp(T + 1)}",    # m_new
+                f"v_sub_f32_e32 {vp(T + 2)}, {vp(m)}, {vp(T + 1)}",
+                f"v_mul_f32_e32 {vp(T + 2)}, {sp(A_C)}, {vp(T + 2)}",
+                f"v_exp_f32_e32 {vp(alpha)}, {vp(T + 2)}",
+                f"v_mov_b32_e32 {vp(m)}, {vp(T + 1)}",
+                f"v_mul_f32_e32 {vp(nmc)}, {sp(A_NEGC)}, {vp(T + 1)}",
+                "s_nop 0",
+                f"v_mul_f32_e32 {vp(l)}, {vp(alpha)}, {vp(l)}"]
+        resc += self.weights(S, nmc, P, dot)
+        # the P V instructions issued so far (old reference) have completed
+        resc += ["s_nop 7", "s_nop 7", "s_nop 7"]
+        resc += [f"v_mul_f32_e32 {vp(V_O[qb] + i)}, {vp(alpha)}, {vp(V_O[qb] + i)}" for i in range(64)]
+        if SUMS_ON_MFMA:
+            for i in range(16):
+                t = V_T + 8 + (i & 7)
+                resc += [f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb] + i)}",
+                         f"v_mul_f32_e32 {vp(t)}, {vp(alpha)}, {vp(t)}",
+                         f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(t)}"]
+        else:
+            resc += [f"v_mul_f32_e32 {vp(lr)}, {vp(alpha)}, {vp(lr)}"]
+        resc += [f"s_branch .Lrback{u}"]
+        self.ool.append(resc)
+        return out
 
     # ---------------------------------------------------------------- matrix work
     @staticmethod
@@ -314,7 +394,7 @@ class Gen:
         # MFMAs are independent
         out = []
         for kk in range(8):
-            for qb, dst in ((0, y_reg), (1, z_reg)):
+            for qb, dst in ((1, z_reg), (0, y_reg)):
                 c = "0" if kk == 0 else vp(dst, 16)
                 out.append(f"v_mfma_f32_32x32x16_bf16 {vp(dst, 16)}, {ap(A_K + 4 * kk, 4)}, "
                            f"{ap(A_Q[qb] + 4 * kk, 4)}, {c}")
@@ -330,7 +410,7 @@ class Gen:
                     o = vp(V_O[qb] + 16 * db, 16)
                     out.append(f"v_mfma_f32_32x32x16_bf16 {o}, {ap(A_V + 16 * s + 4 * db, 4)}, "
                                f"{vp(p + 4 * s, 4)}, {o}")
-            for s in range(2):
+            for s in range(2 if SUMS_ON_MFMA else 0):
                 acc = ap(A_LR[qb], 16)
                 out.append(f"v_mfma_f32_32x32x16_bf16 {acc}, {ap(A_ONES, 4)}, {vp(p + 4 * s, 4)}, {acc}")
         return out
@@ -351,13 +431,41 @@ class Gen:
                 out.append(f"ds_read_b64_tr_b16 {ap(a + 2, 2)}, {vp(V_VADDR + 4 + db)} offset:{imm}")
         return out
 
-    def phase(self, mfma, lds, valu, lds_start=2):
-        """Interleave 16 (or 0) MFMAs with LDS reads and a VALU list."""
+    @staticmethod
+    def cost(item):
+        """Issue cycles of an instruction-list item for one wave (estimates:
+        a VALU op about 4, a transcendental 8, an LDS or buffer op 4 / 8)."""
+        c = 0
+        for ln in item.split("\n"):
+            t = ln.strip()
+            if not t or t.endswith(":"):
+                continue
+            op = t.split()[0]
+            if op.startswith(("v_exp", "v_log", "v_rcp")):
+                c += 8
+            elif op.startswith("v_"):
+                c += 4
+            elif op.startswith("ds_"):
+                c += 4
+            elif op.startswith("buffer_"):
+                c += 8
+            elif op == "s_nop":
+                c += int(t.split()[1]) + 1
+            else:
+                c += 1
+        return c
+
+    def phase(self, mfma, lds, valu, tail=(), lds_start=2, stage=(), pre=()):
+        """Interleave 16 or 20 (or 0) MFMAs with LDS reads, the staging list
+        and a VALU list, then the tail. The LDS reads go two per matrix
+        instruction from the third one on (the operands they overwrite may
+        still be read by the previous phase's last matrix instructions); the
+        staging and VALU lists are merged in proportion to their issue cost
+        and spread so that every matrix instruction carries about the same
+        issue time, with at most one buffer load after each."""
         self.emit("s_waitcnt lgkmcnt(0)")
         if not mfma:
-            for i in lds:
-                self.emit(i)
-            for i in valu:
+            for i in list(pre) + list(lds) + list(stage) + list(valu) + list(tail):
                 self.emit(i)
             return
         n = len(mfma)
@@ -367,16 +475,44 @@ class Gen:
             per = -(-len(lds) // span)
             for k, i in enumerate(lds):
                 lds_slots[lds_start + k // per].append(i)
-        per_v = -(-len(valu) // n)
-        vi = 0
-        for s in range(n):
-            self.emit(mfma[s])
-            for i in lds_slots[s]:
+        if not BALANCED:
+            valu = list(stage) + list(valu)
+            per_v = -(-len(valu) // n)
+            for s_ in range(n):
+                self.emit(mfma[s_], *(pre if s_ == 0 else ()), *lds_slots[s_], *valu[s_ * per_v:(s_ + 1) * per_v])
+            for i in list(valu[n * per_v:]) + list(tail):
                 self.emit(i)
-            for i in valu[vi:vi + per_v]:
+            return
+        # merge the staging and VALU lists by cost (their orders are kept)
+        cs, cv = sum(map(self.cost, stage)), sum(map(self.cost, valu))
+        merged, a, b, da, db = [], 0, 0, 0, 0
+        while a < len(stage) or b < len(valu):
+            if b >= len(valu) or (a < len(stage) and da * max(cv, 1) <= db * max(cs, 1)):
+                merged.append(stage[a]); da += self.cost(stage[a]); a += 1
+            else:
+                merged.append(valu[b]); db += self.cost(valu[b]); b += 1
+        total = sum(map(self.cost, merged)) + sum(self.cost(i) for sl in lds_slots for i in sl)
+        k, done, cum_lds = 0, 0, 0
+        for s_ in range(n):
+            self.emit(mfma[s_])
+            if s_ == 0:
+                for i in pre:
+                    self.emit(i)
+            for i in lds_slots[s_]:
                 self.emit(i)
-            vi += per_v
-        for i in valu[vi:]:
+                cum_lds += self.cost(i)
+            target = total * (s_ + 1) / n - cum_lds
+            vm = 0
+            while k < len(merged) and (done < target or s_ == n - 1):
+                it = merged[k]
+                if "buffer_load" in it:
+                    if vm:
+                        break
+                    vm = 1
+                self.emit(it)
+                done += self.cost(it)
+                k += 1
+        for i in list(merged[k:]) + list(tail):
             self.emit(i)
 
     # ---------------------------------------------------------------- output
@@ -435,8 +571,15 @@ class Gen:
                   f"v_mov_b32_e32 {vp(V_Y)}, 0x40000000")                   # an offset past every record (the scores are dead here)
         for qb in range(2):
             m, l = V_ST[qb], V_ST[qb] + 3
+            if SUMS_ON_MFMA:
+                self.emit(f"v_accvgpr_read_b32 {vp(T + 4)}, {ap(A_LR[qb])}")      # lr total
+            else:
+                self.emit(f"v_mov_b32_e32 {vp(T + 4)}, {vp(V_ST[qb] + 1)}", f"v_mov_b32_e32 {vp(T + 5)}, {vp(V_ST[qb] + 1)}",
+                          "s_nop 1",
+                          f"v_permlane32_swap_b32 {vp(T + 4)}, {vp(T + 5)}",
+                          "s_nop 1",
+                          f"v_add_f32_e32 {vp(T + 4)}, {vp(T + 4)}, {vp(T + 5)}")  # lr total
             self.emit(f"v_mov_b32_e32 {vp(T + 2)}, {vp(l)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(l)}",
-                      f"v_accvgpr_read_b32 {vp(T + 4)}, {ap(A_LR[qb])}",          # lr total
                       "s_nop 1",
                       f"v_permlane32_swap_b32 {vp(T + 2)}, {vp(T + 3)}",
                       "s_nop 1",
@@ -468,7 +611,8 @@ class Gen:
     # ---------------------------------------------------------------- tile loop
     def prologue(self, b):
         """Restart of the compute pipeline at tile t (ring buffer b): the K
-        operands of its first half are in registers."""
+        operands of its first half are in registers. Its block-0 softmax step
+        is resolved by the first phase of the tile body."""
         self.label(f".Lpro{b}")
         self.emit("s_waitcnt lgkmcnt(0)")
         for i in self.mfma_scores(V_Y, V_Z[0]):
@@ -477,43 +621,44 @@ class Gen:
         for i in self.lds_k(b, 1):
             self.emit(i)
         self.emit("s_nop 7", "s_nop 7", "s_nop 7")
-        for i in self.softmax(0, V_Y, V_P0[0], S_NV + b, 0):
+        body, check = self.softmax(0, V_Y, V_P0[0], S_NV + b, 0)
+        for i in body + check:
             self.emit(i)
-        self.deferred_rescale(0)
         self.emit(f"s_branch .Ltile{b}")
 
     def tile_body(self, B):
+        """Tile t in ring buffer B. Each softmax step's trigger is resolved
+        after the first matrix instruction of the following phase."""
         nb = (B + 1) & 3
         self.label(f".Ltile{B}")
         self.emit(f"s_sub_i32 {sp(S_BUDGET)}, {sp(S_BUDGET)}, 1",
                   f"s_cmp_lt_i32 {sp(S_BUDGET)}, 0",
                   "s_cbranch_scc1 .Lend")
         # A(2t): scores of half 2t+1 | softmax of half 2t, block 1 | V of half 2t
-        self.phase(self.mfma_scores(V_Y, V_Z[1]), self.lds_v(B, 0),
-                   self.softmax(1, V_Z[0], V_P1, S_NV + B, 0))
-        self.deferred_rescale(1)
+        # (resolves block 0's step of half 2t, from the prologue or B(2t-1))
+        body, check = self.softmax(1, V_Z[0], V_P1, S_NV + B, 0)
+        self.phase(self.mfma_scores(V_Y, V_Z[1]), self.lds_v(B, 0), body, check,
+                   pre=self.resolve(0, V_Y, V_P0[0]))
         # barrier: tile t+1 resident everywhere; tile t-1's buffer is free
-        u = self.new_uid()
         # (every tile step issues the loads of one tile, so the loads of tile
         # t+2 are the only ones that may still be in flight)
         self.emit("s_waitcnt vmcnt(8)", "s_barrier", f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 3")
-        del u
         # B(2t): P V of half 2t | softmax of half 2t+1, block 0 | K of half 2t+2,
         # with the loads of tile t+3 into the buffer tile t-1 has left
-        self.phase(self.mfma_pv(V_P0[0]), self.lds_k(nb, 0),
-                   self.stage_list(S_X, (B + 3) & 3) + self.softmax(0, V_Y, V_P0[1], S_NV + B, 1))
-        self.deferred_rescale(0)
+        body, check = self.softmax(0, V_Y, V_P0[1], S_NV + B, 1)
+        self.phase(self.mfma_pv(V_P0[0]), self.lds_k(nb, 0), body, check,
+                   stage=self.stage_list(S_X, (B + 3) & 3), pre=self.resolve(1, V_Z[0], V_P1))
         self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 1",
                   f"s_cmp_eq_u32 {sp(S_X)}, {sp(S_FL)}",
                   f"s_cbranch_scc1 .Ltail{B}")
         # A(2t+1): scores of half 2t+2 | softmax of half 2t+1, block 1 | V of half 2t+1
-        self.phase(self.mfma_scores(V_Y, V_Z[0]), self.lds_v(B, 1),
-                   self.softmax(1, V_Z[1], V_P1, S_NV + B, 1))
-        self.deferred_rescale(1)
+        body, check = self.softmax(1, V_Z[1], V_P1, S_NV + B, 1)
+        self.phase(self.mfma_scores(V_Y, V_Z[0]), self.lds_v(B, 1), body, check,
+                   pre=self.resolve(0, V_Y, V_P0[1]))
         # B(2t+1): P V of half 2t+1 | softmax of half 2t+2, block 0 | K of half 2t+3
-        self.phase(self.mfma_pv(V_P0[1]), self.lds_k(nb, 1),
-                   self.softmax(0, V_Y, V_P0[0], S_NV + nb, 0))
-        self.deferred_rescale(0)
+        body, check = self.softmax(0, V_Y, V_P0[0], S_NV + nb, 0)
+        self.phase(self.mfma_pv(V_P0[1]), self.lds_k(nb, 1), body, check,
+                   pre=self.resolve(1, V_Z[1], V_P1))
         self.emit(f"s_add_u32 {sp(S_T)}, {sp(S_T)}, 1")
         if B == 3:
             self.emit(".Ltile_wrap:", "s_branch .Ltile0")
@@ -523,8 +668,9 @@ class Gen:
         half, no softmax of the next half."""
         nb = (B + 1) & 3
         self.label(f".Ltail{B}")
-        self.phase([], self.lds_v(B, 1), self.softmax(1, V_Z[1], V_P1, S_NV + B, 1))
-        self.deferred_rescale(1)
+        body, check = self.softmax(1, V_Z[1], V_P1, S_NV + B, 1)
+        self.phase([], self.lds_v(B, 1), body, check + self.resolve(1, V_Z[1], V_P1),
+                   pre=self.resolve(0, V_Y, V_P0[1]))
         self.phase(self.mfma_pv(V_P0[1]), [], [])
         self.emit(f"s_add_u32 {sp(S_T)}, {sp(S_T)}, 1",
                   f"s_cmp_eq_u32 {sp(S_T)}, {sp(S_TB)}",
@@ -579,24 +725,25 @@ class Gen:
                           f"v_lshl_add_u32 {vp(r)}, {vp(T + 10)}, 8, {vp(T + 11)}",
                           f"v_add_u32_e32 {vp(r)}, {vp(r)}, {vp(T + 6)}",
                           f"v_add_u32_e32 {vp(r)}, 0x{V_REGION:x}, {vp(r)}")
-        # staging voffsets of thread tid: row = tid >> 4, stored chunk st = tid & 15;
-        # K: chunk st ^ row, V: st ^ (4 (row & 3) ^ 2 ((row >> 2) & 1)); load q adds 16 q rows
-        self.emit(f"v_lshrrev_b32_e32 {vp(T)}, 4, {vp(V_TID)}",          # row
-                  f"v_and_b32_e32 {vp(T + 1)}, 15, {vp(V_TID)}",         # st
-                  f"v_xor_b32_e32 {vp(T + 2)}, {vp(T + 1)}, {vp(T)}",
-                  f"v_lshlrev_b32_e32 {vp(T + 2)}, 4, {vp(T + 2)}",      # K chunk bytes
-                  f"v_and_b32_e32 {vp(T + 3)}, 3, {vp(T)}",
-                  f"v_lshlrev_b32_e32 {vp(T + 3)}, 2, {vp(T + 3)}",
-                  f"v_bfe_u32 {vp(T + 4)}, {vp(T)}, 2, 1",
-                  f"v_lshlrev_b32_e32 {vp(T + 4)}, 1, {vp(T + 4)}",
-                  f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 4)}",
-                  f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 1)}",
-                  f"v_lshlrev_b32_e32 {vp(T + 3)}, 4, {vp(T + 3)}")      # V chunk bytes
+        # staging voffsets of lane l of wave w, load q: row = 16 w + 4 q + (l >> 4),
+        # stored chunk st = l & 15; K: chunk st ^ (row & 15) = st ^ (4 q + (l >> 4)),
+        # V: st ^ (4 (row & 3) ^ 2 ((row >> 2) & 1)) = st ^ (4 (l >> 4) ^ 2 (q & 1));
+        # less the load's instruction offset 1024 q
+        self.emit(f"v_lshrrev_b32_e32 {vp(T)}, 4, {vp(V_LANE)}",         # l >> 4
+                  f"v_and_b32_e32 {vp(T + 1)}, 15, {vp(V_LANE)}",        # st
+                  f"s_lshl_b32 {sp(S_X)}, {sp(S_WAVE)}, 4",
+                  f"v_add_u32_e32 {vp(T + 4)}, {sp(S_X)}, {vp(T)}",      # 16 w + (l >> 4)
+                  f"v_lshlrev_b32_e32 {vp(T + 5)}, 2, {vp(T)}")          # 4 (l >> 4)
         for q in range(4):
-            self.emit(f"v_add_u32_e32 {vp(T + 5)}, {16 * q}, {vp(T)}",
-                      f"v_mul_lo_u32 {vp(T + 5)}, {vp(T + 5)}, {sp(A_LD2)}",
-                      f"v_add_u32_e32 {vp(V_STK + q)}, {vp(T + 5)}, {vp(T + 2)}",
-                      f"v_add_u32_e32 {vp(V_STV + q)}, {vp(T + 5)}, {vp(T + 3)}")
+            self.emit(f"v_add_u32_e32 {vp(T + 6)}, {4 * q}, {vp(T + 4)}",          # row
+                      f"v_mul_lo_u32 {vp(T + 6)}, {vp(T + 6)}, {sp(A_LD2)}",
+                      f"v_subrev_u32_e32 {vp(T + 6)}, {1024 * q}, {vp(T + 6)}",    # row bytes - 1024 q
+                      f"v_add_u32_e32 {vp(T + 2)}, {4 * q}, {vp(T)}",
+                      f"v_xor_b32_e32 {vp(T + 2)}, {vp(T + 2)}, {vp(T + 1)}",
+                      f"v_lshl_add_u32 {vp(V_STK + q)}, {vp(T + 2)}, 4, {vp(T + 6)}",
+                      f"v_xor_b32_e32 {vp(T + 3)}, {2 * (q & 1)}, {vp(T + 5)}",
+                      f"v_xor_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 1)}",
+                      f"v_lshl_add_u32 {vp(V_STV + q)}, {vp(T + 3)}, 4, {vp(T + 6)}")
         # Q load voffsets: row (32 qb + ql), bytes 16 hh within the head's slice
         self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
                   f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
@@ -641,6 +788,7 @@ class Gen:
         # every wave is done with the previous piece's LDS tiles
         self.emit("s_barrier")
         self.emit(f"s_mov_b32 {sp(S_T)}, {sp(S_TA)}")
+        self.stage_init(S_T)
         self.stage(S_T, 0)
         # Q resource: rows of this wave that exist; the head's 256 bytes of each
         self.mul64(S_X, S_Y, S_QROWB, A_LD2)
@@ -659,19 +807,19 @@ class Gen:
         self.stage(S_X, 1)
         self.emit(f"s_add_u32 {sp(S_X)}, {sp(S_T)}, 2")
         self.stage(S_X, 2)
-        # fresh softmax state and O
+        # fresh softmax state and O: m = -inf, -m c = +inf, so the first
+        # weights are inf (or NaN) and the first half sets the reference
         for qb in range(2):
-            m, thr, nmc, l, lr, alpha = (V_ST[qb] + i for i in range(6))
-            self.emit(f"v_mov_b32_e32 {vp(m)}, 0xff800000", f"v_mov_b32_e32 {vp(thr)}, 0xff800000",
-                      f"v_mov_b32_e32 {vp(nmc)}, 0", f"v_mov_b32_e32 {vp(l)}, 0", f"v_mov_b32_e32 {vp(lr)}, 0",
-                      f"v_mov_b32_e32 {vp(alpha)}, 1.0")
+            m, nmc, l, alpha = V_ST[qb], V_ST[qb] + 2, V_ST[qb] + 3, V_ST[qb] + 5
+            self.emit(f"v_mov_b32_e32 {vp(m)}, 0xff800000", f"v_mov_b32_e32 {vp(nmc)}, 0x7f800000",
+                      f"v_mov_b32_e32 {vp(l)}, 0", f"v_mov_b32_e32 {vp(alpha)}, 1.0",
+                      f"v_mov_b32_e32 {vp(V_ST[qb] + 1)}, 0")
             for i in range(64):
                 self.emit(f"v_mov_b32_e32 {vp(V_O[qb] + i)}, 0")
         self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0")
-        for qb in range(2):
+        for qb in range(2 if SUMS_ON_MFMA else 0):
             for i in range(16):
                 self.emit(f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(V_T)}")
-        self.emit(f"s_mov_b32 {sp(S_FLAG[0])}, 0", f"s_mov_b32 {sp(S_FLAG[1])}, 0")
         # wait for tile ta and Q (the loads of tiles ta+1, ta+2 may stay in flight)
         self.emit("s_waitcnt vmcnt(16)", "s_barrier")
         for i in self.lds_k(0, 0):
@@ -710,7 +858,13 @@ class Gen:
                   "s_nop 1",
                   f"v_readfirstlane_b32 {sp(S_WAVE)}, {vp(V_T)}",
                   "s_waitcnt lgkmcnt(0)",
-                  f"s_lshl_b32 {sp(S_WAVE1K)}, {sp(S_WAVE)}, 10",
+                  f"s_lshl_b32 {sp(S_WAVE4K)}, {sp(S_WAVE)}, 12",
+                  # staging constants: records = nv * 2 ld + 256 - 2 ld, 64 rows = 128 ld bytes,
+                  # the resources' format words
+                  f"s_sub_i32 {sp(S_REC0)}, 0x100, {sp(A_LD2)}",
+                  f"s_lshl_b32 {sp(S_LD128)}, {sp(A_LD2)}, 6",
+                  f"s_mov_b32 {sp(S_RK + 3)}, 0x20000",
+                  f"s_mov_b32 {sp(S_RV + 3)}, 0x20000",
                   # XCD-aware workgroup index
                   f"s_and_b32 {sp(S_X)}, s2, 7",
                   f"s_mul_i32 {sp(S_X)}, {sp(S_X)}, {sp(A_PERXCD)}",
@@ -736,7 +890,7 @@ class Gen:
                   f"s_mov_b32 {sp(S_SLOT)}, 0")
         self.lane_constants()
         self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0x3f803f80")
-        for i in range(4):
+        for i in range(4 if SUMS_ON_MFMA else 0):
             self.emit(f"v_accvgpr_write_b32 {ap(A_ONES + i)}, {vp(V_T)}")
         self.piece_start()
         for b in range(4):
