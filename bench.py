@@ -62,12 +62,12 @@ PEAK_HBM_GBS = 8000.0
 
 # HBM bytes of one dual-stream attention call (the attention kernel plus the
 # merge of its split work items), from rocprofv3 FETCH_SIZE and WRITE_SIZE
-# scaled by the plain-copy calibration (profiles/attn_chunk_wan13b_dual.md,
+# scaled by the plain-copy calibration (profiles/attn_fast_wan13b_dual.md,
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "60624b284a1a0c75", "bytes_per_launch": 767.3e6},
-    "14b": {"attn_chunk_sha256_16": "60624b284a1a0c75", "bytes_per_launch": 3059.8e6},
+    "1.3b": {"attn_chunk_sha256_16": "36c703f9f2649746", "bytes_per_launch": 755.8e6},
+    "14b": {"attn_chunk_sha256_16": "36c703f9f2649746", "bytes_per_launch": 3059.8e6},
 }
 
 
@@ -189,43 +189,83 @@ def gpu_run(w, steps, warmup, only="all", extras=True):
         avg["absorb"] = absorb_run(ispa, w, chunks[0][1], chunks[0][2], dw, dev)
         avg["solve_all_layers"] = solve_all_run(ispa, w, stats, dev)
         avg["dual_overhead"] = dual_overhead_run(ispa, w, chunks[0], dev)
+        avg["attn_zero_inputs"] = zero_inputs_run(ispa, w, dev)
     return ms_step, avg
+
+
+def zero_inputs_run(ispa, w, dev, reps=5):
+    """Diagnostic beside the step (not part of it): the same dual-stream call
+    on all-zero Q, K and V. The instruction stream, the tiles visited and the
+    memory traffic are those of the real call; only the operand bits do not
+    toggle. With random bf16 operands the matrix cores' power holds the chip
+    below its peak clock (GRBM_GUI_ACTIVE gives about 1.75 GHz against about
+    2.4 GHz for zero operands at the 14B shape), so the ratio of the two rates
+    separates the power limit from the kernel's own schedule."""
+    H, D = w["heads"], w["heads"] * w["head_dim"]
+    N = w["cache_len"]
+    q = torch.zeros((w["n_q"], D), dtype=torch.bfloat16, device=dev)
+    kv = torch.zeros((N, D), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((w["n_q"], D), dtype=torch.float32, device=dev)
+    out_l = torch.empty_like(out)
+    lse = torch.empty((H, w["n_q"]), dtype=torch.float32, device=dev)
+    lse_l = torch.empty_like(lse)
+    call = lambda: ispa.attn_chunk(q, kv, kv, N, w["window"], H, sink_len=w["sink"], dual=True,
+                                   out=out, lse=lse, out_local=out_l, lse_local=lse_l)
+    for _ in range(6):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del q, kv
+    fl = flops(w)["attn_dual"]
+    return {"attn_dual_ms": round(ms, 4), "attn_dual_tflops": round(fl / ms / 1e9, 1),
+            "frac": round(fl / ms / 1e9 / PEAK_BF16_TFLOPS, 4),
+            "what": "diagnostic: the dual call on all-zero inputs (same instructions and traffic, no operand "
+                    "toggling, so the clock is not power-limited); mean of %d back-to-back calls" % reps}
 
 
 def dual_overhead_run(ispa, w, qkv, dev, reps=20):
     """The dual-stream call (full and local results from one pass) against a
     single-stream call over the same full cache (an F-Layer), on the same
-    inputs: medians of `reps` HIP-event timings each. Sec. 3.4 states that the
-    LSE fusion costs under 1 % of execution time."""
+    inputs. The two calls alternate back to back on the stream (no host
+    synchronisation between them, so both see the same clock and power
+    state); each is bracketed by HIP events and the medians of `reps`
+    timings are compared. Sec. 3.4 states that the LSE fusion costs under 1 %
+    of execution time."""
     q, k, v = qkv
     H = w["heads"]
     N = w["cache_len"]
-
-    def timed(fn):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        ms = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            torch.cuda.synchronize()
-            ms.append(e0.elapsed_time(e1))
-        return sorted(ms)[len(ms) // 2]
-
     out = torch.empty((w["n_q"], H * w["head_dim"]), dtype=torch.float32, device=dev)
     out_l = torch.empty_like(out)
     lse = torch.empty((H, w["n_q"]), dtype=torch.float32, device=dev)
     lse_l = torch.empty_like(lse)
-    t_dual = timed(lambda: ispa.attn_chunk(q, k, v, N, w["window"], H, sink_len=w["sink"], dual=True,
-                                           out=out, lse=lse, out_local=out_l, lse_local=lse_l))
-    t_full = timed(lambda: ispa.attn_chunk(q, k, v, N, N, H, out=out, lse=lse))
+    dual = lambda: ispa.attn_chunk(q, k, v, N, w["window"], H, sink_len=w["sink"], dual=True,
+                                   out=out, lse=lse, out_local=out_l, lse_local=lse_l)
+    full = lambda: ispa.attn_chunk(q, k, v, N, N, H, out=out, lse=lse)
+    for _ in range(3):
+        dual()
+        full()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for e in ev:
+        e[0].record()
+        dual()
+        e[1].record()
+        e[2].record()
+        full()
+        e[3].record()
+    torch.cuda.synchronize()
+    t_dual = sorted(e[0].elapsed_time(e[1]) for e in ev)[reps // 2]
+    t_full = sorted(e[2].elapsed_time(e[3]) for e in ev)[reps // 2]
     return {"dual_ms": round(t_dual, 4), "full_single_ms": round(t_full, 4),
             "overhead": round(t_dual / t_full - 1.0, 4),
             "what": "dual-stream call (full + local outputs) / single-stream full-cache call - 1, same inputs, "
-                    "median of %d HIP-event timings each" % reps}
+                    "the two calls alternating back to back, median of %d HIP-event timings each" % reps}
 
 
 def absorb_run(ispa, w, k, v, dw, dev, reps=10):
@@ -655,6 +695,7 @@ def main():
             "solve_all_layers": avg.get("solve_all_layers"),
         },
         "dual_overhead": avg.get("dual_overhead"),
+        "attn_zero_inputs": avg.get("attn_zero_inputs"),
     }
     if args.only != "all":
         rec["only"] = args.only
@@ -702,6 +743,7 @@ def breakdown_14b(w, ms_step, avg, steps):
         "solve_all_layers": sa,
         "absorb": avg.get("absorb"),
         "dual_overhead": avg.get("dual_overhead"),
+        "attn_zero_inputs": avg.get("attn_zero_inputs"),
         "per": "attention and accum_stats (discrepancy + Gram): ms per chunk call (4 per step); solve: ms per "
                "layer; fractions against 2500 TFLOP/s bf16 and 157.3 TFLOP/s fp32",
         "flop": f,
