@@ -40,6 +40,7 @@ namespace ispa {
 namespace {
 
 constexpr int kNb = 64;
+constexpr int kSup = 4;  // panels per super-panel of the deferred trailing update
 constexpr int kThreads = 256;
 constexpr int kLd = 65;  // LDS row stride (floats) of a 64 x 64 tile
 
@@ -330,19 +331,30 @@ __global__ void solve_init_kernel(const float* G, float* L, int n, float lambda,
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
-// Trailing update of launch k for a 2 x 2 group of 64-blocks with top-left block
-// (R, T), R >= T >= k + 2: A_rt -= L_rk L_tk^T, block (R + w / 2, T + w % 2) on
-// wave w (blocks past the matrix or above the diagonal are skipped). The four
-// waves share L_rk (rows of blocks R, R + 1) and L_tk staged in LDS; each
-// wave's C block is loaded into registers at the start and stored at the end.
-// The k order per accumulator is that of a single-block update.
-__device__ void trailing_2x2(float* L, int n, int nblk, int k, int R, int T, Tile* tiles) {
+// Trailing update by the panels p0 .. p0 + NP - 1 of a 2 x 2 group of 64-blocks
+// with top-left block (R, T), R >= T: A_rt -= L_rp L_tp^T for p in order, block
+// (R + w / 2, T + w % 2) on wave w (blocks past the matrix, above the diagonal
+// or in a column >= t_end are skipped). The four waves share L_rp (rows of
+// blocks R, R + 1) and L_tp staged in LDS, one panel at a time, the next
+// panel's tiles loaded into registers during this one's MFMAs; each wave's C
+// block stays in registers from the first panel to the last. Each panel's
+// product is subtracted on its own, in panel order, so the result is bit for
+// bit that of one launch per panel.
+template <int NP>
+__device__ void trailing_2x2(float* L, int n, int nblk, int p0, int R, int T, int t_end, Tile* tiles) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, h = lane >> 5;
   float (*Ub)[kLd] = tiles[0];  // [128][kLd]: rows of blocks R, R + 1 (two consecutive tiles)
   float (*Vb)[kLd] = tiles[2];  // [128][kLd]: rows of blocks T, T + 1
   const int br = R + (wave >> 1), bc = T + (wave & 1);
-  const bool mine = br < nblk && bc <= br;
+  const bool mine = br < nblk && bc <= br && bc < t_end;
+  const int rows_r0 = min(kNb, n - R * kNb), rows_r1 = min(kNb, n - (R + 1) * kNb);
+  const int rows_t0 = min(kNb, n - T * kNb), rows_t1 = min(kNb, n - (T + 1) * kNb);
+  Frag f0, f1, f2, f3;
+  fetch(f0, L + (int64_t)R * kNb * n + p0 * kNb, n, rows_r0, kNb);
+  fetch(f1, L + (int64_t)(R + 1) * kNb * n + p0 * kNb, n, rows_r1, kNb);
+  fetch(f2, L + (int64_t)T * kNb * n + p0 * kNb, n, rows_t0, kNb);
+  fetch(f3, L + (int64_t)(T + 1) * kNb * n + p0 * kNb, n, rows_t1, kNb);
   float c[2][2][16];
   if (mine) {
 #pragma unroll
@@ -355,33 +367,45 @@ __device__ void trailing_2x2(float* L, int n, int nblk, int k, int R, int T, Til
           c[i][j][r] = row < n && col < n ? L[(int64_t)row * n + col] : 0.f;
         }
   }
-  {
-    Frag f0, f1, f2, f3;
-    fetch(f0, L + (int64_t)R * kNb * n + k * kNb, n, min(kNb, n - R * kNb), kNb);
-    fetch(f1, L + (int64_t)(R + 1) * kNb * n + k * kNb, n, min(kNb, n - (R + 1) * kNb), kNb);
-    fetch(f2, L + (int64_t)T * kNb * n + k * kNb, n, min(kNb, n - T * kNb), kNb);
-    fetch(f3, L + (int64_t)(T + 1) * kNb * n + k * kNb, n, min(kNb, n - (T + 1) * kNb), kNb);
+  const int qr = (wave >> 1) * kNb, qc = (wave & 1) * kNb;
+#pragma unroll
+  for (int pi = 0; pi < NP; ++pi) {
+    const int p = p0 + pi;
+    if (pi > 0) __syncthreads();  // every wave is done with the previous panel's tiles
     put(tiles[0], f0);
     put(tiles[1], f1);
     put(tiles[2], f2);
     put(tiles[3], f3);
+    __syncthreads();
+    if (pi + 1 < NP) {
+      fetch(f0, L + (int64_t)R * kNb * n + (p + 1) * kNb, n, rows_r0, kNb);
+      fetch(f1, L + (int64_t)(R + 1) * kNb * n + (p + 1) * kNb, n, rows_r1, kNb);
+      fetch(f2, L + (int64_t)T * kNb * n + (p + 1) * kNb, n, rows_t0, kNb);
+      fetch(f3, L + (int64_t)(T + 1) * kNb * n + (p + 1) * kNb, n, rows_t1, kNb);
+    }
+    if (mine) {
+      f32x16 acc[2][2] = {};
+#pragma unroll
+      for (int kk = 0; kk < kNb; kk += 2) {
+        float a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = Ub[qr + 32 * i + l32][kk + h];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = Vb[qc + 32 * j + l32][kk + h];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma_f32(a[i], b[j], acc[i][j]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) c[i][j][r] -= acc[i][j][r];
+    }
   }
-  __syncthreads();
   if (!mine) return;
-  const int qr = (wave >> 1) * kNb, qc = (wave & 1) * kNb;
-  f32x16 acc[2][2] = {};
-#pragma unroll
-  for (int kk = 0; kk < kNb; kk += 2) {
-    float a[2], b[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) a[i] = Ub[qr + 32 * i + l32][kk + h];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) b[j] = Vb[qc + 32 * j + l32][kk + h];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = mfma_f32(a[i], b[j], acc[i][j]);
-  }
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -389,15 +413,29 @@ __device__ void trailing_2x2(float* L, int n, int nblk, int k, int R, int T, Til
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = br * kNb + 32 * i + acc_row(r, lane), col = bc * kNb + 32 * j + l32;
-        if (row < n && col < n) L[(int64_t)row * n + col] = c[i][j][r] - acc[i][j][r];
+        if (row < n && col < n) L[(int64_t)row * n + col] = c[i][j][r];
       }
 }
 
+// The deferred update of a super-panel of kSup panels (p0 .. p0 + kSup - 1): the
+// trailing triangle from block e on (rows r >= t >= e) in 2 x 2 groups.
+__global__ __launch_bounds__(kThreads) void chol_trail_kernel(float* L, int n, int p0, int e, int64_t ws) {
+  __shared__ __attribute__((aligned(16))) Tile tiles[4];
+  L = at_layer(L, ws, blockIdx.y);
+  const int nblk = (n + kNb - 1) / kNb;
+  int ti, tj;
+  tri_index((int)blockIdx.x, ti, tj);
+  trailing_2x2<kSup>(L, n, nblk, p0, e + 2 * ti, e + 2 * tj, nblk, tiles);
+}
+
 // Cholesky launch k (k = -1 .. nblk - 2): workgroups 0 .. m - 1 own the next
-// panel column, blocks (k + 1 + i, k + 1); the others the trailing triangle from
-// block k + 2 in 2 x 2 groups of blocks (the first launch has no trailing part).
-__global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int* status,
-                                                            int64_t ws) {
+// panel column, blocks (k + 1 + i, k + 1), and (when `apply`) first subtract
+// panel k from it; the others apply panel k to the trailing columns k + 2 ..
+// t_end - 1 (all rows below) in 2 x 2 groups of blocks, group column by group
+// column. Columns from t_end on receive panel k later, with the rest of its
+// super-panel (chol_trail_kernel).
+__global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int t_end,
+                                                            int apply, int* status, int64_t ws) {
   __shared__ __attribute__((aligned(16))) Tile tiles[6];
   __shared__ int bad;
   L = at_layer(L, ws, blockIdx.y);
@@ -406,11 +444,17 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   const int nblk = (n + kNb - 1) / kNb;
   const int m = nblk - 1 - k;
   if ((int)blockIdx.x >= m) {
-    int ti, tj;
-    tri_index((int)blockIdx.x - m, ti, tj);
-    trailing_2x2(L, n, nblk, k, k + 2 + 2 * ti, k + 2 + 2 * tj, tiles);
+    const int rows = (nblk - k - 2 + 1) / 2;  // group rows of the trailing part
+    int idx = (int)blockIdx.x - m, gj = 0;
+    while (gj < rows && idx >= rows - gj) {
+      idx -= rows - gj;
+      ++gj;
+    }
+    if (gj >= rows) return;
+    trailing_2x2<1>(L, n, nblk, k, k + 2 + 2 * (gj + idx), k + 2 + 2 * gj, t_end, tiles);
     return;
   }
+  apply = apply && k >= 0;
   Tile &S = tiles[0], &M = tiles[1], &T = tiles[2], &U = tiles[3], &V = tiles[4], &P = tiles[5];
   const int r = k + 1 + (int)blockIdx.x, t = k + 1;  // block coordinates
   const int rr = min(kNb, n - r * kNb);
@@ -423,25 +467,25 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   const bool off = r != d;
   Frag fs, fv, ft, fu;
   fetch(fs, L + (int64_t)d * kNb * n + d * kNb, n, nd, nd);
-  if (k >= 0) fetch(fv, L + (int64_t)d * kNb * n + k * kNb, n, nd, kNb);
+  if (apply) fetch(fv, L + (int64_t)d * kNb * n + k * kNb, n, nd, kNb);
   if (off) {
     fetch(ft, Lrt, n, rr, nd);
-    if (k >= 0) fetch(fu, L + (int64_t)r * kNb * n + k * kNb, n, rr, kNb);
+    if (apply) fetch(fu, L + (int64_t)r * kNb * n + k * kNb, n, rr, kNb);
   }
   put(S, fs);
-  if (k >= 0) put(V, fv);
+  if (apply) put(V, fv);
   if (off) {
     put(P, ft);
-    if (k >= 0) put(U, fu);
+    if (apply) put(U, fu);
   }
   __syncthreads();
-  if (k >= 0) {
+  if (apply) {
     quad_store(S, quad<false, true>(V, V), -1.f, true);
     __syncthreads();
   }
   // factor the diagonal block; an off-diagonal workgroup's other waves form
   // A_rd - L_rk L_dk^T meanwhile
-  factor64(S, M, T, nd, &bad, off && k >= 0 ? &P : nullptr, &U, &V);
+  factor64(S, M, T, nd, &bad, off && apply ? &P : nullptr, &U, &V);
   if (!off) {
     store_tile(M, Dinv + (int64_t)d * kNb * kNb, kNb, kNb, kNb);
     if (threadIdx.x == 0 && bad) atomicOr(status, 1);
@@ -1043,11 +1087,39 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     if (grid > 8192) grid = 8192;
     hipLaunchKernelGGL(solve_init_kernel, dim3(grid, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
   }
+  // With several layers, panels are grouped kSup at a time: launch k applies
+  // panel k only to the columns of its own super-panel; the rest of the
+  // trailing triangle receives the super-panel's panels together, in one
+  // launch that keeps each block in registers across them, once its last
+  // panel is factored (a quarter of the trailing-matrix traffic of applying
+  // each panel everywhere; the same arithmetic in the same order). A single
+  // layer's factorisation is a chain of launches bound by their latency, to
+  // which the extra launch per super-panel would add: it applies every panel
+  // everywhere at once.
+  const int sup = nl > 1 ? kSup : nblk + 1;
   for (int k = -1; k <= nblk - 2; ++k) {
+    const int c = k + 1;                          // the panel column this launch factors
+    int apply = k >= 0 ? 1 : 0;
+    int t_end;
+    if (sup > nblk) {
+      t_end = nblk;
+    } else if (c % sup == 0) {
+      if (c > 0) {
+        const int gr = (nblk - c + 1) / 2;
+        hipLaunchKernelGGL(chol_trail_kernel, dim3(gr * (gr + 1) / 2, nl), dim3(kThreads), 0, stream, L, d,
+                           c - sup, c, ws);
+      }
+      apply = 0;                                  // panel k reached column c with its super-panel
+      t_end = c;                                  // and no column of its super-panel is left
+    } else {
+      t_end = min(nblk, (c / sup + 1) * sup);
+    }
     const int m = nblk - 1 - k;                   // blocks of the next panel column
-    const int groups = (nblk - 2 - k + 1) / 2;    // 2 x 2 groups per side of the trailing triangle
-    const int grid = m + (k < 0 ? 0 : groups * (groups + 1) / 2);
-    hipLaunchKernelGGL(chol_step_kernel, dim3(grid, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, w.status, ws);
+    const int rows = (nblk - k - 2 + 1) / 2;      // group rows of the trailing part
+    const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;  // launch -1 has no panel to apply
+    const int grid = m + cols * rows - cols * (cols - 1) / 2;
+    hipLaunchKernelGGL(chol_step_kernel, dim3(grid, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end, apply,
+                       w.status, ws);
   }
   // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above
   hipLaunchKernelGGL(inv256_kernel, dim3(nb, 4, nl), dim3(kThreads), 0, stream, L, w.dinv, xinv, d, ws);
