@@ -434,15 +434,20 @@ __global__ __launch_bounds__(kThreads) void chol_trail_kernel(float* L, int n, i
 // t_end - 1 (all rows below) in 2 x 2 groups of blocks, group column by group
 // column. Columns from t_end on receive panel k later, with the rest of its
 // super-panel (chol_trail_kernel).
+// split = 0: every workgroup of the panel column factors the diagonal block
+// itself (no launch waits for another). split = 1: only the diagonal block
+// (one workgroup), which leaves its inverse in Dinv; split = 2: the blocks
+// below it, which read that inverse, and the trailing part. Both forms do the
+// same arithmetic in the same order.
 __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int t_end,
-                                                            int apply, int* status, int64_t ws) {
+                                                            int apply, int split, int* status, int64_t ws) {
   __shared__ __attribute__((aligned(16))) Tile tiles[6];
   __shared__ int bad;
   L = at_layer(L, ws, blockIdx.y);
   Dinv = at_layer(Dinv, ws, blockIdx.y);
   status = at_layer(status, ws, blockIdx.y);
   const int nblk = (n + kNb - 1) / kNb;
-  const int m = nblk - 1 - k;
+  const int m = split == 2 ? nblk - 2 - k : nblk - 1 - k;  // panel-column workgroups of this launch
   if ((int)blockIdx.x >= m) {
     const int rows = (nblk - k - 2 + 1) / 2;  // group rows of the trailing part
     int idx = (int)blockIdx.x - m, gj = 0;
@@ -456,7 +461,7 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   }
   apply = apply && k >= 0;
   Tile &S = tiles[0], &M = tiles[1], &T = tiles[2], &U = tiles[3], &V = tiles[4], &P = tiles[5];
-  const int r = k + 1 + (int)blockIdx.x, t = k + 1;  // block coordinates
+  const int r = k + 1 + (split == 2 ? 1 : 0) + (int)blockIdx.x, t = k + 1;  // block coordinates
   const int rr = min(kNb, n - r * kNb);
   float* Lrt = L + (int64_t)r * kNb * n + t * kNb;
   if (threadIdx.x == 0) bad = 0;
@@ -466,6 +471,34 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   const int nd = min(kNb, n - d * kNb);
   const bool off = r != d;
   Frag fs, fv, ft, fu;
+  if (split == 2) {
+    // below the diagonal block: A_rd - L_rk L_dk^T (the quadrants as the
+    // factor's other waves form them), then times the stored inverse
+    if (apply) fetch(fv, L + (int64_t)d * kNb * n + k * kNb, n, nd, kNb);
+    fetch(ft, Lrt, n, rr, nd);
+    if (apply) fetch(fu, L + (int64_t)r * kNb * n + k * kNb, n, rr, kNb);
+    fetch(fs, Dinv + (int64_t)d * kNb * kNb, kNb, kNb, kNb);
+    if (apply) put(V, fv);
+    put(P, ft);
+    if (apply) put(U, fu);
+    put(M, fs);
+    __syncthreads();
+    if (apply) {
+      const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+      const int r0 = (wave >> 1) * 32, c0 = (wave & 1) * 32;
+      f32x16 acc = {};
+      mma<false, true>(acc, U, r0, 0, V, c0, 0, kNb, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) P[r0 + acc_row(e, lane)][c0 + (lane & 31)] -= acc[e];
+      __syncthreads();
+    }
+    const f32x16 x = quad<false, true>(P, M);
+    __syncthreads();
+    quad_store(P, x, 1.f, false);
+    __syncthreads();
+    store_tile(P, Lrt, n, rr, nd);
+    return;
+  }
   fetch(fs, L + (int64_t)d * kNb * n + d * kNb, n, nd, nd);
   if (apply) fetch(fv, L + (int64_t)d * kNb * n + k * kNb, n, nd, kNb);
   if (off) {
@@ -1117,9 +1150,19 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     const int m = nblk - 1 - k;                   // blocks of the next panel column
     const int rows = (nblk - k - 2 + 1) / 2;      // group rows of the trailing part
     const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;  // launch -1 has no panel to apply
-    const int grid = m + cols * rows - cols * (cols - 1) / 2;
-    hipLaunchKernelGGL(chol_step_kernel, dim3(grid, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end, apply,
-                       w.status, ws);
+    const int groups = cols * rows - cols * (cols - 1) / 2;
+    if (nl == 1) {
+      hipLaunchKernelGGL(chol_step_kernel, dim3(m + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end,
+                         apply, 0, w.status, ws);
+    } else {
+      // with many layers the diagonal block is factored once per layer, in its
+      // own launch, rather than once per block of the column
+      hipLaunchKernelGGL(chol_step_kernel, dim3(1, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end, apply, 1,
+                         w.status, ws);
+      if (m - 1 + groups > 0)
+        hipLaunchKernelGGL(chol_step_kernel, dim3(m - 1 + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k,
+                           t_end, apply, 2, w.status, ws);
+    }
   }
   // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above
   hipLaunchKernelGGL(inv256_kernel, dim3(nb, 4, nl), dim3(kThreads), 0, stream, L, w.dinv, xinv, d, ws);
