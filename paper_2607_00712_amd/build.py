@@ -13,7 +13,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libispa.so")
 
-SOURCES = ["ispa_abi.cpp", "attn_fast.cpp", "attn_chunk.hip", "stats.hip", "solve.hip", "absorb.hip", "project.hip"]
+SOURCES = ["ispa_abi.cpp", "attn_fast.cpp", "gram_fast.cpp", "attn_chunk.hip", "stats.hip", "solve.hip", "absorb.hip",
+           "project.hip"]
 BUILD = os.path.join(PKG, "_build")
 LLVM_BIN = os.environ.get("ROCM_LLVM_BIN", "/opt/rocm/lib/llvm/bin")
 
@@ -42,33 +43,34 @@ def _run(cmd):
         raise subprocess.CalledProcessError(res.returncode, cmd, res.stdout)
 
 
-def build_attn_fast():
-    """Generate the assembly of the head_dim-128 attention kernel, assemble it
-    into a gfx950 code object and write it as a C initializer list that
-    attn_fast.cpp embeds."""
+def assemble(module, stem):
+    """Generate the assembly of a hand-scheduled kernel (generator `module` in
+    csrc), assemble it into a gfx950 code object and write that as a C
+    initializer list (_build/<stem>_hsaco.inc) that <stem>.cpp embeds."""
     sys.path.insert(0, CSRC)
     try:
-        import attn_fast_gen
+        gen = __import__(module)
     finally:
         sys.path.pop(0)
     os.makedirs(BUILD, exist_ok=True)
-    asm = os.path.join(BUILD, "attn_fast.s")
-    obj = os.path.join(BUILD, "attn_fast.o")
-    co = os.path.join(BUILD, "attn_fast.hsaco")
+    asm = os.path.join(BUILD, stem + ".s")
+    obj = os.path.join(BUILD, stem + ".o")
+    co = os.path.join(BUILD, stem + ".hsaco")
     with open(asm, "w") as f:
-        f.write(attn_fast_gen.generate())
+        f.write(gen.generate())
     _run([os.path.join(LLVM_BIN, "clang"), "-x", "assembler", "-target", "amdgcn-amd-amdhsa", "-mcpu=gfx950",
           "-c", asm, "-o", obj])
     _run([os.path.join(LLVM_BIN, "ld.lld"), "-shared", obj, "-o", co])
     data = open(co, "rb").read()
-    with open(os.path.join(BUILD, "attn_fast_hsaco.inc"), "w") as f:
+    with open(os.path.join(BUILD, stem + "_hsaco.inc"), "w") as f:
         for i in range(0, len(data), 24):
             f.write(", ".join(str(b) for b in data[i:i + 24]) + ",\n")
 
 
 def build(verbose=False):
     """Compile every source into libispa.so; raises CalledProcessError on failure."""
-    build_attn_fast()
+    assemble("attn_fast_gen", "attn_fast")   # head_dim-128 chunk attention
+    assemble("gram_fast_gen", "gram_fast")   # Gram of widths that are multiples of 256
     srcs = []
     for s in SOURCES:
         p = os.path.join(CSRC, s)

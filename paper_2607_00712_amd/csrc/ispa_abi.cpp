@@ -365,8 +365,10 @@ int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* 
                                  h->stream) != hipSuccess)
       return ISPA_ERR_HIP;
     const uint16_t* xg = x_dtype == ISPA_DTYPE_BF16 ? (const uint16_t*)xp : xb;
+    // the solve's right-hand-side area is free between solves: scratch for the Gram
     if (ispa::launch_gram(xg, rb, rows, h->d_in, h->d_out, G, C, sqp,
-                          ispa::discrepancy_grid(rows, h->d_in, h->d_out), sq, h->stream) != hipSuccess)
+                          ispa::discrepancy_grid(rows, h->d_in, h->d_out), sq, (float*)(h->ws + h->lay.W),
+                          (size_t)h->d_in * h->d_out * sizeof(float), h->stream) != hipSuccess)
       return ISPA_ERR_HIP;
   }
   h->n_rows += n_rows;

@@ -101,8 +101,16 @@ constexpr int kGramSplitTiles = 256;
 int gram_tiles(int d_in, int d_out);
 hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out,
                        float* G, float* C, const double* sq_part, int n_sq_part, double* sq_norm,
-                       hipStream_t stream);
+                       float* scratch, size_t scratch_bytes, hipStream_t stream);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
+// the hand-scheduled Gram kernel (gram_fast.cpp): widths that are multiples of
+// 256 with at least kGramSplitTiles tiles of 256 x 256
+bool gram_fast_eligible(int64_t rows, int d_in, int d_out);
+// (scratch: room for the sums of split tiles' second halves; n_whole / n_split:
+// the tiles computed whole and split, for the fixed-order add that follows)
+hipError_t launch_gram_fast(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out, float* G,
+                            float* C, float* scratch, size_t scratch_bytes, int* n_whole, int* n_split,
+                            hipStream_t stream);
 
 // ---- absorption (absorb.hip) ----
 // W += dW (transposed: W[j][i] += dW[i][j]); dtype 0 bf16, 1 fp32

@@ -346,21 +346,43 @@ __device__ __forceinline__ void gram2_stage(const GramArgs& a, const GramTile& t
   __builtin_amdgcn_s_barrier();
 }
 
+// The norm partials of the discrepancy kernel that ran before on the stream,
+// added to s in workgroup order (one wave: lane i takes partials i, i + 64,
+// ..., then a fixed shuffle tree).
+__device__ void add_sq_parts(const GramArgs& a) {
+  double sq = 0.0;
+  for (int b = threadIdx.x; b < a.n_sq_part; b += 64) sq += a.sq_part[b];
+  sq = wave_sum(sq);
+  if (threadIdx.x == 0) *a.sq_norm += sq;
+}
+
+// The same on its own, beside the hand-scheduled Gram kernel (one wave).
+__global__ __launch_bounds__(64) void sq_norm_kernel(GramArgs a) { add_sq_parts(a); }
+
+// After a hand-scheduled Gram launch that split its last tiles into row
+// halves: tile n_whole + q (256 x 256, the panel-group order) += the second
+// half's sums in scratch slot q; the first half has already added its own, so
+// every element is summed in a fixed order. 64 workgroups per tile, 4 rows each.
+__global__ __launch_bounds__(256) void gram_fixup_kernel(float* G, float* C, const float* ws, int n_whole,
+                                                         int tiles_in, int tiles_out, int d_in, int d_out) {
+  const int q = blockIdx.y;
+  int ti, tj;
+  const bool is_g = gram_tile_of(n_whole + q, tiles_in, tiles_out, ti, tj);
+  float* out = is_g ? G : C;
+  const int ld = is_g ? d_in : d_out;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), col = (threadIdx.x & 63) * 4;
+  f32x4* o = (f32x4*)(out + (int64_t)(256 * ti + row) * ld + 256 * tj + col);
+  const f32x4 w = *(const f32x4*)(ws + (int64_t)q * 65536 + row * 256 + col);
+  *o = *o + w;
+}
+
 // SPLIT = 2: 16 waves, waves 8..15 take the second half of the rows with
 // their own ring, and their partial tile reaches waves 0..7 through LDS.
 template <int SPLIT>
 __global__ __launch_bounds__(kG2Threads * SPLIT) __attribute__((amdgpu_waves_per_eu(2 * SPLIT))) void gram_kernel(
     GramArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_all[SPLIT * kGRing * kG2Stage];
-  // the norm partials of the discrepancy kernel that ran before this launch,
-  // in workgroup order (one wave: lane i takes partials i, i + 64, ..., then a
-  // fixed shuffle tree)
-  if (blockIdx.x == 0 && threadIdx.x < 64) {
-    double sq = 0.0;
-    for (int b = threadIdx.x; b < a.n_sq_part; b += 64) sq += a.sq_part[b];
-    sq = wave_sum(sq);
-    if (threadIdx.x == 0) *a.sq_norm += sq;
-  }
+  if (blockIdx.x == 0 && threadIdx.x < 64) add_sq_parts(a);
   // The work list (tiles in panel-group order) is cut into 8 contiguous
   // ranges, one per XCD (workgroups are dealt to the XCDs round robin), so
   // that the workgroups resident on one XCD at a time work on few distinct
@@ -511,13 +533,24 @@ int gram_tiles(int d_in, int d_out) {
 
 hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out,
                        float* G, float* C, const double* sq_part, int n_sq_part, double* sq_norm,
-                       hipStream_t stream) {
+                       float* scratch, size_t scratch_bytes, hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
   GramArgs a;
   a.x = x; a.r = r; a.G = G; a.C = C; a.rows = rows; a.d_in = d_in; a.d_out = d_out;
   a.sq_part = sq_part;
   a.n_sq_part = n_sq_part;
   a.sq_norm = sq_norm;
+  if (gram_fast_eligible(rows, d_in, d_out)) {
+    hipLaunchKernelGGL(sq_norm_kernel, dim3(1), dim3(64), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int n_whole = 0, n_split = 0;
+    e = launch_gram_fast(x, r, rows, d_in, d_out, G, C, scratch, scratch_bytes, &n_whole, &n_split, stream);
+    if (e != hipSuccess || n_split == 0) return e;
+    hipLaunchKernelGGL(gram_fixup_kernel, dim3(64, n_split), dim3(256), 0, stream, G, C, scratch, n_whole,
+                       d_in / 256, d_out / 256, d_in, d_out);
+    return hipGetLastError();
+  }
   a.tiles_in = (d_in + kG2T - 1) / kG2T;
   a.tiles_out = (d_out + kG2T - 1) / kG2T;
   a.n_g_tiles = a.tiles_in * (a.tiles_in + 1) / 2;

@@ -134,3 +134,27 @@ def test_warmup_bitwise_reproducible():
     assert sa == sb
     assert torch.equal(dwa, dwb)
     assert ea == eb
+
+
+@pytest.mark.parametrize("d_in,d_out,chunks", [(5120, 2560, (777, 1, 64)), (4096, 4096, (1000,)),
+                                                (5120, 5120, (777, 33))])
+def test_gram_256_tiles(d_in, d_out, chunks):
+    """Widths that are multiples of 256 with enough 256 x 256 tiles to fill the
+    chip take the hand-scheduled Gram kernel: G and C against the oracle over
+    ragged chunks (a last 32-row stage part empty, a one-row chunk), and a
+    second run bitwise equal to the first. At 5120 x 5120 (610 tiles on 256
+    compute units) the last 98 tiles are computed as two row halves each (a
+    33-row chunk: halves of one row stage each)."""
+    print(f"[stats] 256-tile Gram {d_in} x {d_out}, chunks {chunks}", flush=True)
+    blocks = [rand_block(26, i, r, d_in, d_out, torch.bfloat16, torch.float32) for i, r in enumerate(chunks)]
+    runs = []
+    for _ in range(2):
+        st = ispa.Stats(d_in, d_out, max_rows=max(chunks), device=DEV)
+        for b in blocks:
+            st.accum(*b)
+        torch.cuda.synchronize()
+        G, C, s, n = st.views()
+        runs.append((G.clone(), C.clone(), float(s.item())))
+    check(st, blocks, d_in, d_out)
+    (Ga, Ca, sa), (Gb, Cb, sb) = runs
+    assert torch.equal(torch.tril(Ga), torch.tril(Gb)) and torch.equal(Ca, Cb) and sa == sb
