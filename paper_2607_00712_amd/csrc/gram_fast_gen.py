@@ -404,36 +404,54 @@ class Gen:
                   f"v_mul_lo_u32 {vp(T)}, {vp(T)}, {sp(S_Z)}",
                   f"v_and_b32_e32 {vp(T + 1)}, 31, {vp(V_LANE)}",
                   f"v_lshl_add_u32 {vp(T)}, {vp(T + 1)}, 2, {vp(T)}")       # lane's voffset in a block
-        D = T + 8                                                            # 16 values
+        # block (ai, bj) adds 32 ai rows and 32 bj columns to the lane's voffset;
+        # the read-modify-write is pipelined over two 16-value buffers (the
+        # operand registers, free here): the loads of block k + 1 are in flight
+        # while block k is added and stored (memory operations retire in order,
+        # so vmcnt(16) / vmcnt(32) leave exactly the younger block's loads, or
+        # those and the older block's stores, outstanding)
+        blocks = [(ai, bj) for ai in range(4) for bj in range(4)]
+        VB = (V_OPS[0], V_OPS[0] + 16)
+        VO = (V_OPS[1], V_OPS[1] + 1)                                        # voffsets per buffer
+
+        def voff(k):
+            ai, bj = blocks[k]
+            return [f"s_mul_i32 {sp(S_X)}, {sp(S_Z)}, {32 * ai}",
+                    f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {128 * bj}",
+                    f"v_add_u32_e32 {vp(VO[k & 1])}, {sp(S_X)}, {vp(T)}"]
+
+        def loads(k):
+            return [f"buffer_load_dword {vp(VB[k & 1] + r)}, {vp(VO[k & 1])}, {sp(S_OUT, 4)}, {sp(S_EO + r)} offen"
+                    for r in range(16)]
+
+        def stores(k, src):
+            return [f"buffer_store_dword {vp(src + r)}, {vp(VO[k & 1])}, {sp(S_OUT, 4)}, {sp(S_EO + r)} offen"
+                    for r in range(16)]
+
         self.emit(f"s_cmp_eq_u32 {sp(S_PIECE)}, 1", f"s_cbranch_scc1 .Lstore_ws{u}")
-        for add in (True, False):
-            if not add:
-                self.label(f".Lstore_ws{u}")
-            for ai in range(4):
-                for bj in range(4):
-                    acc = 16 * (4 * ai + bj)
-                    # block (ai, bj): + 32 ai rows, + 32 bj columns
-                    self.emit(f"s_mul_i32 {sp(S_X)}, {sp(S_Z)}, {32 * ai}",
-                              f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {128 * bj}",
-                              f"v_add_u32_e32 {vp(T + 2)}, {sp(S_X)}, {vp(T)}")
-                    if add:
-                        for r in range(16):
-                            self.emit(f"buffer_load_dword {vp(D + r)}, {vp(T + 2)}, {sp(S_OUT, 4)}, "
-                                      f"{sp(S_EO + r)} offen")
-                        self.emit("s_waitcnt vmcnt(0)")
-                        for r in range(16):
-                            self.emit(f"v_accvgpr_read_b32 {vp(T + 3)}, {ap(acc + r)}",
-                                      f"v_add_f32_e32 {vp(D + r)}, {vp(D + r)}, {vp(T + 3)}")
-                    else:
-                        self.emit("s_waitcnt vmcnt(0)")
-                        for r in range(16):
-                            self.emit(f"v_accvgpr_read_b32 {vp(D + r)}, {ap(acc + r)}")
-                        self.emit("s_nop 1")
-                    for r in range(16):
-                        self.emit(f"buffer_store_dword {vp(D + r)}, {vp(T + 2)}, {sp(S_OUT, 4)}, "
-                                  f"{sp(S_EO + r)} offen")
-            if add:
-                self.emit("s_branch .Lstored")
+        self.emit(*voff(0), *loads(0))
+        for k in range(16):
+            acc = 16 * (4 * blocks[k][0] + blocks[k][1])
+            if k + 1 < 16:
+                self.emit(*voff(k + 1), *loads(k + 1))
+                self.emit("s_waitcnt vmcnt(16)" if k == 0 else "s_waitcnt vmcnt(32)")
+            else:
+                self.emit("s_waitcnt vmcnt(16)")
+            for r in range(16):
+                self.emit(f"v_accvgpr_read_b32 {vp(T + 3)}, {ap(acc + r)}",
+                          f"v_add_f32_e32 {vp(VB[k & 1] + r)}, {vp(VB[k & 1] + r)}, {vp(T + 3)}")
+            self.emit(*stores(k, VB[k & 1]))
+        self.emit("s_branch .Lstored")
+        # the second half of a split tile: plain stores of the sums
+        self.label(f".Lstore_ws{u}")
+        for k in range(16):
+            acc = 16 * (4 * blocks[k][0] + blocks[k][1])
+            self.emit(*voff(k))
+            for r in range(16):
+                self.emit(f"v_accvgpr_read_b32 {vp(VB[k & 1] + r)}, {ap(acc + r)}")
+            self.emit("s_nop 1", *stores(k, VB[k & 1]))
+            if k + 1 < 16:
+                self.emit("s_waitcnt vmcnt(16)")    # the other buffer's stores have read their data
         self.label(".Lstored")
         self.emit("s_waitcnt vmcnt(0)")
 
