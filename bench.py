@@ -419,6 +419,74 @@ def hbm_copy(steps, warmup, nbytes=1 << 30):
             "GB/s": round(2 * nbytes / ms / 1e6, 1)}
 
 
+def lib_ref(steps, warmup):
+    """Library references on the same shapes, for context beside the kernels
+    here (never part of the step): torch's scaled-dot-product attention limited
+    to its flash backend (bf16, one output per call: the full cache and the
+    window timed separately), torch's bf16 GEMM for X^T R, torch's fp32
+    Cholesky factor plus triangular solves for one ridge system, and torch's
+    bf16 GEMM for the chunk's projection A W^T. Inputs are random; each entry is
+    the mean of `steps` calls after `warmup`, timed with events on torch's
+    stream."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    import torch.nn.functional as F
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev).manual_seed(7)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    out = {"only": "lib_ref", "steps": steps, "warmup": warmup}
+    for key in ("1.3b", "14b"):
+        w = WORKLOADS[key]
+        H, hd, n_q, N, win = w["heads"], w["head_dim"], w["n_q"], w["cache_len"], w["window"]
+        D = H * hd
+        r = {}
+        q = torch.randn(1, H, n_q, hd, device=dev, dtype=torch.bfloat16, generator=g)
+        k = torch.randn(1, H, N, hd, device=dev, dtype=torch.bfloat16, generator=g)
+        v = torch.randn(1, H, N, hd, device=dev, dtype=torch.bfloat16, generator=g)
+        kw, vw = k[:, :, N - win:].contiguous(), v[:, :, N - win:].contiguous()
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            ms = timed(lambda: F.scaled_dot_product_attention(q, k, v))
+            r["sdpa_flash_full"] = {"ms": round(ms, 4), "tflops": round(4.0 * n_q * N * D / ms / 1e9, 1)}
+            ms = timed(lambda: F.scaled_dot_product_attention(q, kw, vw))
+            r["sdpa_flash_window"] = {"ms": round(ms, 4), "tflops": round(4.0 * n_q * win * D / ms / 1e9, 1)}
+        del q, k, v, kw, vw
+        xt = torch.randn(D, n_q, device=dev, dtype=torch.bfloat16, generator=g)
+        rr = torch.randn(n_q, D, device=dev, dtype=torch.bfloat16, generator=g)
+        ms = timed(lambda: torch.mm(xt, rr))
+        r["gemm_bf16_xtr"] = {"shape": [D, D, n_q], "ms": round(ms, 4),
+                              "tflops": round(2.0 * n_q * D * D / ms / 1e9, 1)}
+        wt = torch.randn(D, D, device=dev, dtype=torch.bfloat16, generator=g)
+        ms = timed(lambda: torch.mm(rr, wt))
+        r["gemm_bf16_proj"] = {"shape": [n_q, D, D], "ms": round(ms, 4),
+                               "tflops": round(2.0 * n_q * D * D / ms / 1e9, 1)}
+        del xt, rr, wt
+        a = torch.randn(D, 2 * D, device=dev, dtype=torch.float32, generator=g)
+        spd = a @ a.t() / (2 * D) + 1e-3 * torch.eye(D, device=dev)
+        c = torch.randn(D, D, device=dev, dtype=torch.float32, generator=g)
+
+        def chol_solve():
+            fac = torch.linalg.cholesky(spd)
+            return torch.cholesky_solve(c, fac)
+        ms = timed(chol_solve)
+        r["torch_cholesky_solve_fp32"] = {"shape": [D, D], "ms": round(ms, 4),
+                                          "tflops": round((D ** 3 / 3.0 + 2.0 * D ** 3) / ms / 1e9, 2)}
+        del a, spd, c
+        torch.cuda.empty_cache()
+        out[key] = r
+    return out
+
+
 def cpu_baseline(w, budget_rows=512, heads=None):
     """The oracle on a bounded sample of one step, scaled to TFLOP/s: attention
     of `budget_rows` query rows over all keys for `heads` of the heads (all by
@@ -620,7 +688,7 @@ def main():
     ap.add_argument("--no-14b", action="store_true",
                     help="skip the 14B-shaped step that the default 1.3B run also times (breakdown_14b)")
     ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy",
-                                       "discrepancy"],
+                                       "discrepancy", "lib_ref"],
                     default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
@@ -630,6 +698,9 @@ def main():
         sys.exit(2)
     if args.only == "hbm_copy":
         print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "lib_ref":
+        print(json.dumps(lib_ref(args.steps, args.warmup)), flush=True)
         return
     if args.only == "discrepancy":
         print(json.dumps(discrepancy_rotating(WORKLOADS[args.workload], args.steps, args.warmup)), flush=True)

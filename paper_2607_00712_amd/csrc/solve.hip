@@ -646,6 +646,8 @@ struct GemmJob {
   int sub;                    // 1: C -= A B, 0: C = A B
   const float* Cin = nullptr;  // with sub: read the minuend here instead of C (same ldc)
   int64_t la = 0, lc = 0;      // bytes per layer (blockIdx.z) of A and of C / Cin
+  const float* B = nullptr;    // this job's own B operand and depth (gemm_ring_kernel only);
+  int K = 0;                   // null / 0: the shared B and K below
 };
 struct GemmArgs {
   GemmJob job[2];
@@ -1020,11 +1022,14 @@ __global__ __launch_bounds__(kThreads) void gemm_ring_kernel(GemmArgs g) {
     C = at_layer(C, lc, layer);
     Cin = at_layer(Cin, lc, layer);
   }
-  t.B = at_layer(g.B, g.lb, blockIdx.z);
+  {
+    const GemmJob& jb = second ? g.job[1] : g.job[0];
+    t.B = at_layer(jb.B ? jb.B : g.B, g.lb, blockIdx.z);
+    t.K = jb.K ? jb.K : g.K;
+  }
   t.ldb = g.ldb;
   t.N = g.N;
-  t.K = g.K;
-  t.steps = (g.K + kKc - 1) / kKc;
+  t.steps = (t.K + kKc - 1) / kKc;
   t.lane = threadIdx.x & 63;
   t.wave = threadIdx.x >> 6;
   const int h = t.lane >> 5, l32 = t.lane & 31;
@@ -1199,48 +1204,82 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
                        stream, g);
     hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk, nl), dim3(kThreads), 0, stream, L, d, ws);
   }
-  // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I
-  for (int I = 0; I < nb; ++I) {
-    const int kI = min(kBb, d - I * kBb);
+  // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I. After the first
+  // block the blocks go in pairs (I, I+1): one launch finishes Y_{I+1} and forms
+  // dW_I, the next updates every later block with both (depth 512, so the
+  // read-modify-write of the right-hand side below is shared by two blocks)
+  // and forms dW_{I+1}. The A operand is the mirrored Lh above the diagonal,
+  // whose rows I*256 .. of blocks I and I+1 are consecutive.
+  auto fwd_launch = [&](const float* A, float* Ydst, const float* Ysrc, int M, const float* Bsum, int Ksum,
+                        int P, const float* Bp, int Kp) -> hipError_t {
     GemmArgs g = {};
-    const int below = d - (I + 1) * kBb;
     int j = 0;
-    // the first step reads the right-hand side C itself (Y = C before any update)
-    const float* Yin = I == 0 ? C : Y;
-    if (below > 0) {
-      g.job[j] = GemmJob{L + (int64_t)I * kBb * d + (int64_t)(I + 1) * kBb, Y + (int64_t)(I + 1) * kBb * d_out,
-                         below, d, d_out, 1, Yin + (int64_t)(I + 1) * kBb * d_out};
+    if (M > 0) {
+      g.job[j] = GemmJob{A, Ydst, M, d, d_out, 1, Ysrc};
       g.job[j].la = g.job[j].lc = ws;
+      g.job[j].B = Bsum;
+      g.job[j].K = Ksum;
       ++j;
     }
-    g.job[j] = GemmJob{pinv + (int64_t)I * kBb * kBb, delta_w + (int64_t)I * kBb * d_out, kI, kBb, d_out, 0};
+    g.job[j] = GemmJob{pinv + (int64_t)P * kBb * kBb, delta_w + (int64_t)P * kBb * d_out, Kp, kBb, d_out, 0};
     g.job[j].la = ws;
     g.job[j].lc = dws;
+    g.job[j].B = Bp;
+    g.job[j].K = Kp;
     ++j;
     g.n_jobs = j;
     g.lb = ws;
-    g.B = Yin + (int64_t)I * kBb * d_out;
+    g.B = Bp;
     g.N = d_out;
-    g.K = kI;
+    g.K = Kp;
     g.ldb = d_out;
-    const hipError_t e = launch_gemm(g, nl, stream);
+    return launch_gemm(g, nl, stream);
+  };
+  auto yblk = [&](auto* base, int I) { return base + (int64_t)I * kBb * d_out; };
+  auto kblk = [&](int I) { return min(kBb, d - I * kBb); };
+  auto lup = [&](int I, int r) { return L + (int64_t)I * kBb * d + (int64_t)r * kBb; };  // rows of I, columns of r
+  {
+    // the first step reads the right-hand side C itself (Y = C before any update)
+    const hipError_t e = fwd_launch(lup(0, 1), yblk(Y, 1), yblk(C, 1), d - kBb, C, kblk(0), 0, C, kblk(0));
     if (e != hipSuccess) return e;
   }
-  // backward sweep: dW_I -= Lh_JI^T dW_J (I < J)
-  for (int J = nb - 1; J >= 1; --J) {
-    const int kJ = min(kBb, d - J * kBb);
+  for (int I = 1; I < nb; I += 2) {
+    hipError_t e;
+    if (I + 1 == nb) {
+      e = fwd_launch(nullptr, nullptr, nullptr, 0, nullptr, 0, I, yblk(Y, I), kblk(I));
+      if (e != hipSuccess) return e;
+      break;
+    }
+    e = fwd_launch(lup(I, I + 1), yblk(Y, I + 1), yblk(Y, I + 1), kblk(I + 1), yblk(Y, I), kBb, I, yblk(Y, I), kBb);
+    if (e != hipSuccess) return e;
+    const int below = d - (I + 2) * kBb;
+    e = fwd_launch(below > 0 ? lup(I, I + 2) : nullptr, yblk(Y, I + 2), yblk(Y, I + 2), max(below, 0), yblk(Y, I),
+                   kBb + kblk(I + 1), I + 1, yblk(Y, I + 1), kblk(I + 1));
+    if (e != hipSuccess) return e;
+  }
+  // backward sweep: dW_I -= Lh_JI^T dW_J (I < J), from the last block down in
+  // pairs (J, J-1): one launch finishes dW_{J-1}, the next updates every earlier
+  // block with both (rows (J-1)*256 .. of L, depth 512)
+  auto bwd_launch = [&](int J, int M, int K, float* Cdst) -> hipError_t {
     GemmArgs g = {};
-    g.job[0] = GemmJob{L + (int64_t)J * kBb * d, delta_w, J * kBb, d, d_out, 1};
+    g.job[0] = GemmJob{L + (int64_t)J * kBb * d + (Cdst - delta_w) / d_out, Cdst, M, d, d_out, 1};
     g.job[0].la = ws;
     g.job[0].lc = dws;
     g.lb = dws;
     g.n_jobs = 1;
-    g.B = delta_w + (int64_t)J * kBb * d_out;
+    g.B = yblk(delta_w, J);
     g.N = d_out;
-    g.K = kJ;
+    g.K = K;
     g.ldb = d_out;
-    const hipError_t e = launch_gemm(g, nl, stream);
+    return launch_gemm(g, nl, stream);
+  };
+  for (int J = nb - 1; J >= 1; J -= 2) {
+    hipError_t e = bwd_launch(J, kBb, kblk(J), yblk(delta_w, J - 1));
     if (e != hipSuccess) return e;
+    if (J - 1 >= 1) {
+      e = bwd_launch(J - 1, (J - 1) * kBb, kBb + kblk(J), delta_w);
+      if (e != hipSuccess) return e;
+    }
   }
   // the P_I area is free once the forward sweep has run: it holds the partial sums
   const int64_t n = (int64_t)d * d_out;

@@ -19,10 +19,12 @@ def rows(wid, i, n, d, dtype=torch.bfloat16):
     return synth.normal((n, d), synth.seed_of(wid, i, synth.X), DEV, dtype=dtype)
 
 
-@pytest.mark.parametrize("d_in,d_out,n", [(200, 72, 700), (776, 328, 1600)])
+@pytest.mark.parametrize("d_in,d_out,n", [(200, 72, 700), (600, 136, 1300), (776, 328, 1600), (1288, 64, 2000)])
 def test_solve_matches_oracle_ragged(d_in, d_out, n):
     # d not a multiple of the 64-wide panel (776: three 256-blocks and a ragged
-    # fourth of 8 rows); rows > d so G is well conditioned
+    # fourth of 8 rows); 600 and 1288 give three and six 256-blocks, so the
+    # sweeps' pairs of blocks end on a ragged pair and on a ragged single;
+    # rows > d so G is well conditioned
     lam = 0.5
     x = rows(30, 0, n, d_in)
     yf = synth.normal((n, d_out), synth.seed_of(30, 0, synth.Y_FULL), DEV, dtype=torch.float32)
@@ -161,7 +163,7 @@ def _fill_batch(sb, wid, n):
     return refs
 
 
-@pytest.mark.parametrize("d_in,d_out,n,layers", [(200, 72, 700, 3), (776, 328, 1600, 4)])
+@pytest.mark.parametrize("d_in,d_out,n,layers", [(200, 72, 700, 3), (600, 136, 1300, 2), (776, 328, 1600, 4)])
 def test_batch_solve_matches_single(d_in, d_out, n, layers):
     # the batched solve runs every layer's arithmetic unchanged: dW and eps bit
     # for bit those of the single-layer solve, and within the oracle's bound
