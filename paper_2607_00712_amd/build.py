@@ -13,8 +13,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libispa.so")
 
-SOURCES = ["ispa_abi.cpp", "attn_fast.cpp", "gram_fast.cpp", "attn_chunk.hip", "stats.hip", "solve.hip", "absorb.hip",
-           "project.hip"]
+SOURCES = ["ispa_abi.cpp", "attn_fast.cpp", "gram_fast.cpp", "proj_fast.cpp", "attn_chunk.hip", "stats.hip",
+           "solve.hip", "absorb.hip", "project.hip"]
 BUILD = os.path.join(PKG, "_build")
 LLVM_BIN = os.environ.get("ROCM_LLVM_BIN", "/opt/rocm/lib/llvm/bin")
 
@@ -71,6 +71,7 @@ def build(verbose=False):
     """Compile every source into libispa.so; raises CalledProcessError on failure."""
     assemble("attn_fast_gen", "attn_fast")   # head_dim-128 chunk attention
     assemble("gram_fast_gen", "gram_fast")   # Gram of widths that are multiples of 256
+    assemble("proj_fast_gen", "proj_fast")   # projection (bf16 and W8A8) of widths that are multiples of 256
     srcs = []
     for s in SOURCES:
         p = os.path.join(CSRC, s)

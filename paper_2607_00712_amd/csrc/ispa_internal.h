@@ -129,6 +129,11 @@ hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int
 // [d_out, d_in]; d_in a multiple of 64
 hipError_t launch_project_w8a8(const int8_t* qa, const float* sa, const int8_t* qw, const float* sw, int64_t n,
                                int d_in, int d_out, void* y, int y_bf16, int n_cu, hipStream_t stream);
+// the hand-scheduled projection kernels (proj_fast.cpp): d_out a multiple of
+// 256 and at least 512 rows; with i8 the W8A8 form (sa, sw its scales)
+bool proj_fast_eligible(int64_t n, int d_in, int d_out, bool i8);
+hipError_t launch_proj_fast(const void* a, const void* w, const float* sa, const float* sw, int64_t n, int d_in,
+                            int d_out, void* y, int y_bf16, bool i8, int n_cu, hipStream_t stream);
 // per-row int8 codes and scales of x (fp32 or bf16) [rows, cols]; cols a
 // multiple of 8, x 16-byte aligned
 hipError_t launch_quantize_rows(const void* x, int x_bf16, int64_t rows, int cols, int8_t* q, float* scale,

@@ -376,6 +376,8 @@ static hipError_t launch_proj(ProjArgs p, bool i8, int d_out, int n_cu, hipStrea
 
 hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int d_out, void* y, int y_bf16,
                           int n_cu, hipStream_t stream) {
+  if (proj_fast_eligible(n, d_in, d_out, false))
+    return launch_proj_fast(a, w, nullptr, nullptr, n, d_in, d_out, y, y_bf16, false, n_cu, stream);
   ProjArgs p{};
   p.a = (const char*)a;
   p.w = (const char*)w;
@@ -389,6 +391,8 @@ hipError_t launch_project(const void* a, const void* w, int64_t n, int d_in, int
 
 hipError_t launch_project_w8a8(const int8_t* qa, const float* sa, const int8_t* qw, const float* sw, int64_t n,
                                int d_in, int d_out, void* y, int y_bf16, int n_cu, hipStream_t stream) {
+  if (proj_fast_eligible(n, d_in, d_out, true))
+    return launch_proj_fast(qa, qw, sa, sw, n, d_in, d_out, y, y_bf16, true, n_cu, stream);
   ProjArgs p{};
   p.a = (const char*)qa;
   p.w = (const char*)qw;

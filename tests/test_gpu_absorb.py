@@ -106,7 +106,8 @@ def test_attention_over_the_ring():
 # the L-Layer's output projection y = a W^T (W in the linear-layer layout),
 # fp32 accumulation: compared with the fp64 oracle on the same bf16 operands
 @pytest.mark.parametrize("shape", [(64, 128, 64), (300, 256, 200), (4680, 1536, 1536), (777, 5120, 640),
-                                   (1, 32, 8), (4000, 128, 4000)])
+                                   (1, 32, 8), (4000, 128, 4000), (700, 384, 512), (2560, 96, 5120),
+                                   (4200, 256, 4096), (600, 32, 256)])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_projection(shape, out_dtype):
     n, d_in, d_out = shape
@@ -124,6 +125,49 @@ def test_projection(shape, out_dtype):
         tol = tol + 2.0 ** -8 * np.abs(ref)
     err = np.abs(f64(y) - ref)
     assert np.all(err <= tol + 1e-30), f"max excess {np.max(err - tol):.3e}"
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_projection_14b_sampled_rows(out_dtype):
+    # the chunk's projection at the 14B width (4680 x 5120 x 5120: whole
+    # 256 x 256 tiles and the last round's 128-column halves); the oracle
+    # recomputes 24 sampled rows, the last row among them
+    n, d = 4680, 5120
+    g = torch.Generator().manual_seed(14)
+    a = torch.randn((n, d), generator=g).to(torch.bfloat16)
+    w = (torch.randn((d, d), generator=g) / d ** 0.5).to(torch.bfloat16)
+    print(f"projection 14b sampled {out_dtype}", flush=True)
+    y = ispa.project(a.to(DEV), w.to(DEV), out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(5).choice(n, 24, replace=False))
+    rows[-1] = n - 1
+    A = f64(a)[rows]
+    ref = oracle.project(A, f64(w), transposed=True)
+    tol = d * 2.0 ** -24 * (np.abs(A) @ np.abs(f64(w)).T)
+    if out_dtype == torch.bfloat16:
+        tol = tol + 2.0 ** -8 * np.abs(ref)
+    err = np.abs(f64(y)[rows] - ref)
+    assert np.all(err <= tol + 1e-30), f"max excess {np.max(err - tol):.3e}"
+
+
+@pytest.mark.parametrize("shape", [(700, 384, 512), (4200, 256, 4096)])
+def test_projection_fast_and_legacy_kernels(shape, monkeypatch):
+    # widths that are multiples of 256 take the hand-scheduled kernel, others
+    # (and ISPA_PROJ_LEGACY=1) the C++ one: both within the fp32 bound of the
+    # oracle, and each bit for bit the same on a second call
+    n, d_in, d_out = shape
+    g = torch.Generator().manual_seed(n + 3 * d_in)
+    a = torch.randn((n, d_in), generator=g).to(torch.bfloat16).to(DEV)
+    w = (torch.randn((d_out, d_in), generator=g) / d_in ** 0.5).to(torch.bfloat16).to(DEV)
+    ref = oracle.project(f64(a.cpu()), f64(w.cpu()), transposed=True)
+    tol = d_in * 2.0 ** -24 * (np.abs(f64(a.cpu())) @ np.abs(f64(w.cpu())).T)
+    for legacy in ("0", "1"):
+        monkeypatch.setenv("ISPA_PROJ_LEGACY", legacy)
+        y1 = ispa.project(a, w)
+        y2 = ispa.project(a, w)
+        torch.cuda.synchronize()
+        assert torch.equal(y1.view(torch.int32), y2.view(torch.int32))
+        assert np.all(np.abs(f64(y1) - ref) <= tol + 1e-30), f"legacy={legacy}"
 
 
 def test_absorbed_layer_projection():

@@ -61,7 +61,7 @@ def scales(n, g):
 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("shape", [(1, 64, 1), (300, 192, 200), (513, 1536, 384), (257, 320, 131),
-                                   (40, 128, 1000)])
+                                   (40, 128, 1000), (700, 384, 512), (2560, 128, 5120), (4200, 256, 4096)])
 def test_project_w8a8_bitwise(shape, out_dtype):
     n, d_in, d_out = shape
     g = torch.Generator().manual_seed(n * 3 + d_in + d_out)
@@ -75,6 +75,25 @@ def test_project_w8a8_bitwise(shape, out_dtype):
         assert np.array_equal(f32_bits(y), want.view(np.int32))
     else:
         assert np.array_equal(bf16_bits(y), bf16_bits(torch.from_numpy(want).to(torch.bfloat16)))
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_w8a8_fast_kernel_matches_legacy(out_dtype, monkeypatch):
+    # the hand-scheduled kernel (widths that are multiples of 256; whole tiles
+    # and 128-column halves) and the C++ kernel (ISPA_PROJ_LEGACY=1) are both
+    # exact in int32 and dequantise in the same order: bit for bit equal
+    n, d_in, d_out = 4200, 512, 4096
+    g = torch.Generator().manual_seed(42)
+    qa, qw = codes(n, d_in, g).to(DEV), codes(d_out, d_in, g).to(DEV)
+    sa, sw = scales(n, g).to(DEV), scales(d_out, g).to(DEV)
+    monkeypatch.setenv("ISPA_PROJ_LEGACY", "0")
+    y_fast = ispa.project_w8a8(qa, sa, qw, sw, out_dtype=out_dtype)
+    monkeypatch.setenv("ISPA_PROJ_LEGACY", "1")
+    y_old = ispa.project_w8a8(qa, sa, qw, sw, out_dtype=out_dtype)
+    monkeypatch.delenv("ISPA_PROJ_LEGACY")
+    torch.cuda.synchronize()
+    bits = f32_bits if out_dtype == torch.float32 else bf16_bits
+    assert np.array_equal(bits(y_fast), bits(y_old))
 
 
 def test_extreme_codes_accumulate_exactly():
