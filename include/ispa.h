@@ -111,9 +111,13 @@ int ispa_attn_chunk(const void* q, const void* k_cache, const void* v_cache,
  * large part of the last round of workgroups idle (e.g. 12 heads x 19 query
  * blocks = 228 work items on 256 compute units). Split, every workgroup takes
  * an equal run of (work item, 64-key tile) units; runs that end inside a work
- * item leave a normalised partial output and LSE in the workspace, and a merge
- * kernel combines them with Eq. 11-12. The results agree with ispa_attn_chunk
- * within rounding (the merge reassociates the softmax sums).
+ * item leave a normalised partial output and LSE in the workspace, combined
+ * with Eq. 11-12 in run order. At head_dim 128 the run that completes a work
+ * item combines them inside the same kernel (the runs count themselves on
+ * per-item counters in the workspace, which the call clears first); at
+ * head_dim 64 a merge kernel combines them after the launch. The results
+ * agree with ispa_attn_chunk within rounding (the merge reassociates the
+ * softmax sums) and do not depend on which run finishes last.
  *
  *   segments   < 0: never split (exactly ispa_attn_chunk)
  *              0:   split when whole work items would fill the device poorly
@@ -152,7 +156,8 @@ size_t ispa_attn_workspace_bytes(int64_t cache_len, int64_t window, int64_t sink
  *   segments = 0 tells; the 1.3B-shaped dual-stream chunk needs 129 MiB).
  * Every call on one GPU uses the same array: calls that overlap on one GPU
  * (other streams, other threads) race and give undefined results. The array
- * needs no clearing: every partial result is written before it is read.
+ * needs no clearing: the call clears the counters it uses and writes every
+ * partial result before it is read.
  */
 #define ISPA_STATIC_SCRATCH_BYTES ((size_t)160 << 20)
 int ispa_attn_chunk_noalloc(const void* q, const void* k_cache, const void* v_cache,

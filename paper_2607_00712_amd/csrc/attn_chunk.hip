@@ -45,6 +45,8 @@
 // Workgroups are remapped so that the 8 XCDs (dispatched round-robin) each own
 // a contiguous run of (head, query tile) work items: tiles of one head share
 // the K/V stream through one XCD's L2.
+#include <stdlib.h>
+
 #include "ispa_internal.h"
 
 #include <limits.h>
@@ -724,6 +726,8 @@ size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit*
   s->max_pieces = 0;
   s->part_o = nullptr;
   s->part_lse = nullptr;
+  s->ctr = nullptr;
+  s->lse_offset = s->ctr_offset = 0;
   const int T = attn_tiles(a.r, nullptr);
   const int64_t n_work = (int64_t)((a.n_q + kBq - 1) / kBq) * a.n_heads;
   if (segments < 0 || T <= 0) return 0;
@@ -753,8 +757,9 @@ size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit*
   s->n_seg = (int32_t)G;
   s->max_pieces = (int32_t)((seg_max + T - 1) / T + 1);
   const size_t slots = (size_t)G * s->max_pieces * 2 * kBq;
-  const size_t o_bytes = (slots * head_dim * 4 + 255) / 256 * 256;
-  return o_bytes + slots * 4;
+  s->lse_offset = (slots * head_dim * 4 + 255) / 256 * 256;
+  s->ctr_offset = (s->lse_offset + slots * 4 + 255) / 256 * 256;
+  return s->ctr_offset + (size_t)n_work * 2 * 4 * sizeof(uint32_t);
 }
 
 hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream) {
@@ -765,6 +770,14 @@ hipError_t launch_attn_chunk(const AttnArgs& a, int head_dim, hipStream_t stream
   const int grid = per_xcd * kXcds;
   hipError_t e;
   if (attn_fast_eligible(a, head_dim)) {
+    // split: the pieces complete their work items (counters cleared first);
+    // no merge kernel (ISPA_ATTN_MERGE_KERNEL=1: the merge kernel instead)
+    const char* env = getenv("ISPA_ATTN_MERGE_KERNEL");
+    if (a.split.n_seg > 0 && a.split.ctr != nullptr && !(env != nullptr && env[0] == '1')) {
+      e = launch_zero(a.split.ctr, (size_t)n_work * 2 * 4 * sizeof(uint32_t), stream);
+      if (e != hipSuccess) return e;
+      return launch_attn_fast(a, stream);
+    }
     e = launch_attn_fast(a, stream);
   } else {
     if (head_dim == 128) {

@@ -82,6 +82,11 @@ A_U, A_LD, A_NQ, A_QT, A_T, A_LT, A_NSEG, A_MAXP, A_PERXCD, A_NLOG = (arg(o) for
 A_B0, A_E0, A_B1, A_E1, A_B2, A_E2, A_TB1, A_TB2 = (arg(o) for o in range(112, 144, 4))
 A_SCALE, A_C, A_LAZY, A_DUAL, A_NEGC, A_LD2, A_LD4 = (arg(o) for o in range(144, 172, 4))
 
+A_CTR = arg(176)                # split fold: counters [item][stream][wave] (null: no fold)
+# SGPRs of the split fold (argument registers that only the setup reads, and padding)
+S_MFLAG = 54                    # bit w: this piece completes stream w of its item
+S_GLO, S_GHI, S_GG, S_SL = 34, 35, 51, 55
+
 K_REGION, V_REGION, BUF_BYTES, HALF_BYTES = 0, 65536, 16384, 8192
 LDS_BYTES = 131072
 
@@ -522,30 +527,11 @@ class Gen:
         slot S_SLOT (part `which`)."""
         u = self.new_uid()
         T = V_T
+        # partial results are stored coherent at device scope (sc1), so that a
+        # piece on another XCD reads them (also sc1) once the count says so
+        coh = "" if rows else " sc1"
         if rows:
-            optr, lptr = (A_OUT, A_LSE) if which == 0 else (A_OUTL, A_LSEL)
-            # O: base = out + (qrow_b * ld + hoff) * 4; this wave's rows that exist
-            self.mul64(S_X, S_Y, S_QROWB, A_LD4)
-            self.emit(f"s_lshl_b32 {sp(S_W)}, {sp(S_HOFF2)}, 1",
-                      f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_W)}", f"s_addc_u32 {sp(S_Y)}, {sp(S_Y)}, 0")
-            self.add64_to(S_RO, optr, S_X, S_Y)
-            self.emit(f"s_sub_i32 {sp(S_W)}, {sp(A_NQ)}, {sp(S_QROWB)}",
-                      f"s_min_i32 {sp(S_W)}, {sp(S_W)}, 64",
-                      f"s_max_i32 {sp(S_W)}, {sp(S_W)}, 0",
-                      f"s_mul_i32 {sp(S_RO + 2)}, {sp(S_W)}, {sp(A_LD4)}",     # (covers the rows' head slices)
-                      f"s_mov_b32 {sp(S_RO + 3)}, 0x20000",
-                      f"s_mov_b32 {sp(S_X)}, {sp(A_LD4)}")                    # lane stride
-            # LSE: base = lse + (head * n_q + qrow_b) * 4; none when the pointer is null
-            self.emit(f"s_mul_i32 {sp(S_Y)}, {sp(S_HEAD)}, {sp(A_NQ)}",
-                      f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_QROWB)}",
-                      f"s_mul_hi_u32 {sp(S_RL + 3)}, {sp(S_Y)}, 4",
-                      f"s_mul_i32 {sp(S_Y)}, {sp(S_Y)}, 4")
-            self.emit(f"s_add_u32 {sp(S_RL)}, {sp(lptr)}, {sp(S_Y)}",
-                      f"s_addc_u32 {sp(S_RL + 1)}, {sp(lptr + 1)}, {sp(S_RL + 3)}",
-                      f"s_lshl_b32 {sp(S_RL + 2)}, {sp(S_W)}, 2",
-                      f"s_cmp_eq_u64 {sp(lptr, 2)}, 0",
-                      f"s_cselect_b32 {sp(S_RL + 2)}, 0, {sp(S_RL + 2)}",
-                      f"s_mov_b32 {sp(S_RL + 3)}, 0x20000")
+            self.row_resources(which)
         else:
             # O: part_o + ((slot * 2 + which) * 256 + wave * 64) * 512
             self.emit(f"s_lshl_b32 {sp(S_Y)}, {sp(S_SLOT)}, 1")
@@ -595,7 +581,7 @@ class Gen:
                     for i in range(4):
                         self.emit(f"v_mul_f32_e32 {vp(d + i)}, {vp(T + 4)}, {vp(src + i)}")
                     self.emit(f"buffer_store_dwordx4 {vp(d, 4)}, {vp(T + 7)}, {sp(S_RO, 4)}, 0 offen "
-                              f"offset:{128 * db + 32 * j}")
+                              f"offset:{128 * db + 32 * j}{coh}")
             # LSE = m scale + ln(l total), from the lanes of the lower half
             self.emit(f"v_log_f32_e32 {vp(T + 2)}, {vp(T + 2)}",
                       f"v_lshlrev_b32_e32 {vp(T + 6)}, 2, {vp(T + 6)}",
@@ -604,9 +590,370 @@ class Gen:
                       f"v_fma_f32 {vp(T + 3)}, {vp(m)}, {sp(A_SCALE)}, {vp(T + 2)}",
                       f"v_cndmask_b32_e32 {vp(T + 6)}, {vp(T + 6)}, {vp(V_Y)}, vcc",
                       "s_nop 1",
-                      f"buffer_store_dword {vp(T + 3)}, {vp(T + 6)}, {sp(S_RL, 4)}, 0 offen")
+                      f"buffer_store_dword {vp(T + 3)}, {vp(T + 6)}, {sp(S_RL, 4)}, 0 offen{coh}")
         self.emit("s_waitcnt vmcnt(0)")
         del u
+
+    def row_resources(self, which):
+        """S_RO, S_RL: this wave's rows of the output O and LSE of stream
+        `which` (rows past n_q have no records; no LSE records when its
+        pointer is null); S_X = the lane stride of O (bytes per row)."""
+        optr, lptr = (A_OUT, A_LSE) if which == 0 else (A_OUTL, A_LSEL)
+        # O: base = out + (qrow_b * ld + hoff) * 4; this wave's rows that exist
+        self.mul64(S_X, S_Y, S_QROWB, A_LD4)
+        self.emit(f"s_lshl_b32 {sp(S_W)}, {sp(S_HOFF2)}, 1",
+                  f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_W)}", f"s_addc_u32 {sp(S_Y)}, {sp(S_Y)}, 0")
+        self.add64_to(S_RO, optr, S_X, S_Y)
+        self.emit(f"s_sub_i32 {sp(S_W)}, {sp(A_NQ)}, {sp(S_QROWB)}",
+                  f"s_min_i32 {sp(S_W)}, {sp(S_W)}, 64",
+                  f"s_max_i32 {sp(S_W)}, {sp(S_W)}, 0",
+                  f"s_mul_i32 {sp(S_RO + 2)}, {sp(S_W)}, {sp(A_LD4)}",     # (covers the rows' head slices)
+                  f"s_mov_b32 {sp(S_RO + 3)}, 0x20000",
+                  f"s_mov_b32 {sp(S_X)}, {sp(A_LD4)}")                    # lane stride
+        # LSE: base = lse + (head * n_q + qrow_b) * 4; none when the pointer is null
+        self.emit(f"s_mul_i32 {sp(S_Y)}, {sp(S_HEAD)}, {sp(A_NQ)}",
+                  f"s_add_u32 {sp(S_Y)}, {sp(S_Y)}, {sp(S_QROWB)}",
+                  f"s_mul_hi_u32 {sp(S_RL + 3)}, {sp(S_Y)}, 4",
+                  f"s_mul_i32 {sp(S_Y)}, {sp(S_Y)}, 4")
+        self.emit(f"s_add_u32 {sp(S_RL)}, {sp(lptr)}, {sp(S_Y)}",
+                  f"s_addc_u32 {sp(S_RL + 1)}, {sp(lptr + 1)}, {sp(S_RL + 3)}",
+                  f"s_lshl_b32 {sp(S_RL + 2)}, {sp(S_W)}, 2",
+                  f"s_cmp_eq_u64 {sp(lptr, 2)}, 0",
+                  f"s_cselect_b32 {sp(S_RL + 2)}, 0, {sp(S_RL + 2)}",
+                  f"s_mov_b32 {sp(S_RL + 3)}, 0x20000")
+
+    # ---------------------------------------------------------------- split fold
+    # With a counter array (A_CTR non-null), the pieces of a split work item
+    # complete it themselves instead of a merge kernel after the launch: every
+    # piece writes its normalised partial result and LSE to its slot (as for
+    # the merge kernel) with device-coherent stores, and once they are complete
+    # counts itself on the item's counter of that stream with an atomic add;
+    # the piece that brings the count to the number of pieces reads every
+    # piece's partial back with device-coherent loads and combines them with
+    # Eq. 11-12 in piece order, so the result does not depend on which piece
+    # finishes last. No piece ever waits for another, and no cache is written
+    # back or invalidated as a whole.
+    def seg_of(self, s_out, s_unit):
+        """s_out = the segment (workgroup run) that holds unit s_unit:
+        ((u + 1) n_seg - 1) / units (32-bit, as the host checks)."""
+        self.emit(f"s_add_u32 {sp(S_W)}, {sp(s_unit)}, 1",
+                  f"s_mul_i32 {sp(S_W)}, {sp(S_W)}, {sp(A_NSEG)}",
+                  f"s_sub_u32 {sp(S_Y)}, {sp(S_W)}, 1")
+        self.udiv(s_out, S_Y, A_U)
+
+    def piece_segments(self, which):
+        """S_GLO, S_GHI: the first and last segments of this item's stream
+        `which` (all T tiles, or the LT tiles of the local set)."""
+        self.emit(f"s_mul_i32 {sp(S_GG)}, {sp(S_ITEM)}, {sp(A_T)}")
+        self.seg_of(S_GLO, S_GG)
+        self.emit(f"s_add_u32 {sp(S_GG)}, {sp(S_GG)}, {sp(A_T if which == 0 else A_LT)}",
+                  f"s_sub_u32 {sp(S_GG)}, {sp(S_GG)}, 1")
+        self.seg_of(S_GHI, S_GG)
+
+    def counter(self, which):
+        """S_RQ: the record of this wave's counter of stream `which`
+        ((item * 2 + which) * 4 + wave); V_T: lane 0's offset in it, the other
+        lanes' offsets past the record (so one lane accesses it)."""
+        T = V_T
+        self.emit(f"s_lshl_b32 {sp(S_W)}, {sp(S_ITEM)}, 5",
+                  f"s_lshl_b32 {sp(S_Y)}, {sp(S_WAVE)}, 2",
+                  f"s_add_u32 {sp(S_W)}, {sp(S_W)}, {sp(S_Y)}",
+                  f"s_add_u32 {sp(S_RQ)}, {sp(A_CTR)}, {sp(S_W)}",
+                  f"s_addc_u32 {sp(S_RQ + 1)}, {sp(A_CTR + 1)}, 0",
+                  f"s_mov_b32 {sp(S_RQ + 2)}, {16 * which + 4}",
+                  f"s_mov_b32 {sp(S_RQ + 3)}, 0x20000",
+                  f"v_cmp_eq_u32_e32 vcc, 0, {vp(V_LANE)}",
+                  f"v_mov_b32_e32 {vp(T)}, 0x40000000",
+                  "s_nop 1",
+                  f"v_cndmask_b32_e64 {vp(T)}, {vp(T)}, {16 * which}, vcc",
+                  "s_nop 1")
+
+    def count(self, which, done):
+        """Adds this piece to its counter of stream `which` (its partial's
+        device-coherent stores are complete: vmcnt(0) at the end of
+        write_state); branches to `done` unless it completes the stream.
+        Needs S_GLO, S_GHI."""
+        T = V_T
+        self.counter(which)
+        self.emit(f"v_mov_b32_e32 {vp(T + 1)}, 1",
+                  f"buffer_atomic_add {vp(T + 1)}, {vp(T)}, {sp(S_RQ, 4)}, 0 offen sc0",
+                  "s_waitcnt vmcnt(0)",
+                  f"v_readfirstlane_b32 {sp(S_Y)}, {vp(T + 1)}",
+                  "s_nop 4",
+                  f"s_sub_u32 {sp(S_W)}, {sp(S_GHI)}, {sp(S_GLO)}",         # pieces - 1
+                  f"s_cmp_eq_u32 {sp(S_Y)}, {sp(S_W)}",
+                  f"s_cbranch_scc0 {done}")
+
+    def publish(self, which):
+        """At the local snapshot inside a piece, after this piece's partial of
+        stream `which` is in its slot: the count, and the merge flag (the
+        merge from the slots follows at the piece end) when this piece
+        completes the item's stream."""
+        u = self.new_uid()
+        self.emit(f"s_cmp_eq_u64 {sp(A_CTR, 2)}, 0", f"s_cbranch_scc1 .Lpub_done{u}")
+        self.piece_segments(which)
+        self.count(which, f".Lpub_done{u}")
+        self.emit(f"s_or_b32 {sp(S_MFLAG)}, {sp(S_MFLAG)}, {1 << which}",
+                  f".Lpub_done{u}:")
+
+    def finish_stream(self, which):
+        """At the end of a piece that holds part of stream `which` of its item:
+        the partial to the slot and the count; the piece that completes the
+        stream merges. With two pieces the merge takes this piece's own part
+        from its registers, and a piece that finds the other one already
+        counted merges without storing its own part."""
+        u = self.new_uid()
+        T = V_T
+        done = f".Lfin_done{u}"
+        self.emit(f"s_cmp_eq_u64 {sp(A_CTR, 2)}, 0", f"s_cbranch_scc0 .Lfin_fold{u}")
+        self.write_state(False, which)
+        self.emit(f"s_branch {done}", f".Lfin_fold{u}:")
+        self.piece_segments(which)
+        self.emit(f"s_sub_u32 {sp(S_W)}, {sp(S_GHI)}, {sp(S_GLO)}",
+                  f"s_cmp_eq_u32 {sp(S_W)}, 1",
+                  f"s_cbranch_scc0 .Lfin_store{u}")
+        # two pieces: has the other one counted already?
+        self.counter(which)
+        self.emit(f"buffer_load_dword {vp(T + 1)}, {vp(T)}, {sp(S_RQ, 4)}, 0 offen sc1",
+                  "s_waitcnt vmcnt(0)",
+                  f"v_readfirstlane_b32 {sp(S_Y)}, {vp(T + 1)}",
+                  "s_nop 4",
+                  f"s_cmp_eq_u32 {sp(S_Y)}, 1",
+                  f"s_cbranch_scc1 .Lfin_merge2{u}",
+                  f".Lfin_store{u}:")
+        self.write_state(False, which)
+        self.count(which, done)
+        self.emit(f"s_sub_u32 {sp(S_W)}, {sp(S_GHI)}, {sp(S_GLO)}",
+                  f"s_cmp_eq_u32 {sp(S_W)}, 1",
+                  f"s_cbranch_scc1 .Lfin_merge2{u}",
+                  f"s_or_b32 {sp(S_MFLAG)}, {sp(S_MFLAG)}, {1 << which}",
+                  f"s_branch {done}",
+                  f".Lfin_merge2{u}:")
+        self.merge2(which)
+        self.label(done)
+
+    def slot_resources(self, s_g, which):
+        """S_RO, S_RL: this wave's rows of the partial O and LSE of stream
+        `which` that segment s_g left for this item."""
+        # slot of segment g: g max_pieces + item - (its first item)
+        self.emit(f"s_mul_i32 {sp(S_Y)}, {sp(s_g)}, {sp(A_U)}")
+        self.udiv(S_SL, S_Y, A_NSEG)
+        self.udiv(S_SL, S_SL, A_T)
+        self.emit(f"s_mul_i32 {sp(S_W)}, {sp(s_g)}, {sp(A_MAXP)}",
+                  f"s_add_u32 {sp(S_W)}, {sp(S_W)}, {sp(S_ITEM)}",
+                  f"s_sub_u32 {sp(S_SL)}, {sp(S_W)}, {sp(S_SL)}",
+                  # rows of this wave in part (slot, which): ((slot * 2 + which) * 256 + 64 wave)
+                  f"s_lshl_b32 {sp(S_W)}, {sp(S_SL)}, 1")
+        if which:
+            self.emit(f"s_add_u32 {sp(S_W)}, {sp(S_W)}, 1")
+        self.emit(f"s_lshl_b32 {sp(S_W)}, {sp(S_W)}, 8",
+                  f"s_lshl_b32 {sp(S_Y)}, {sp(S_WAVE)}, 6",
+                  f"s_add_u32 {sp(S_W)}, {sp(S_W)}, {sp(S_Y)}",
+                  f"s_mov_b32 {sp(S_Y)}, 512")
+        self.mul64(S_RO, S_RO + 1, S_W, S_Y)
+        self.add64_to(S_RO, A_PO, S_RO, S_RO + 1)
+        self.emit(f"s_mov_b32 {sp(S_Y)}, 4")
+        self.mul64(S_RL, S_RL + 1, S_W, S_Y)
+        self.add64_to(S_RL, A_PL, S_RL, S_RL + 1)
+        self.emit(f"s_mov_b32 {sp(S_RO + 2)}, 32768", f"s_mov_b32 {sp(S_RO + 3)}, 0x20000",
+                  f"s_mov_b32 {sp(S_RL + 2)}, 256", f"s_mov_b32 {sp(S_RL + 3)}, 0x20000")
+
+    def merge2(self, which):
+        """Complete stream `which` of a two-piece item: the other piece's
+        partial from its slot, this piece's own part from its registers
+        (normalised exactly as write_state stores it), combined in piece order
+        with the same operations as merge(), so either piece gives the same
+        bits. O, m, l and the weight sums are this piece's end state."""
+        u = self.new_uid()
+        T = V_T
+        VL, INV, LSO = (T + 4, T + 5), (T + 6, T + 7), (T + 8, T + 9)
+        VA, VB, VM, VI, VO = T + 10, T + 11, T + 12, T + 13, T + 14
+        OUT = V_Y                                   # 64: one block's output rows
+        other = S_GG
+        # every P V and weight-sum MFMA has completed (O and the sums are read below)
+        self.emit("s_nop 7", "s_nop 7", "s_nop 7")
+        # the other segment, and whether this piece comes first
+        self.emit(f"s_cmp_eq_u32 {sp(S_G)}, {sp(S_GLO)}",
+                  f"s_cselect_b32 {sp(other)}, {sp(S_GHI)}, {sp(S_GLO)}")
+        self.slot_resources(other, which)
+        self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}")
+        for qb in range(2):
+            # the other piece's rows 32 qb + ql: LSE and O (into the operand AGPRs)
+            self.emit(f"v_add_u32_e32 {vp(T + 2)}, {32 * qb}, {vp(T)}",
+                      f"v_lshlrev_b32_e32 {vp(T + 3)}, 2, {vp(T + 2)}",
+                      f"v_lshl_add_u32 {vp(VO)}, {vp(T + 2)}, 9, {vp(T + 1)}",
+                      "s_nop 1",
+                      f"buffer_load_dword {vp(VL[qb])}, {vp(T + 3)}, {sp(S_RL, 4)}, 0 offen sc1")
+            for db in range(4):
+                for j in range(4):
+                    self.emit(f"buffer_load_dwordx4 {ap(64 * qb + 16 * db + 4 * j, 4)}, {vp(VO)}, {sp(S_RO, 4)}, 0 "
+                              f"offen offset:{128 * db + 32 * j} sc1")
+        # own part: 1 / (sum of the rounded weights), LSE = m scale + ln(l total)
+        for qb in range(2):
+            m, l = V_ST[qb], V_ST[qb] + 3
+            if SUMS_ON_MFMA:
+                self.emit(f"v_accvgpr_read_b32 {vp(INV[qb])}, {ap(A_LR[qb])}")
+            else:
+                self.emit(f"v_mov_b32_e32 {vp(INV[qb])}, {vp(V_ST[qb] + 1)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(V_ST[qb] + 1)}",
+                          "s_nop 1",
+                          f"v_permlane32_swap_b32 {vp(INV[qb])}, {vp(T + 3)}",
+                          "s_nop 1",
+                          f"v_add_f32_e32 {vp(INV[qb])}, {vp(INV[qb])}, {vp(T + 3)}")
+            self.emit(f"v_mov_b32_e32 {vp(T + 2)}, {vp(l)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(l)}",
+                      "s_nop 1",
+                      f"v_permlane32_swap_b32 {vp(T + 2)}, {vp(T + 3)}",
+                      "s_nop 1",
+                      f"v_add_f32_e32 {vp(T + 2)}, {vp(T + 2)}, {vp(T + 3)}",
+                      f"v_rcp_f32_e32 {vp(INV[qb])}, {vp(INV[qb])}",
+                      f"v_log_f32_e32 {vp(T + 2)}, {vp(T + 2)}",
+                      "s_nop 1",
+                      f"v_mul_f32_e32 {vp(T + 2)}, 0x3f317218, {vp(T + 2)}",
+                      f"v_fma_f32 {vp(LSO[qb])}, {vp(m)}, {sp(A_SCALE)}, {vp(T + 2)}")
+        self.emit("s_waitcnt vmcnt(0)")
+        self.row_resources(which)
+        self.emit(f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_cmp_ne_u32_e32 vcc, 0, {vp(T + 1)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}",
+                  f"s_cmp_eq_u32 {sp(S_G)}, {sp(S_GLO)}",
+                  f"s_cbranch_scc0 .Lm2_second{u}")
+        for own_first in (True, False):
+            if not own_first:
+                self.emit(f".Lm2_second{u}:")
+            for qb in range(2):
+                L1, L2 = (LSO[qb], VL[qb]) if own_first else (VL[qb], LSO[qb])
+                self.emit(f"v_max_f32_e32 {vp(VM)}, {vp(L1)}, {vp(L2)}",
+                          f"v_sub_f32_e32 {vp(VA)}, {vp(L1)}, {vp(VM)}",
+                          f"v_sub_f32_e32 {vp(VB)}, {vp(L2)}, {vp(VM)}",
+                          f"v_mul_f32_e32 {vp(VA)}, 0x3fb8aa3b, {vp(VA)}",
+                          f"v_mul_f32_e32 {vp(VB)}, 0x3fb8aa3b, {vp(VB)}",
+                          f"v_exp_f32_e32 {vp(VA)}, {vp(VA)}",
+                          f"v_exp_f32_e32 {vp(VB)}, {vp(VB)}",
+                          "s_nop 1",
+                          f"v_add_f32_e32 {vp(VI)}, {vp(VA)}, {vp(VB)}",
+                          "s_nop 1",
+                          f"v_log_f32_e32 {vp(T + 2)}, {vp(VI)}",
+                          f"v_rcp_f32_e32 {vp(VI)}, {vp(VI)}",
+                          f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
+                          f"v_add_u32_e32 {vp(T)}, {32 * qb}, {vp(T)}",
+                          f"v_mul_lo_u32 {vp(VO)}, {vp(T)}, {sp(S_X)}",
+                          f"v_add_u32_e32 {vp(VO)}, {vp(VO)}, {vp(T + 1)}",       # O voffset
+                          "s_nop 1")
+                for i in range(64):
+                    own, oth, acc = T + 3, T + 15, OUT + i
+                    self.emit(f"v_mul_f32_e32 {vp(own)}, {vp(INV[qb])}, {vp(V_O[qb] + i)}",
+                              f"v_accvgpr_read_b32 {vp(oth)}, {ap(64 * qb + i)}")
+                    x1, x2 = (own, oth) if own_first else (oth, own)
+                    self.emit(f"v_mul_f32_e32 {vp(acc)}, {vp(x1)}, {vp(VA)}",
+                              f"v_fmac_f32_e32 {vp(acc)}, {vp(VB)}, {vp(x2)}",
+                              f"v_mul_f32_e32 {vp(acc)}, {vp(VI)}, {vp(acc)}")
+                for db in range(4):
+                    for j in range(4):
+                        self.emit(f"buffer_store_dwordx4 {vp(OUT + 16 * db + 4 * j, 4)}, {vp(VO)}, {sp(S_RO, 4)}, 0 "
+                                  f"offen offset:{128 * db + 32 * j}")
+                self.emit(f"v_fmac_f32_e32 {vp(VM)}, 0x3f317218, {vp(T + 2)}",
+                          f"v_lshlrev_b32_e32 {vp(T)}, 2, {vp(T)}",
+                          f"v_mov_b32_e32 {vp(T + 2)}, 0x40000000",
+                          "s_nop 1",
+                          f"v_cndmask_b32_e32 {vp(T)}, {vp(T)}, {vp(T + 2)}, vcc",
+                          "s_nop 1",
+                          f"buffer_store_dword {vp(VM)}, {vp(T)}, {sp(S_RL, 4)}, 0 offen",
+                          "s_waitcnt vmcnt(0)")
+            if own_first:
+                self.emit(f"s_branch .Lm2_done{u}")
+        self.emit(f".Lm2_done{u}:")
+
+    def merge(self, which):
+        """Complete stream `which` of this item from every piece's partial
+        (this wave's 64 rows, both 32-row blocks per round trip): online
+        Eq. 11-12 in piece order, then the normalised rows and LSE to the
+        output. O, the score and operand registers are free here (the piece
+        has ended): block 0 accumulates in O's first half and loads into its
+        second, block 1 accumulates in the score registers and loads into the
+        Q operand registers."""
+        u = self.new_uid()
+        T = V_T
+        ACC = (V_O[0], V_Y)                 # 64 each: accumulators of blocks 0 / 1
+        BUF = (V_O[1], A_Q[0])              # 64 each: a piece's rows (block 1 in AGPRs)
+        VM, VS, VL, VOL, VOO = ((T + 4, T + 5), (T + 6, T + 7), (T + 8, T + 9), (T + 10, T + 11), (T + 12, T + 13))
+        VA, VB = T + 14, T + 15
+        self.piece_segments(which)
+        # lane offsets in a slot: row 32 qb + ql; O bytes 16 hh within the row
+        self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 1)}, 4, {vp(T + 1)}")
+        for qb in range(2):
+            self.emit(f"v_add_u32_e32 {vp(T + 2)}, {32 * qb}, {vp(T)}",
+                      f"v_lshlrev_b32_e32 {vp(VOL[qb])}, 2, {vp(T + 2)}",
+                      f"v_lshl_add_u32 {vp(VOO[qb])}, {vp(T + 2)}, 9, {vp(T + 1)}",
+                      f"v_mov_b32_e32 {vp(VM[qb])}, 0xff800000",
+                      f"v_mov_b32_e32 {vp(VS[qb])}, 0")
+            for i in range(64):
+                self.emit(f"v_mov_b32_e32 {vp(ACC[qb] + i)}, 0")
+        self.emit(f"s_mov_b32 {sp(S_GG)}, {sp(S_GLO)}",
+                  f".Lmg{u}:")
+        self.slot_resources(S_GG, which)
+        for qb in range(2):
+            self.emit(f"buffer_load_dword {vp(VL[qb])}, {vp(VOL[qb])}, {sp(S_RL, 4)}, 0 offen sc1")
+            reg = vp if qb == 0 else ap
+            for db in range(4):
+                for j in range(4):
+                    self.emit(f"buffer_load_dwordx4 {reg(BUF[qb] + 16 * db + 4 * j, 4)}, {vp(VOO[qb])}, "
+                              f"{sp(S_RO, 4)}, 0 offen offset:{128 * db + 32 * j} sc1")
+        self.emit("s_waitcnt vmcnt(0)")
+        for qb in range(2):
+            # m' = max(m, l); a = e^(m - m'), b = e^(l - m'); acc = a acc + b o; s = a s + b
+            self.emit(f"v_max_f32_e32 {vp(T)}, {vp(VM[qb])}, {vp(VL[qb])}",
+                      f"v_sub_f32_e32 {vp(VA)}, {vp(VM[qb])}, {vp(T)}",
+                      f"v_sub_f32_e32 {vp(VB)}, {vp(VL[qb])}, {vp(T)}",
+                      f"v_mov_b32_e32 {vp(VM[qb])}, {vp(T)}",
+                      f"v_mul_f32_e32 {vp(VA)}, 0x3fb8aa3b, {vp(VA)}",
+                      f"v_mul_f32_e32 {vp(VB)}, 0x3fb8aa3b, {vp(VB)}",
+                      f"v_exp_f32_e32 {vp(VA)}, {vp(VA)}",
+                      f"v_exp_f32_e32 {vp(VB)}, {vp(VB)}",
+                      "s_nop 1",
+                      f"v_mul_f32_e32 {vp(VS[qb])}, {vp(VS[qb])}, {vp(VA)}",
+                      f"v_add_f32_e32 {vp(VS[qb])}, {vp(VS[qb])}, {vp(VB)}")
+            for i in range(64):
+                acc = ACC[qb] + i
+                if qb == 0:
+                    src = BUF[0] + i
+                else:
+                    src = T + 2 + (i & 1)
+                    self.emit(f"v_accvgpr_read_b32 {vp(src)}, {ap(BUF[1] + i)}")
+                self.emit(f"v_mul_f32_e32 {vp(acc)}, {vp(acc)}, {vp(VA)}",
+                          f"v_fmac_f32_e32 {vp(acc)}, {vp(VB)}, {vp(src)}")
+        self.emit(f"s_add_u32 {sp(S_GG)}, {sp(S_GG)}, 1",
+                  f"s_cmp_le_u32 {sp(S_GG)}, {sp(S_GHI)}",
+                  f"s_cbranch_scc1 .Lmg{u}")
+        # the completed rows: O = acc / s, LSE = m + ln s (lanes of the lower half)
+        self.row_resources(which)
+        self.emit(f"v_and_b32_e32 {vp(T)}, 31, {vp(V_LANE)}",
+                  f"v_lshrrev_b32_e32 {vp(T + 1)}, 5, {vp(V_LANE)}",
+                  f"v_lshlrev_b32_e32 {vp(T + 2)}, 4, {vp(T + 1)}",
+                  f"v_cmp_ne_u32_e32 vcc, 0, {vp(T + 1)}",
+                  f"v_mov_b32_e32 {vp(T + 1)}, 0x40000000")
+        for qb in range(2):
+            self.emit(f"v_rcp_f32_e32 {vp(VA)}, {vp(VS[qb])}",
+                      f"v_add_u32_e32 {vp(T + 3)}, {32 * qb}, {vp(T)}",
+                      f"v_mul_lo_u32 {vp(VB)}, {vp(T + 3)}, {sp(S_X)}",
+                      f"v_add_u32_e32 {vp(VB)}, {vp(VB)}, {vp(T + 2)}",         # O voffset
+                      "s_nop 1")
+            for i in range(64):
+                self.emit(f"v_mul_f32_e32 {vp(ACC[qb] + i)}, {vp(VA)}, {vp(ACC[qb] + i)}")
+            for db in range(4):
+                for j in range(4):
+                    self.emit(f"buffer_store_dwordx4 {vp(ACC[qb] + 16 * db + 4 * j, 4)}, {vp(VB)}, "
+                              f"{sp(S_RO, 4)}, 0 offen offset:{128 * db + 32 * j}")
+            self.emit(f"v_log_f32_e32 {vp(VL[qb])}, {vp(VS[qb])}",
+                      f"v_lshlrev_b32_e32 {vp(T + 3)}, 2, {vp(T + 3)}",
+                      "s_nop 1",
+                      f"v_fmac_f32_e32 {vp(VM[qb])}, 0x3f317218, {vp(VL[qb])}",
+                      f"v_cndmask_b32_e32 {vp(T + 3)}, {vp(T + 3)}, {vp(T + 1)}, vcc",
+                      "s_nop 1",
+                      f"buffer_store_dword {vp(VM[qb])}, {vp(T + 3)}, {sp(S_RL, 4)}, 0 offen")
+        self.emit("s_waitcnt vmcnt(0)")
 
     # ---------------------------------------------------------------- tile loop
     def prologue(self, b):
@@ -682,6 +1029,7 @@ class Gen:
         self.write_state(True, 1)
         self.emit(f"s_branch .Lsnap_done{u}", f".Lsnap_slot{u}:")
         self.write_state(False, 1)
+        self.publish(1)
         self.emit(f".Lsnap_done{u}:",
                   f"s_mov_b32 {sp(S_FL)}, {sp(S_TB)}",
                   f"s_branch .Lpro{nb}")
@@ -833,17 +1181,26 @@ class Gen:
                   f"s_cmp_eq_u32 {sp(S_TB)}, {sp(A_T)}", "s_cbranch_scc0 .Lpe_slot")
         self.write_state(True, 0)
         self.emit("s_branch .Lpe_local", ".Lpe_slot:")
-        self.write_state(False, 0)
+        self.finish_stream(0)
         self.label(".Lpe_local")
         # a piece that ends inside (or at the end of) the local set also holds
         # its local result
-        self.emit(f"s_cmp_eq_u32 {sp(A_DUAL)}, 0", "s_cbranch_scc1 .Lnext_item",
-                  f"s_cmp_le_i32 {sp(S_TB)}, {sp(A_LT)}", "s_cbranch_scc0 .Lnext_item",
+        self.emit(f"s_cmp_eq_u32 {sp(A_DUAL)}, 0", "s_cbranch_scc1 .Lmerges",
+                  f"s_cmp_le_i32 {sp(S_TB)}, {sp(A_LT)}", "s_cbranch_scc0 .Lmerges",
                   f"s_cmp_eq_u32 {sp(S_TA)}, 0", "s_cbranch_scc0 .Lpl_slot",
                   f"s_cmp_eq_u32 {sp(S_TB)}, {sp(A_LT)}", "s_cbranch_scc0 .Lpl_slot")
         self.write_state(True, 1)
-        self.emit("s_branch .Lnext_item", ".Lpl_slot:")
-        self.write_state(False, 1)
+        self.emit("s_branch .Lmerges", ".Lpl_slot:")
+        self.finish_stream(1)
+        # the streams this piece completes (one of them may have been counted at
+        # the local snapshot inside the piece)
+        self.label(".Lmerges")
+        for which in range(2):
+            self.emit(f"s_and_b32 {sp(S_X)}, {sp(S_MFLAG)}, {1 << which}",
+                      f"s_cbranch_scc0 .Lmerged{which}")
+            self.merge(which)
+            self.label(f".Lmerged{which}")
+        self.emit(f"s_mov_b32 {sp(S_MFLAG)}, 0")
         self.label(".Lnext_item")
         self.emit(f"s_sub_i32 {sp(S_ITEM)}, {sp(S_ITEM)}, 1",
                   f"s_cmp_ge_i32 {sp(S_ITEM)}, {sp(S_IFIRST)}",
@@ -858,6 +1215,7 @@ class Gen:
                   "s_nop 1",
                   f"v_readfirstlane_b32 {sp(S_WAVE)}, {vp(V_T)}",
                   "s_waitcnt lgkmcnt(0)",
+                  f"s_mov_b32 {sp(S_MFLAG)}, 0",
                   f"s_lshl_b32 {sp(S_WAVE4K)}, {sp(S_WAVE)}, 12",
                   # staging constants: records = nv * 2 ld + 256 - 2 ld, 64 rows = 128 ld bytes,
                   # the resources' format words

@@ -183,9 +183,9 @@ int ispa_attn_chunk_ws(const void* q, const void* k_cache, const void* v_cache, 
   const size_t need = ispa::attn_plan_split(a, head_dim, segments, &a.split);
   if (a.split.n_seg > 0) {
     if (!workspace || ((uintptr_t)workspace & 255u) || workspace_bytes < need) return ISPA_ERR_INVALID_ARG;
-    const size_t slots = (size_t)a.split.n_seg * a.split.max_pieces * 2 * ispa::kAttnBq;
     a.split.part_o = (float*)workspace;
-    a.split.part_lse = (float*)((char*)workspace + round_up(slots * head_dim * 4, 256));
+    a.split.part_lse = (float*)((char*)workspace + a.split.lse_offset);
+    a.split.ctr = (uint32_t*)((char*)workspace + a.split.ctr_offset);
   }
   return ispa::launch_attn_chunk(a, head_dim, stream) == hipSuccess ? ISPA_OK : ISPA_ERR_HIP;
 }

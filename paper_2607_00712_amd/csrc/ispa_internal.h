@@ -44,6 +44,11 @@ struct AttnSplit {
   int32_t max_pieces;  // partial slots per segment
   float* part_o;       // [G * max_pieces][2][kAttnBq][head_dim]: [.][0] end state, [.][1] local set
   float* part_lse;     // [G * max_pieces][2][kAttnBq]
+  // counters [work item][2 streams][4 waves] of the split fold (the assembly
+  // kernel's pieces complete their work items themselves); null: the merge
+  // kernel completes them after the launch
+  uint32_t* ctr;
+  size_t lse_offset, ctr_offset;  // byte offsets of part_lse and ctr in the workspace
 };
 constexpr int kAttnBq = 256;  // queries per work item
 

@@ -80,6 +80,9 @@ V_EOFF = (96, 112)              # 16 each: epilogue voffsets of the elements of 
 N_VGPR = 128
 N_AGPR = 256
 
+GROUP = 4                       # row panels per group of the work order
+EARLY = 4                       # phase 1 issues 1 / EARLY of its MFMAs before the wait for the next stage
+
 REGION_B = 65536
 STAGE_BYTES = 16384             # one region's share of a stage: 256 rows x 64 bytes
 LDS_BYTES = 131072
@@ -121,24 +124,24 @@ class Gen:
 
     # ---------------------------------------------------------------- setup
     def decode_tile(self):
-        """S_ITEM -> (S_TI, S_TJ): row panels four at a time (the last group
+        """S_ITEM -> (S_TI, S_TJ): row panels GROUP at a time (the last group
         may hold fewer), within a group column by column."""
         k, gm, r0, t = S_K, S_GM, S_R0, S_T
         self.emit(f"s_mov_b32 {sp(k)}, {sp(S_ITEM)}", f"s_mov_b32 {sp(r0)}, 0",
-                  f"s_lshl_b32 {sp(t)}, {sp(A_TN)}, 2",                      # items of a full group
+                  f"s_mul_i32 {sp(t)}, {sp(A_TN)}, {GROUP}",                 # items of a full group
                   self.L("grp") + ":",
                   f"s_sub_i32 {sp(gm)}, {sp(A_TM)}, {sp(r0)}",
-                  f"s_cmp_lt_i32 {sp(gm)}, 4",
+                  f"s_cmp_lt_i32 {sp(gm)}, {GROUP}",
                   f"s_cbranch_scc1 {self.L('grp_last')}",
                   f"s_cmp_lt_i32 {sp(k)}, {sp(t)}",
                   f"s_cbranch_scc1 {self.L('grp_full')}",
                   f"s_sub_i32 {sp(k)}, {sp(k)}, {sp(t)}",
-                  f"s_add_i32 {sp(r0)}, {sp(r0)}, 4",
+                  f"s_add_i32 {sp(r0)}, {sp(r0)}, {GROUP}",
                   f"s_branch {self.L('grp')}",
                   self.L("grp_full") + ":",
-                  f"s_mov_b32 {sp(gm)}, 4",
+                  f"s_mov_b32 {sp(gm)}, {GROUP}",
                   self.L("grp_last") + ":",
-                  # tj = k / gm, ti = r0 + k % gm (gm <= 4: by subtraction)
+                  # tj = k / gm, ti = r0 + k % gm (gm <= GROUP: by subtraction)
                   f"s_mov_b32 {sp(S_TJ)}, 0",
                   self.L("dm") + ":",
                   f"s_cmp_lt_i32 {sp(k)}, {sp(gm)}",
@@ -283,7 +286,7 @@ class Gen:
             self.interleave(self.mfmas(X, nbj), other, start=1)
             # phase 1: k half 1 (set Y) | wait for stage s + 1 | reads of its half 0 (set X)
             m = self.mfmas(Y, nbj)
-            first = len(m) // 4
+            first = len(m) // EARLY
             self.emit("s_waitcnt lgkmcnt(0)")
             for i in m[:first]:
                 self.emit(i)

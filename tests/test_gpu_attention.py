@@ -126,6 +126,16 @@ def test_split_parity(case):
     run_and_check(n_q, N, w, s, H, d, dual, wid=12, segments=seg)
 
 
+@pytest.mark.parametrize("merge_kernel", ["0", "1"])
+def test_split_completion_paths(merge_kernel, monkeypatch):
+    # head_dim 128 completes split work items inside the attention kernel (the
+    # last piece of an item merges, its own part from registers when the item
+    # has two pieces); ISPA_ATTN_MERGE_KERNEL=1 leaves them to the merge kernel
+    monkeypatch.setenv("ISPA_ATTN_MERGE_KERNEL", merge_kernel)
+    run_and_check(300, 1000, 200, 0, 2, 128, True, wid=14, segments=5)     # two and three pieces per item
+    run_and_check(700, 2600, 900, 0, 3, 128, True, wid=15, segments=16)   # local set split inside pieces
+
+
 def test_split_matches_unsplit_and_is_deterministic():
     q, k, v = synth.chunk_qkv(13, 0, 0, 500, 2200, 256, DEV)
     ref = ispa.attn_chunk(q, k, v, 2200, 700, 2, sink_len=5, dual=True, segments=-1)
