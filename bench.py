@@ -60,14 +60,14 @@ PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA
 PEAK_FP32_TFLOPS = 157.3   # MI355X fp32 matrix / vector (published)
 PEAK_HBM_GBS = 8000.0
 
-# HBM bytes of one dual-stream attention call (the attention kernel plus the
-# merge of its split work items), from rocprofv3 FETCH_SIZE and WRITE_SIZE
+# HBM bytes of one dual-stream attention call (the attention kernel, which
+# completes its split work items itself), from rocprofv3 FETCH_SIZE and WRITE_SIZE
 # scaled by the plain-copy calibration (profiles/attn_fast_wan13b_dual.md,
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "36c703f9f2649746", "bytes_per_launch": 755.8e6},
-    "14b": {"attn_chunk_sha256_16": "36c703f9f2649746", "bytes_per_launch": 3059.8e6},
+    "1.3b": {"attn_chunk_sha256_16": "42b7243b33953803", "bytes_per_launch": 650.8e6},
+    "14b": {"attn_chunk_sha256_16": "42b7243b33953803", "bytes_per_launch": 3059.9e6},
 }
 
 
@@ -741,14 +741,16 @@ def main():
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
-            "kernel": "ispa_attn_fast_d128 + attn_merge_split_kernel<128> (F-Layer, dual stream; one call)",
+            "kernel": "ispa_attn_fast_d128 (F-Layer, dual stream; one call: the counters' fill kernel and the "
+                      "attention kernel, which completes its split work items)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE of both kernels, copy-calibrated)",
+            "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE of the attention kernel, "
+                            "copy-calibrated)",
         },
         "breakdown": {
             "attn_dual_ms": round(avg["attn_dual"], 4),
