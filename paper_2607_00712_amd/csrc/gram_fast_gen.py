@@ -28,7 +28,11 @@ time: the group's G tiles column by column, then its C tiles), cut into one
 contiguous range per XCD, so the workgroups resident on an XCD stream few
 distinct panels through its L2. The epilogue adds each block to G or C with
 one read-modify-write per element (no atomics: every element is written by
-one workgroup, in a fixed order).
+one workgroup, in a fixed order). Tiles that would leave a round of the chip
+mostly idle (the last round, or all of them when there are fewer tiles than
+compute units) are cut into 2^k row pieces: piece 0 adds into G or C, the
+others store their sums to workspace slots that a fixed-order add applies
+after the launch.
 
 Run as a script it prints the assembly; build.py assembles it.
 """
@@ -40,7 +44,7 @@ ARGS_BYTES = 96
 ARG_X, ARG_R, ARG_G, ARG_C = 0, 8, 16, 24
 ARG_ROWS, ARG_LDX, ARG_LDR, ARG_LDG, ARG_LDC = 32, 36, 40, 44, 48
 ARG_TIN, ARG_TOUT, ARG_NT, ARG_PERXCD, ARG_STEPS = 52, 56, 60, 64, 68
-ARG_NWHOLE, ARG_PERXCDH, ARG_SPLIT, ARG_WS = 72, 76, 80, 88
+ARG_NWHOLE, ARG_PERXCDH, ARG_SPLIT, ARG_LOGS, ARG_WS = 72, 76, 80, 84, 88
 
 S_ARG = 8                       # s[8:31]
 
@@ -52,7 +56,7 @@ def arg(off):
 A_X, A_R, A_G, A_C = arg(ARG_X), arg(ARG_R), arg(ARG_G), arg(ARG_C)
 A_ROWS, A_LDX, A_LDR, A_LDG, A_LDC = (arg(o) for o in (ARG_ROWS, ARG_LDX, ARG_LDR, ARG_LDG, ARG_LDC))
 A_TIN, A_TOUT, A_NT, A_PERXCD, A_STEPS = (arg(o) for o in (ARG_TIN, ARG_TOUT, ARG_NT, ARG_PERXCD, ARG_STEPS))
-A_NWHOLE, A_PERXCDH, A_SPLIT, A_WS = (arg(o) for o in (ARG_NWHOLE, ARG_PERXCDH, ARG_SPLIT, ARG_WS))
+A_NWHOLE, A_PERXCDH, A_SPLIT, A_LOGS, A_WS = (arg(o) for o in (ARG_NWHOLE, ARG_PERXCDH, ARG_SPLIT, ARG_LOGS, ARG_WS))
 
 # SGPRs
 S_RA = (32, 36)                 # resources of region A halves 0 / 1
@@ -65,7 +69,7 @@ S_WAVE, S_W2K = 59, 60          # wave, wave * 2048
 S_ITEM, S_TI, S_TJ, S_ISG = 61, 62, 63, 64
 S_K, S_R0, S_GM, S_NG, S_N, S_T = 65, 66, 67, 68, 69, 70
 S_STEP, S_BUDGET = 71, 72
-S_PIECE, S_NSTEPS, S_RB0, S_RE = 96, 97, 98, 99   # piece (-1 whole, 0, 1), its stages, first / end row
+S_PIECE, S_NSTEPS, S_RB0, S_RE = 96, 97, 98, 99   # piece (-1 whole, 0 ..), its stages, first / end row
 S_X, S_Y, S_Z = 73, 74, 75
 S_OUT = 76                      # 4: output resource
 S_EO = 80                       # 16: epilogue row offsets (bytes) of accumulator element r
@@ -347,8 +351,8 @@ class Gen:
     # ---------------------------------------------------------------- epilogue
     def epilogue(self):
         """out[rows of this wave's quarter][cols] += the accumulators; the
-        second half of a split tile writes its sums to its workspace slot
-        instead (a fixed-order add follows the launch)."""
+        later row pieces of a split tile write their sums to their workspace
+        slots instead (a fixed-order add follows the launch)."""
         T = V_T
         self.label(".Ldone")
         # every MFMA has completed before the accumulation registers are read
@@ -356,7 +360,7 @@ class Gen:
         # output: G or C from the tile's first element (row 256 ti, column 256 tj),
         # or workspace slot (tile - n_whole) of 256 x 256 fp32 (row bytes 1024)
         u = self.new_uid()
-        self.emit(f"s_cmp_eq_u32 {sp(S_PIECE)}, 1",
+        self.emit(f"s_cmp_gt_i32 {sp(S_PIECE)}, 0",
                   f"s_cbranch_scc1 .Lout_ws{u}",
                   f"s_cmp_eq_u32 {sp(S_ISG)}, 0",
                   f"s_cbranch_scc1 .Lout_c{u}",
@@ -377,7 +381,12 @@ class Gen:
                   f"s_addc_u32 {sp(S_OUT + 1)}, {sp(S_OUT + 1)}, 0",
                   f"s_branch .Lout_ok{u}",
                   f".Lout_ws{u}:",
-                  f"s_sub_u32 {sp(S_X)}, {sp(S_ITEM)}, {sp(A_NWHOLE)}",
+                  # slot (piece - 1) * split tiles + (tile - n_whole)
+                  f"s_sub_u32 {sp(S_X)}, {sp(A_NT)}, {sp(A_NWHOLE)}",
+                  f"s_sub_u32 {sp(S_Y)}, {sp(S_PIECE)}, 1",
+                  f"s_mul_i32 {sp(S_X)}, {sp(S_X)}, {sp(S_Y)}",
+                  f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_ITEM)}",
+                  f"s_sub_u32 {sp(S_X)}, {sp(S_X)}, {sp(A_NWHOLE)}",
                   f"s_lshr_b32 {sp(S_Y)}, {sp(S_X)}, 14",
                   f"s_lshl_b32 {sp(S_X)}, {sp(S_X)}, 18",                    # 256 KB per slot
                   f"s_add_u32 {sp(S_OUT)}, {sp(A_WS)}, {sp(S_X)}",
@@ -428,7 +437,7 @@ class Gen:
             return [f"buffer_store_dword {vp(src + r)}, {vp(VO[k & 1])}, {sp(S_OUT, 4)}, {sp(S_EO + r)} offen"
                     for r in range(16)]
 
-        self.emit(f"s_cmp_eq_u32 {sp(S_PIECE)}, 1", f"s_cbranch_scc1 .Lstore_ws{u}")
+        self.emit(f"s_cmp_gt_i32 {sp(S_PIECE)}, 0", f"s_cbranch_scc1 .Lstore_ws{u}")
         self.emit(*voff(0), *loads(0))
         for k in range(16):
             acc = 16 * (4 * blocks[k][0] + blocks[k][1])
@@ -442,7 +451,7 @@ class Gen:
                           f"v_add_f32_e32 {vp(VB[k & 1] + r)}, {vp(VB[k & 1] + r)}, {vp(T + 3)}")
             self.emit(*stores(k, VB[k & 1]))
         self.emit("s_branch .Lstored")
-        # the second half of a split tile: plain stores of the sums
+        # the later row pieces of a split tile: plain stores of the sums
         self.label(f".Lstore_ws{u}")
         for k in range(16):
             acc = 16 * (4 * blocks[k][0] + blocks[k][1])
@@ -471,8 +480,9 @@ class Gen:
                   # XCD-aware work: XCD x (workgroups are dealt round robin) takes
                   # whole tiles x per_xcd .. x per_xcd + per_xcd - 1 (tiles below
                   # n_whole), then pieces x per_xcd_h .. of the tiles from n_whole
-                  # on, each cut into two row halves (piece p: tile n_whole + p / 2,
-                  # half p % 2), so that the last round of a launch is not mostly idle
+                  # on, each cut into 2^log_pieces row pieces (piece p: tile
+                  # n_whole + p >> log_pieces, rows p mod 2^log_pieces), so that the
+                  # last round of a launch is not mostly idle
                   f"s_and_b32 {sp(S_X)}, s2, 7",
                   f"s_lshr_b32 {sp(S_Y)}, s2, 3",
                   f"s_mov_b32 {sp(S_PIECE)}, -1",
@@ -488,28 +498,29 @@ class Gen:
                   f"s_mul_i32 {sp(S_Z)}, {sp(S_X)}, {sp(A_PERXCDH)}",
                   f"s_add_u32 {sp(S_Z)}, {sp(S_Z)}, {sp(S_Y)}",                  # piece index p
                   f"s_sub_u32 {sp(S_X)}, {sp(A_NT)}, {sp(A_NWHOLE)}",
-                  f"s_lshl_b32 {sp(S_X)}, {sp(S_X)}, 1",
+                  f"s_lshl_b32 {sp(S_X)}, {sp(S_X)}, {sp(A_LOGS)}",
                   f"s_cmp_ge_u32 {sp(S_Z)}, {sp(S_X)}",
                   "s_cbranch_scc1 .Lend",
-                  f"s_and_b32 {sp(S_PIECE)}, {sp(S_Z)}, 1",
-                  f"s_lshr_b32 {sp(S_Z)}, {sp(S_Z)}, 1",
+                  f"s_lshl_b32 {sp(S_T)}, 1, {sp(A_LOGS)}",
+                  f"s_sub_u32 {sp(S_T)}, {sp(S_T)}, 1",
+                  f"s_and_b32 {sp(S_PIECE)}, {sp(S_Z)}, {sp(S_T)}",
+                  f"s_lshr_b32 {sp(S_Z)}, {sp(S_Z)}, {sp(A_LOGS)}",
                   f"s_add_u32 {sp(S_ITEM)}, {sp(A_NWHOLE)}, {sp(S_Z)}",
                   ".Litem_ok:",
-                  # rows of this work item: all, the first split_steps stages, or the rest
+                  # rows of this work item: all, or the split stages of piece q from
+                  # stage q split on
                   f"s_mov_b32 {sp(S_RB0)}, 0",
                   f"s_mov_b32 {sp(S_RE)}, {sp(A_ROWS)}",
                   f"s_mov_b32 {sp(S_NSTEPS)}, {sp(A_STEPS)}",
                   f"s_cmp_lt_i32 {sp(S_PIECE)}, 0",
                   "s_cbranch_scc1 .Lrows_ok",
-                  f"s_lshl_b32 {sp(S_X)}, {sp(A_SPLIT)}, 5",                    # split row
-                  f"s_cmp_eq_u32 {sp(S_PIECE)}, 0",
-                  "s_cbranch_scc0 .Lsecond_half",
+                  f"s_mul_i32 {sp(S_X)}, {sp(A_SPLIT)}, {sp(S_PIECE)}",         # first stage
+                  f"s_sub_i32 {sp(S_NSTEPS)}, {sp(A_STEPS)}, {sp(S_X)}",
+                  f"s_min_i32 {sp(S_NSTEPS)}, {sp(S_NSTEPS)}, {sp(A_SPLIT)}",
+                  f"s_lshl_b32 {sp(S_RB0)}, {sp(S_X)}, 5",
+                  f"s_lshl_b32 {sp(S_X)}, {sp(A_SPLIT)}, 5",
+                  f"s_add_u32 {sp(S_X)}, {sp(S_X)}, {sp(S_RB0)}",
                   f"s_min_i32 {sp(S_RE)}, {sp(S_RE)}, {sp(S_X)}",
-                  f"s_mov_b32 {sp(S_NSTEPS)}, {sp(A_SPLIT)}",
-                  "s_branch .Lrows_ok",
-                  ".Lsecond_half:",
-                  f"s_mov_b32 {sp(S_RB0)}, {sp(S_X)}",
-                  f"s_sub_i32 {sp(S_NSTEPS)}, {sp(A_STEPS)}, {sp(A_SPLIT)}",
                   ".Lrows_ok:")
         self.decode_tile()
         # side A: X columns 256 ti .. (bytes 512 ti); side B: X (G tile) or R (C tile) columns 256 tj ..

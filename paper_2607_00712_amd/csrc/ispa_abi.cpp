@@ -43,6 +43,12 @@ bool layout_of(int32_t d_in, int32_t d_out, int64_t max_rows, Layout* out) {
   l.L = off; off = round_up(off + (size_t)d_in * d_in * 4, kWsAlign);
   l.W = off; off = round_up(off + (size_t)d_in * d_out * 4, kWsAlign);
   l.Dinv = off; off = round_up(off + ispa::solve_dinv_bytes(d_in), kWsAlign);
+  // L, W and Dinv are free between solves: with the room after them they hold
+  // the Gram kernel's row pieces (the sums it adds in a second pass)
+  {
+    const size_t need = ispa::gram_fast_scratch_bytes(d_in, d_out);
+    if (need > off - l.L) off = round_up(l.L + need, kWsAlign);
+  }
   l.X = off; off = round_up(off + (size_t)max_rows * d_in * 2, kWsAlign);
   l.R = off; off = round_up(off + (size_t)max_rows * d_out * 2, kWsAlign);
   l.scalars = off; off = round_up(off + 4 * sizeof(double), kWsAlign);
@@ -365,10 +371,10 @@ int ispa_accum_stats(ispa_stats* h, const void* x, int32_t x_dtype, const void* 
                                  h->stream) != hipSuccess)
       return ISPA_ERR_HIP;
     const uint16_t* xg = x_dtype == ISPA_DTYPE_BF16 ? (const uint16_t*)xp : xb;
-    // the solve's right-hand-side area is free between solves: scratch for the Gram
+    // the solve's areas (L to X) are free between solves: scratch for the Gram
     if (ispa::launch_gram(xg, rb, rows, h->d_in, h->d_out, G, C, sqp,
-                          ispa::discrepancy_grid(rows, h->d_in, h->d_out), sq, (float*)(h->ws + h->lay.W),
-                          (size_t)h->d_in * h->d_out * sizeof(float), h->stream) != hipSuccess)
+                          ispa::discrepancy_grid(rows, h->d_in, h->d_out), sq, (float*)(h->ws + h->lay.L),
+                          h->lay.X - h->lay.L, h->stream) != hipSuccess)
       return ISPA_ERR_HIP;
   }
   h->n_rows += n_rows;

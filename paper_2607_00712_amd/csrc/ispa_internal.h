@@ -109,13 +109,17 @@ hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d
                        float* scratch, size_t scratch_bytes, hipStream_t stream);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
 // the hand-scheduled Gram kernel (gram_fast.cpp): widths that are multiples of
-// 256 with at least kGramSplitTiles tiles of 256 x 256
-bool gram_fast_eligible(int64_t rows, int d_in, int d_out);
-// (scratch: room for the sums of split tiles' second halves; n_whole / n_split:
-// the tiles computed whole and split, for the fixed-order add that follows)
+// 256; tiles computed whole (n_whole) or as 2^log_pieces row pieces of `split`
+// stages (n_split tiles), the later pieces' sums in (2^log_pieces - 1) x n_split
+// scratch slots of 256 x 256 fp32 that gram_fixup adds after the launch
+struct GramFastPlan {
+  int log_pieces, n_whole, n_split, split;
+};
+bool gram_fast_plan(int64_t rows, int d_in, int d_out, size_t scratch_bytes, GramFastPlan* plan);
+// scratch that gram_fast_plan may ask for at these widths on this device
+size_t gram_fast_scratch_bytes(int d_in, int d_out);
 hipError_t launch_gram_fast(const uint16_t* x, const uint16_t* r, int64_t rows, int d_in, int d_out, float* G,
-                            float* C, float* scratch, size_t scratch_bytes, int* n_whole, int* n_split,
-                            hipStream_t stream);
+                            float* C, float* scratch, const GramFastPlan& plan, hipStream_t stream);
 
 // ---- absorption (absorb.hip) ----
 // W += dW (transposed: W[j][i] += dW[i][j]); dtype 0 bf16, 1 fp32

@@ -359,12 +359,17 @@ __device__ void add_sq_parts(const GramArgs& a) {
 // The same on its own, beside the hand-scheduled Gram kernel (one wave).
 __global__ __launch_bounds__(64) void sq_norm_kernel(GramArgs a) { add_sq_parts(a); }
 
-// After a hand-scheduled Gram launch that split its last tiles into row
-// halves: tile n_whole + q (256 x 256, the panel-group order) += the second
-// half's sums in scratch slot q; the first half has already added its own, so
-// every element is summed in a fixed order. 64 workgroups per tile, 4 rows each.
-__global__ __launch_bounds__(256) void gram_fixup_kernel(float* G, float* C, const float* ws, int n_whole,
-                                                         int tiles_in, int tiles_out, int d_in, int d_out) {
+// After a hand-scheduled Gram launch that split tiles into row pieces: tile
+// n_whole + q (256 x 256, the panel-group order) += the sums of pieces 1 ..
+// pieces - 1 in scratch slots (piece - 1) n_split + q, in piece order; piece 0
+// has already added its own, so every element is summed in a fixed order. 64
+// workgroups per tile, 4 rows each; the first wave of the first one also adds
+// the norm partials (as sq_norm_kernel does without a fixup).
+__global__ __launch_bounds__(256) void gram_fixup_kernel(GramArgs a, const float* ws, int n_whole, int n_split,
+                                                         int pieces, int tiles_in, int tiles_out) {
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < 64) add_sq_parts(a);
+  float *G = a.G, *C = a.C;
+  const int d_in = a.d_in, d_out = a.d_out;
   const int q = blockIdx.y;
   int ti, tj;
   const bool is_g = gram_tile_of(n_whole + q, tiles_in, tiles_out, ti, tj);
@@ -372,8 +377,10 @@ __global__ __launch_bounds__(256) void gram_fixup_kernel(float* G, float* C, con
   const int ld = is_g ? d_in : d_out;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), col = (threadIdx.x & 63) * 4;
   f32x4* o = (f32x4*)(out + (int64_t)(256 * ti + row) * ld + 256 * tj + col);
-  const f32x4 w = *(const f32x4*)(ws + (int64_t)q * 65536 + row * 256 + col);
-  *o = *o + w;
+  // the pieces after the first, in piece order (slot (piece - 1) n_split + q)
+  f32x4 v = *o;
+  for (int p = 1; p < pieces; ++p) v = v + *(const f32x4*)(ws + ((int64_t)(p - 1) * n_split + q) * 65536 + row * 256 + col);
+  *o = v;
 }
 
 // SPLIT = 2: 16 waves, waves 8..15 take the second half of the rows with
@@ -540,15 +547,16 @@ hipError_t launch_gram(const uint16_t* x, const uint16_t* r, int64_t rows, int d
   a.sq_part = sq_part;
   a.n_sq_part = n_sq_part;
   a.sq_norm = sq_norm;
-  if (gram_fast_eligible(rows, d_in, d_out)) {
-    hipLaunchKernelGGL(sq_norm_kernel, dim3(1), dim3(64), 0, stream, a);
-    hipError_t e = hipGetLastError();
+  GramFastPlan plan;
+  if (gram_fast_plan(rows, d_in, d_out, scratch != nullptr ? scratch_bytes : 0, &plan)) {
+    hipError_t e = launch_gram_fast(x, r, rows, d_in, d_out, G, C, scratch, plan, stream);
     if (e != hipSuccess) return e;
-    int n_whole = 0, n_split = 0;
-    e = launch_gram_fast(x, r, rows, d_in, d_out, G, C, scratch, scratch_bytes, &n_whole, &n_split, stream);
-    if (e != hipSuccess || n_split == 0) return e;
-    hipLaunchKernelGGL(gram_fixup_kernel, dim3(64, n_split), dim3(256), 0, stream, G, C, scratch, n_whole,
-                       d_in / 256, d_out / 256, d_in, d_out);
+    if (plan.n_split == 0) {
+      hipLaunchKernelGGL(sq_norm_kernel, dim3(1), dim3(64), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(gram_fixup_kernel, dim3(64, plan.n_split), dim3(256), 0, stream, a, scratch, plan.n_whole,
+                         plan.n_split, 1 << plan.log_pieces, d_in / 256, d_out / 256);
+    }
     return hipGetLastError();
   }
   a.tiles_in = (d_in + kG2T - 1) / kG2T;

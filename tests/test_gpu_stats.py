@@ -137,14 +137,17 @@ def test_warmup_bitwise_reproducible():
 
 
 @pytest.mark.parametrize("d_in,d_out,chunks", [(5120, 2560, (777, 1, 64)), (4096, 4096, (1000,)),
-                                                (5120, 5120, (777, 33))])
+                                                (5120, 5120, (777, 33)), (1536, 1536, (4680, 100)),
+                                                (1024, 512, (777, 300, 5))])
 def test_gram_256_tiles(d_in, d_out, chunks):
-    """Widths that are multiples of 256 with enough 256 x 256 tiles to fill the
-    chip take the hand-scheduled Gram kernel: G and C against the oracle over
-    ragged chunks (a last 32-row stage part empty, a one-row chunk), and a
-    second run bitwise equal to the first. At 5120 x 5120 (610 tiles on 256
-    compute units) the last 98 tiles are computed as two row halves each (a
-    33-row chunk: halves of one row stage each)."""
+    """Widths that are multiples of 256 take the hand-scheduled Gram kernel: G
+    and C against the oracle over ragged chunks (a last 32-row stage part
+    empty, a one-row chunk), and a second run bitwise equal to the first. At
+    5120 x 5120 (610 tiles on 256 compute units) the last 98 tiles are
+    computed as two row pieces each (a 33-row chunk: pieces of one row stage
+    each). With fewer tiles than compute units (1536: 57 tiles; 1024 x 512: 18)
+    every tile is cut into 4 or 8 row pieces, added in piece order after the
+    launch; chunks too short for pieces of 4 stages take the C++ kernel."""
     print(f"[stats] 256-tile Gram {d_in} x {d_out}, chunks {chunks}", flush=True)
     blocks = [rand_block(26, i, r, d_in, d_out, torch.bfloat16, torch.float32) for i, r in enumerate(chunks)]
     runs = []
