@@ -35,6 +35,7 @@
 #include "ispa_internal.h"
 
 #include <math.h>
+#include <stdlib.h>
 
 namespace ispa {
 namespace {
@@ -1107,6 +1108,18 @@ hipError_t launch_gemm(const GemmArgs& g, int layers, hipStream_t stream) {
 
 }  // namespace
 
+// Panels of a single layer's factorisation whose trailing updates are
+// deferred to super-panels (a multiple of kSup): the first quarter from 48
+// panels on, none below (measured at 80 panels: 5.11 ms without, 5.00 ms
+// with 16 to 40 deferred, 5.10 with 60; at 24 panels every deferral is
+// slower, 0.645 -> 0.69 ms and more). ISPA_SOLVE_DEFER_PANELS overrides.
+static int solve_defer_panels(int nblk) {
+  const char* env = getenv("ISPA_SOLVE_DEFER_PANELS");
+  int c = env != nullptr ? atoi(env) : (nblk >= 48 ? nblk / 4 : 0);
+  if (c < 0) c = 0;
+  return c / kSup * kSup;
+}
+
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda, float* delta_w,
                         const SolveWork& w, hipStream_t stream) {
   const int nblk = (d + kNb - 1) / kNb;
@@ -1125,21 +1138,24 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     if (grid > 8192) grid = 8192;
     hipLaunchKernelGGL(solve_init_kernel, dim3(grid, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
   }
-  // With several layers, panels are grouped kSup at a time: launch k applies
-  // panel k only to the columns of its own super-panel; the rest of the
-  // trailing triangle receives the super-panel's panels together, in one
-  // launch that keeps each block in registers across them, once its last
-  // panel is factored (a quarter of the trailing-matrix traffic of applying
-  // each panel everywhere; the same arithmetic in the same order). A single
-  // layer's factorisation is a chain of launches bound by their latency, to
-  // which the extra launch per super-panel would add: it applies every panel
-  // everywhere at once.
-  const int sup = nl > 1 ? kSup : nblk + 1;
+  // Panels are grouped kSup at a time (super-panels) up to column c_def:
+  // launch k applies panel k only to the columns of its own super-panel; the
+  // rest of the trailing triangle receives the super-panel's panels together,
+  // in one launch that keeps each block in registers across them, once its
+  // last panel is factored (a quarter of the trailing-matrix traffic of
+  // applying each panel everywhere; the same arithmetic in the same order).
+  // With several layers every panel is deferred. A single layer's
+  // factorisation is a chain of launches bound by their latency, to which the
+  // extra launch per super-panel adds: it defers only the first panels, whose
+  // trailing updates are large enough to bound their launches, and applies
+  // every later panel everywhere at once.
+  const int sup = kSup;
+  const int c_def = nl > 1 ? nblk + sup : solve_defer_panels(nblk);
   for (int k = -1; k <= nblk - 2; ++k) {
     const int c = k + 1;                          // the panel column this launch factors
     int apply = k >= 0 ? 1 : 0;
     int t_end;
-    if (sup > nblk) {
+    if (c > c_def) {
       t_end = nblk;
     } else if (c % sup == 0) {
       if (c > 0) {
