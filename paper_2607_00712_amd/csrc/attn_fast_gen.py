@@ -15,8 +15,9 @@ softmax, interleaved instruction by instruction.
 Work decomposition, tile enumeration, LDS swizzles, the online softmax with a
 lazy reference (exp2 with the scale folded in, O normalised by the sum of the
 bf16-rounded weights, the LSE from the fp32 sum) and the partial-result layout
-of the split are those of the C++ kernel in attn_chunk.hip; the merge kernel
-there combines the partial results of either.
+of the split are those of the C++ kernel in attn_chunk.hip. Given counters,
+this kernel completes its split work items itself (the split fold below);
+without them the merge kernel there combines the partial results.
 
 Run as a script it prints the assembly; build.py assembles it into a code
 object that the library embeds and loads per device.
