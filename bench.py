@@ -315,6 +315,42 @@ def absorb_run(ispa, w, k, v, dw, dev, reps=10):
             "project_w8a8_frac": round(pj_flop / pj8 / 1e9 / PEAK_INT8_TOPS, 4)}
 
 
+def project_run(w, steps, warmup):
+    """The chunk's output projection alone (`--only project`, for profiling):
+    A [n_q, D] W^T with random bf16 operands, then its W8A8 form on the codes
+    of the same operands; mean of `steps` calls each after `warmup`."""
+    import paper_2607_00712_amd as ispa
+    dev = torch.device("cuda", 0)
+    D, n = w["heads"] * w["head_dim"], w["n_q"]
+    g = torch.Generator(device=dev).manual_seed(11)
+    a = torch.randn((n, D), device=dev, generator=g).to(torch.bfloat16)
+    weight = (torch.randn((D, D), device=dev, generator=g) / D ** 0.5).to(torch.bfloat16)
+    y = torch.empty((n, D), dtype=torch.bfloat16, device=dev)
+    qa, sa = ispa.quantize_rows(a)
+    qw, sw = ispa.quantize_rows(weight)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    pj = timed(lambda: ispa.project(a, weight, out=y))
+    pj8 = timed(lambda: ispa.project_w8a8(qa, sa, qw, sw, out=y))
+    fl = 2.0 * n * D * D
+    return {"only": "project", "workload": w["name"], "shape": [n, D, D],
+            "project_ms": round(pj, 4), "project_tflops": round(fl / pj / 1e9, 1),
+            "project_frac": round(fl / pj / 1e9 / PEAK_BF16_TFLOPS, 4),
+            "project_w8a8_ms": round(pj8, 4), "project_w8a8_tops": round(fl / pj8 / 1e9, 1),
+            "project_w8a8_frac": round(fl / pj8 / 1e9 / PEAK_INT8_TOPS, 4)}
+
+
 def solve_all_run(ispa, w, stats, dev, reps=3):
     """The end of warmup solves every layer (Sec. 3.3, the eps ranking needs
     all of them): n_layers systems of the step's size (copies of the step's
@@ -688,7 +724,7 @@ def main():
     ap.add_argument("--no-14b", action="store_true",
                     help="skip the 14B-shaped step that the default 1.3B run also times (breakdown_14b)")
     ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy",
-                                       "discrepancy", "lib_ref"],
+                                       "discrepancy", "lib_ref", "project"],
                     default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
@@ -698,6 +734,9 @@ def main():
         sys.exit(2)
     if args.only == "hbm_copy":
         print(json.dumps(hbm_copy(args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "project":
+        print(json.dumps(project_run(WORKLOADS[args.workload], args.steps, args.warmup)), flush=True)
         return
     if args.only == "lib_ref":
         print(json.dumps(lib_ref(args.steps, args.warmup)), flush=True)
