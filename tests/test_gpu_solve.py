@@ -228,6 +228,25 @@ def test_batch_solve_wan13b_size():
         assert float(eps_b[i].item()) == float(eps_1.item())
 
 
+def test_batch_matches_single_with_deferred_panels():
+    # d = 3072 (48 panels): the single-layer factorisation defers its first 12
+    # panels to super-panels and applies the later ones everywhere at once,
+    # the batch defers all of them; every panel's product is subtracted on its
+    # own in panel order either way, so dW and eps agree bit for bit
+    d, d_out, n, layers, lam = 3072, 256, 4000, 2, 1e-1
+    print("[solve] batch of 2 at 3072", flush=True)
+    sb = ispa.StatsBatch(layers, d, d_out, max_rows=n, device=DEV)
+    _fill_batch(sb, 38, n)
+    dw_b, eps_b, status_b = sb.solve(lam)
+    torch.cuda.synchronize()
+    assert status_b.tolist() == [0] * layers
+    for i in range(layers):
+        dw_1, eps_1, _ = sb.layers[i].solve_async(lam)
+        torch.cuda.synchronize()
+        assert torch.equal(dw_b[i].view(torch.int32), dw_1.view(torch.int32))
+        assert float(eps_b[i].item()) == float(eps_1.item())
+
+
 @pytest.mark.timeout(900)
 def test_14b_absorption():
     # the 14B layer's absorption: G (5120 x 5120) and C from 4 warmup chunks of
