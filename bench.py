@@ -60,14 +60,14 @@ PEAK_INT8_TOPS = 5000.0    # MI355X dense int8 MFMA
 PEAK_FP32_TFLOPS = 157.3   # MI355X fp32 matrix / vector (published)
 PEAK_HBM_GBS = 8000.0
 
-# HBM bytes of one dual-stream attention call (the attention kernel, which
-# completes its split work items itself), from rocprofv3 FETCH_SIZE and WRITE_SIZE
+# HBM bytes of one dual-stream attention call (one launch of the attention
+# kernel; neither shape splits its work items), from rocprofv3 FETCH_SIZE and WRITE_SIZE
 # scaled by the plain-copy calibration (profiles/attn_fast_wan13b_dual.md,
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "749c1f13a0c57a41", "bytes_per_launch": 650.8e6},
-    "14b": {"attn_chunk_sha256_16": "749c1f13a0c57a41", "bytes_per_launch": 3059.9e6},
+    "1.3b": {"attn_chunk_sha256_16": "5af46fc20b23db4b", "bytes_per_launch": 391.7e6},
+    "14b": {"attn_chunk_sha256_16": "5af46fc20b23db4b", "bytes_per_launch": 3059.9e6},
 }
 
 
@@ -780,8 +780,8 @@ def main():
             "accumulate": "fp32 (attention, Gram); solve fp32",
         },
         "roofline": {
-            "kernel": "ispa_attn_fast_d128 (F-Layer, dual stream; one call: the counters' fill kernel and the "
-                      "attention kernel, which completes its split work items)",
+            "kernel": "ispa_attn_fast_d128 (F-Layer, dual stream; one launch per call, whole work items: "
+                      "228 of them fill 89% of the chip, which at its power limit runs them as fast as split)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,

@@ -64,6 +64,7 @@ constexpr int kBk = 64;                // keys per tile
 constexpr int kXcds = 8;
 constexpr float kLazyLog2 = 8.f;       // rescale threshold of the softmax reference
 constexpr int kSplitMinTiles = 384;    // automatic split only from this many key tiles per item
+constexpr int kSplitFillPct = 85;      // automatic split only below this fill of the last round
 
 template <int D>
 struct Cfg {
@@ -738,12 +739,17 @@ size_t attn_plan_split(const AttnArgs& a, int head_dim, int segments, AttnSplit*
   } else {
     // whole work items per workgroup leave a fraction of the last round of
     // workgroups idle; split only when that fraction is large and the launch
-    // is long enough to repay the partial results' traffic and the merge
-    // (measured at about 40-60 us per launch on 256 CUs)
+    // is long enough to repay the partial results' traffic and the merge.
+    // The chip runs these launches at its power limit, where idle compute
+    // units let the busy ones clock higher: 228 items on 256 CUs (89% full)
+    // take as long whole as split, with 40% fewer HBM bytes; at 82% and
+    // below the split is faster (ISPA_ATTN_SPLIT_FILL overrides the percent)
     const int n_cu = attn_cu_count();
     if (n_cu <= 0 || T < kSplitMinTiles) return 0;
     const int64_t rounds = (n_work + n_cu - 1) / n_cu;
-    if (n_work * 100 >= rounds * n_cu * 92) return 0;
+    const char* fill_env = getenv("ISPA_ATTN_SPLIT_FILL");
+    const int fill_pct = fill_env != nullptr ? atoi(fill_env) : kSplitFillPct;
+    if (n_work * 100 >= rounds * n_cu * fill_pct) return 0;
     G = n_cu;
     if (U / G < 16) G = U / 16;
     if (G < 2) return 0;

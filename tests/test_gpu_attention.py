@@ -153,15 +153,16 @@ def test_split_matches_unsplit_and_is_deterministic():
         assert_lse(f64(x), f64(y), "split vs unsplit lse")
 
 
-def test_split_is_used_for_the_12_head_chunk():
-    # 12 heads x 19 query blocks = 228 work items: whole items would leave 28 of
-    # 256 compute units idle, so the automatic choice splits
+def test_automatic_split_choice():
+    # 12 heads x 19 query blocks = 228 work items fill 89% of 256 compute units:
+    # whole items (the launch is power-limited, so the idle units cost little);
+    # 10 heads = 190 items fill 74%: split over the chip
     L = ispa.lib()
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
-    nbytes = L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 12, 128, 1, 0)
-    if n_cu >= 240:
-        assert nbytes > 0
-    assert L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 12, 128, 1, -1) == 0
+    if n_cu == 256:
+        assert L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 12, 128, 1, 0) == 0
+        assert L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 10, 128, 1, 0) > 0
+    assert L.ispa_attn_workspace_bytes(32760, 9360, 0, 4680, 10, 128, 1, -1) == 0
 
 
 # the paper's literal decomposable form (Eq. 9-12): local and history branches
@@ -238,6 +239,12 @@ def test_wan13b_chunk_all_rows():
 def test_wan13b_chunk_sink_sampled():
     # the same chunk with a one-chunk sink (the paper's local set of Eq. 7)
     run_and_check(4680, 32760, 9360, 4680, 12, 128, True, wid=10, rows=BLOCK_ROWS)
+
+
+def test_wan13b_chunk_split_sampled():
+    # the same chunk split over 256 runs (the automatic choice for fills of the
+    # chip below 85%), each work item completed inside the kernel
+    run_and_check(4680, 32760, 9360, 0, 12, 128, True, wid=10, rows=BLOCK_ROWS, segments=256)
 
 
 def test_14b_chunk_sampled_heads():

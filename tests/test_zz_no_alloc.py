@@ -70,9 +70,10 @@ def _check_case(wid, n_q, N, w, sink, heads, hd, dual, expect_split, oracle_rows
 
 
 def test_noalloc_two_calls_second_smaller():
-    # the 1.3B-shaped dual-stream chunk (12 heads x 128, 4680 queries, 7 chunks
-    # of cache, window of 2 chunks): split over the chip, 129 MiB of partials
-    _check_case(10, 4680, 32760, 9360, 0, 12, 128, True, True)
+    # a 1.3B-shaped dual-stream chunk with 10 heads x 128 (4680 queries, 7
+    # chunks of cache, window of 2 chunks): 190 work items, split over the
+    # chip, 129 MiB of partials
+    _check_case(10, 4680, 32760, 9360, 0, 10, 128, True, True)
     # then a smaller split problem on the same scratch (head_dim 64, sink):
     # stale partials of the first call must not leak into it
     _check_case(12, 1000, 32760, 9360, 4680, 4, 64, True, True, oracle_rows=[0, 255, 256, 511, 999])
