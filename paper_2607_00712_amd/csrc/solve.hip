@@ -36,6 +36,9 @@
 
 #include <math.h>
 #include <stdlib.h>
+#include <string.h>
+
+#include <utility>
 
 namespace ispa {
 namespace {
@@ -342,7 +345,7 @@ __global__ void solve_init_kernel(const float* G, float* L, int n, float lambda,
 // product is subtracted on its own, in panel order, so the result is bit for
 // bit that of one launch per panel.
 template <int NP>
-__device__ void trailing_2x2(float* L, int n, int nblk, int p0, int R, int T, int t_end, Tile* tiles) {
+__device__ __forceinline__ void trailing_2x2(float* L, int n, int nblk, int p0, int R, int T, int t_end, Tile* tiles) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, h = lane >> 5;
   float (*Ub)[kLd] = tiles[0];  // [128][kLd]: rows of blocks R, R + 1 (two consecutive tiles)
@@ -429,19 +432,35 @@ __global__ __launch_bounds__(kThreads) void chol_trail_kernel(float* L, int n, i
   trailing_2x2<kSup>(L, n, nblk, p0, e + 2 * ti, e + 2 * tj, nblk, tiles);
 }
 
+// Panel-group updates that ride along in a single layer's panel launches (the
+// look-ahead form of the factorisation), kLa panels at a time. Band b is block
+// columns kLa b + 1 .. kLa b + kLa; task t applies the kLa panels of group
+// sp[t] (panels kLa sp[t] ..) to every block of band band[t] at or below the
+// diagonal, in groups[t] 2 x 2 groups, group column by group column. The
+// tasks' workgroups follow the launch's `trail` groups.
+constexpr int kLa = 2;
+constexpr int kMaxTasks = 64;
+struct CholExtra {
+  int trail;  // -1: no tasks
+  int n_tasks;
+  int band[kMaxTasks], sp[kMaxTasks], groups[kMaxTasks];
+};
+
 // Cholesky launch k (k = -1 .. nblk - 2): workgroups 0 .. m - 1 own the next
 // panel column, blocks (k + 1 + i, k + 1), and (when `apply`) first subtract
 // panel k from it; the others apply panel k to the trailing columns k + 2 ..
 // t_end - 1 (all rows below) in 2 x 2 groups of blocks, group column by group
-// column. Columns from t_end on receive panel k later, with the rest of its
-// super-panel (chol_trail_kernel).
+// column, then run the extra super-panel groups of `x` (none: x.trail = -1).
+// Columns from t_end on receive panel k later, with the rest of its
+// super-panel (chol_trail_kernel, or the extra groups of a later launch).
 // split = 0: every workgroup of the panel column factors the diagonal block
 // itself (no launch waits for another). split = 1: only the diagonal block
 // (one workgroup), which leaves its inverse in Dinv; split = 2: the blocks
 // below it, which read that inverse, and the trailing part. Both forms do the
 // same arithmetic in the same order.
 __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Dinv, int n, int k, int t_end,
-                                                            int apply, int split, int* status, int64_t ws) {
+                                                            int apply, int split, int* status, int64_t ws,
+                                                            CholExtra ex) {
   __shared__ __attribute__((aligned(16))) Tile tiles[6];
   __shared__ int bad;
   L = at_layer(L, ws, blockIdx.y);
@@ -449,6 +468,25 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   status = at_layer(status, ws, blockIdx.y);
   const int nblk = (n + kNb - 1) / kNb;
   const int m = split == 2 ? nblk - 2 - k : nblk - 1 - k;  // panel-column workgroups of this launch
+  if (ex.trail >= 0 && (int)blockIdx.x >= m + ex.trail) {
+    int idx = (int)blockIdx.x - m - ex.trail;
+    for (int t = 0; t < ex.n_tasks; ++t) {
+      if (idx < ex.groups[t]) {
+        const int e = ex.band[t] * kLa + 1, end = min(nblk, e + kLa);
+        for (int T = e; T < end; T += 2) {
+          const int gr = (nblk - T + 1) / 2;  // groups of this group column
+          if (idx < gr) {
+            trailing_2x2<kLa>(L, n, nblk, ex.sp[t] * kLa, T + 2 * idx, T, end, tiles);
+            return;
+          }
+          idx -= gr;
+        }
+        return;
+      }
+      idx -= ex.groups[t];
+    }
+    return;
+  }
   if ((int)blockIdx.x >= m) {
     const int rows = (nblk - k - 2 + 1) / 2;  // group rows of the trailing part
     int idx = (int)blockIdx.x - m, gj = 0;
@@ -1108,16 +1146,15 @@ hipError_t launch_gemm(const GemmArgs& g, int layers, hipStream_t stream) {
 
 }  // namespace
 
-// Panels of a single layer's factorisation whose trailing updates are
-// deferred to super-panels (a multiple of kSup): the first quarter from 48
-// panels on, none below (measured at 80 panels: 5.11 ms without, 5.00 ms
-// with 16 to 40 deferred, 5.10 with 60; at 24 panels every deferral is
-// slower, 0.645 -> 0.69 ms and more). ISPA_SOLVE_DEFER_PANELS overrides.
-static int solve_defer_panels(int nblk) {
-  const char* env = getenv("ISPA_SOLVE_DEFER_PANELS");
-  int c = env != nullptr ? atoi(env) : (nblk >= 48 ? nblk / 4 : 0);
-  if (c < 0) c = 0;
-  return c / kSup * kSup;
+// A single layer's factorisation in the look-ahead form (below) from 48
+// panels on (measured: 80 panels 5.07 -> 4.74 ms per solve, 48 panels 1.76 ->
+// 1.70 ms, 24 panels 0.654 -> 0.656 ms); ISPA_SOLVE_LOOKAHEAD=0 / 1 switches
+// it off / on at every size.
+static bool solve_lookahead(int nblk) {
+  if ((nblk - 2) / kLa + 1 >= kMaxTasks) return false;  // bands beyond the task table
+  const char* env = getenv("ISPA_SOLVE_LOOKAHEAD");
+  if (env != nullptr) return env[0] == '1';
+  return nblk >= 48;
 }
 
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda, float* delta_w,
@@ -1138,51 +1175,122 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     if (grid > 8192) grid = 8192;
     hipLaunchKernelGGL(solve_init_kernel, dim3(grid, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
   }
-  // Panels are grouped kSup at a time (super-panels) up to column c_def:
-  // launch k applies panel k only to the columns of its own super-panel; the
-  // rest of the trailing triangle receives the super-panel's panels together,
-  // in one launch that keeps each block in registers across them, once its
-  // last panel is factored (a quarter of the trailing-matrix traffic of
-  // applying each panel everywhere; the same arithmetic in the same order).
-  // With several layers every panel is deferred. A single layer's
-  // factorisation is a chain of launches bound by their latency, to which the
-  // extra launch per super-panel adds: it defers only the first panels, whose
-  // trailing updates are large enough to bound their launches, and applies
-  // every later panel everywhere at once.
+  // Several layers: the panels are grouped kSup at a time (super-panels);
+  // launch k applies panel k only to the columns of its own super-panel, and
+  // the rest of the trailing triangle receives the super-panel's panels
+  // together, in one launch that keeps each block in registers across them,
+  // once its last panel is factored (a quarter of the trailing-matrix traffic
+  // of applying each panel everywhere; the same arithmetic in the same order).
+  // A single layer's factorisation is a chain of launches bound by their
+  // latency, to which an extra launch per super-panel would add: it takes the
+  // look-ahead form below from 48 panels on, and below that applies every
+  // panel everywhere at once.
   const int sup = kSup;
-  const int c_def = nl > 1 ? nblk + sup : solve_defer_panels(nblk);
-  for (int k = -1; k <= nblk - 2; ++k) {
-    const int c = k + 1;                          // the panel column this launch factors
-    int apply = k >= 0 ? 1 : 0;
-    int t_end;
-    if (c > c_def) {
-      t_end = nblk;
-    } else if (c % sup == 0) {
-      if (c > 0) {
-        const int gr = (nblk - c + 1) / 2;
-        hipLaunchKernelGGL(chol_trail_kernel, dim3(gr * (gr + 1) / 2, nl), dim3(kThreads), 0, stream, L, d,
-                           c - sup, c, ws);
+  CholExtra none;
+  memset(&none, 0, sizeof(none));
+  none.trail = -1;
+  if (nl == 1 && solve_lookahead(nblk)) {
+    // Look-ahead form (one layer), with the panels in groups of kLa = 2: launch k
+    // applies panel k only up to block column 2 s + 2, s = k / 2 its group (the
+    // rest of the group and the first column of the next). The other columns
+    // receive whole groups in tasks (band, group) that ride along as extra
+    // workgroups in the panel launches: task (b, s) can run once panel 2 s + 1
+    // is factored (launch 2 s + 1 on), after task (b, s - 1), and must be done
+    // before launch 2 b applies panel 2 b to band b, so (b, b - 1) runs in
+    // launch 2 b - 1 and (b, s < b - 1) by launch b + s. Each launch takes
+    // every task whose deadline it is, then more of its available tasks,
+    // earliest deadline first, as many as fill the rounds of workgroups on
+    // the chip that the launch needs anyway (one at least). A task's
+    // workgroup (two panels on a 2 x 2 group of blocks, ~18.5 us) takes a
+    // little longer than the launch's panel chain (~15.5 us); with groups of
+    // four panels it took ~26 us (at 80 panels: 4.93 ms per solve, against
+    // 4.74 ms with groups of two and 5.07 ms without look-ahead). Each block
+    // still receives every panel once, in panel order, with the same
+    // arithmetic: bit for bit the factor of the other forms.
+    const int n_cu = attn_cu_count() > 0 ? attn_cu_count() : 256;
+    int next_sp[kMaxTasks] = {};               // per band: the next group it receives
+    const int n_bands = (nblk - 2) / kLa + 1;  // bands 1 .. n_bands - 1 start inside the matrix
+    for (int k = -1; k <= nblk - 2; ++k) {
+      const int m = nblk - 1 - k;
+      const int t_end = k >= 0 ? min(nblk, k / kLa * kLa + kLa + 1) : 0;
+      const int rows = (nblk - k - 2 + 1) / 2;
+      const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;
+      CholExtra x = none;
+      x.trail = cols * rows - cols * (cols - 1) / 2;
+      int cand[kMaxTasks][3], n_cand = 0;  // deadline, band, group
+      for (int b = 1; b < n_bands; ++b) {
+        const int sp = next_sp[b];
+        if (sp <= b - 1 && k >= sp * kLa + kLa - 1) {
+          cand[n_cand][0] = sp == b - 1 ? kLa * b - 1 : (kLa - 1) * b + sp;
+          cand[n_cand][1] = b;
+          cand[n_cand][2] = sp;
+          ++n_cand;
+        }
       }
-      apply = 0;                                  // panel k reached column c with its super-panel
-      t_end = c;                                  // and no column of its super-panel is left
-    } else {
-      t_end = min(nblk, (c / sup + 1) * sup);
+      for (int i = 1; i < n_cand; ++i)  // by deadline, then band
+        for (int j = i; j > 0 && (cand[j][0] < cand[j - 1][0] ||
+                                  (cand[j][0] == cand[j - 1][0] && cand[j][1] < cand[j - 1][1])); --j)
+          for (int f = 0; f < 3; ++f) std::swap(cand[j][f], cand[j - 1][f]);
+      auto band_groups = [&](int b) {
+        int g = 0;
+        for (int T = b * kLa + 1; T < min(nblk, b * kLa + kLa + 1); T += 2) g += (nblk - T + 1) / 2;
+        return g;
+      };
+      // the rounds of workgroups the launch needs for its due tasks, filled up
+      int used = m + x.trail, due = used;
+      for (int i = 0; i < n_cand; ++i)
+        if (cand[i][0] == k) due += band_groups(cand[i][1]);
+      const int cap = (due + n_cu - 1) / n_cu * n_cu;
+      for (int i = 0; i < n_cand; ++i) {
+        const int b = cand[i][1];
+        const int g = band_groups(b);
+        if (cand[i][0] == k || used + g <= cap) {
+          x.band[x.n_tasks] = b;
+          x.sp[x.n_tasks] = cand[i][2];
+          x.groups[x.n_tasks] = g;
+          ++x.n_tasks;
+          used += g;
+          ++next_sp[b];
+        }
+      }
+      hipLaunchKernelGGL(chol_step_kernel, dim3(used, 1), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end,
+                         k >= 0 ? 1 : 0, 0, w.status, ws, x);
     }
-    const int m = nblk - 1 - k;                   // blocks of the next panel column
-    const int rows = (nblk - k - 2 + 1) / 2;      // group rows of the trailing part
-    const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;  // launch -1 has no panel to apply
-    const int groups = cols * rows - cols * (cols - 1) / 2;
-    if (nl == 1) {
-      hipLaunchKernelGGL(chol_step_kernel, dim3(m + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end,
-                         apply, 0, w.status, ws);
-    } else {
-      // with many layers the diagonal block is factored once per layer, in its
-      // own launch, rather than once per block of the column
-      hipLaunchKernelGGL(chol_step_kernel, dim3(1, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end, apply, 1,
-                         w.status, ws);
-      if (m - 1 + groups > 0)
-        hipLaunchKernelGGL(chol_step_kernel, dim3(m - 1 + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k,
-                           t_end, apply, 2, w.status, ws);
+  } else {
+    const int c_def = nl > 1 ? nblk + sup : 0;
+    for (int k = -1; k <= nblk - 2; ++k) {
+      const int c = k + 1;                          // the panel column this launch factors
+      int apply = k >= 0 ? 1 : 0;
+      int t_end;
+      if (c > c_def) {
+        t_end = nblk;
+      } else if (c % sup == 0) {
+        if (c > 0) {
+          const int gr = (nblk - c + 1) / 2;
+          hipLaunchKernelGGL(chol_trail_kernel, dim3(gr * (gr + 1) / 2, nl), dim3(kThreads), 0, stream, L, d,
+                             c - sup, c, ws);
+        }
+        apply = 0;                                  // panel k reached column c with its super-panel
+        t_end = c;                                  // and no column of its super-panel is left
+      } else {
+        t_end = min(nblk, (c / sup + 1) * sup);
+      }
+      const int m = nblk - 1 - k;                   // blocks of the next panel column
+      const int rows = (nblk - k - 2 + 1) / 2;      // group rows of the trailing part
+      const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;  // launch -1 has no panel to apply
+      const int groups = cols * rows - cols * (cols - 1) / 2;
+      if (nl == 1) {
+        hipLaunchKernelGGL(chol_step_kernel, dim3(m + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end,
+                           apply, 0, w.status, ws, none);
+      } else {
+        // with many layers the diagonal block is factored once per layer, in its
+        // own launch, rather than once per block of the column
+        hipLaunchKernelGGL(chol_step_kernel, dim3(1, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end, apply, 1,
+                           w.status, ws, none);
+        if (m - 1 + groups > 0)
+          hipLaunchKernelGGL(chol_step_kernel, dim3(m - 1 + groups, nl), dim3(kThreads), 0, stream, L, w.dinv, d, k,
+                             t_end, apply, 2, w.status, ws, none);
+      }
     }
   }
   // X_I, P_I = X_I^T X_I, Lh below the 256-block diagonal, its mirror above

@@ -228,11 +228,12 @@ def test_batch_solve_wan13b_size():
         assert float(eps_b[i].item()) == float(eps_1.item())
 
 
-def test_batch_matches_single_with_deferred_panels():
-    # d = 3072 (48 panels): the single-layer factorisation defers its first 12
-    # panels to super-panels and applies the later ones everywhere at once,
-    # the batch defers all of them; every panel's product is subtracted on its
-    # own in panel order either way, so dW and eps agree bit for bit
+def test_batch_matches_single_with_look_ahead():
+    # d = 3072 (48 panels): the single-layer factorisation takes its look-ahead
+    # form (panel groups applied by extra workgroups of later panel launches),
+    # the batch defers every super-panel to launches of its own; every panel's
+    # product is subtracted on its own in panel order either way, so dW and
+    # eps agree bit for bit
     d, d_out, n, layers, lam = 3072, 256, 4000, 2, 1e-1
     print("[solve] batch of 2 at 3072", flush=True)
     sb = ispa.StatsBatch(layers, d, d_out, max_rows=n, device=DEV)
@@ -245,6 +246,29 @@ def test_batch_matches_single_with_deferred_panels():
         torch.cuda.synchronize()
         assert torch.equal(dw_b[i].view(torch.int32), dw_1.view(torch.int32))
         assert float(eps_b[i].item()) == float(eps_1.item())
+
+
+@pytest.mark.parametrize("d", [200, 776, 1288, 2560, 3000])
+def test_look_ahead_factorisation_is_bitwise(d, monkeypatch):
+    # the look-ahead form against one launch per panel applied everywhere, at
+    # sizes where the schedule's bands end ragged or the form is not the
+    # default (ISPA_SOLVE_LOOKAHEAD forces it): the same bits
+    d_out, n, lam = 64, 4000, 1e-1
+    print(f"[solve] look-ahead on / off at d={d}", flush=True)
+    st = ispa.Stats(d, d_out, max_rows=n, device=DEV)
+    x = rows(39, 0, n, d)
+    yf = synth.normal((n, d_out), synth.seed_of(39, 0, synth.Y_FULL), DEV, dtype=torch.float32)
+    yl = synth.normal((n, d_out), synth.seed_of(39, 0, synth.Y_LOCAL), DEV, dtype=torch.float32)
+    st.accum(x, yf, yl)
+    out = {}
+    for v in ("0", "1"):
+        monkeypatch.setenv("ISPA_SOLVE_LOOKAHEAD", v)
+        dw, eps, status = st.solve_async(lam)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        out[v] = (dw.clone(), float(eps.item()))
+    assert torch.equal(out["0"][0].view(torch.int32), out["1"][0].view(torch.int32))
+    assert out["0"][1] == out["1"][1]
 
 
 @pytest.mark.timeout(900)
