@@ -235,8 +235,8 @@ def dual_overhead_run(ispa, w, qkv, dev, reps=20):
     inputs. The two calls alternate back to back on the stream (no host
     synchronisation between them, so both see the same clock and power
     state); each is bracketed by HIP events and the medians of `reps`
-    timings are compared. Sec. 3.4 states that the LSE fusion costs under 1 %
-    of execution time."""
+    timings are compared. Sec. 3.4 puts the cost of the LSE fusion below one
+    percent of the run time."""
     q, k, v = qkv
     H = w["heads"]
     N = w["cache_len"]
