@@ -38,6 +38,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <utility>
 
 namespace ispa {
@@ -1146,6 +1147,39 @@ hipError_t launch_gemm(const GemmArgs& g, int layers, hipStream_t stream) {
 
 }  // namespace
 
+// A second stream per device for one half of the sweeps' columns, with the
+// events of the fork and the join (created once, kept for the process), from
+// d = kSweepTwoFrom on; ISPA_SOLVE_TWO_STREAMS=0 / 1 switches it off / on at
+// every size with at least two column tiles.
+namespace {
+constexpr int kSweepCols = 64;  // the halves split at a multiple of the tile width
+constexpr int kSweepTwoFrom = 4096;  // smallest d whose sweeps go on two streams
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool tried = false;
+};
+std::mutex g_side_mu;
+SideStream g_side[64];
+
+SideStream* side_stream(int d) {
+  const char* env = getenv("ISPA_SOLVE_TWO_STREAMS");
+  if (env != nullptr ? env[0] != '1' : d < kSweepTwoFrom) return nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  SideStream& t = g_side[dev];
+  if (!t.tried) {
+    t.tried = true;
+    if (hipStreamCreateWithFlags(&t.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&t.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&t.join, hipEventDisableTiming) != hipSuccess)
+      t.s = nullptr;
+  }
+  return t.s != nullptr ? &t : nullptr;
+}
+}  // namespace
+
 // A single layer's factorisation in the look-ahead form (below) from 48
 // panels on (measured: 80 panels 5.07 -> 4.74 ms per solve, 48 panels 1.76 ->
 // 1.70 ms, 24 panels 0.654 -> 0.656 ms); ISPA_SOLVE_LOOKAHEAD=0 / 1 switches
@@ -1328,81 +1362,108 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
                        stream, g);
     hipLaunchKernelGGL(mirror_kernel, dim3(nblk * nblk, nl), dim3(kThreads), 0, stream, L, d, ws);
   }
-  // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I. After the first
-  // block the blocks go in pairs (I, I+1): one launch finishes Y_{I+1} and forms
-  // dW_I, the next updates every later block with both (depth 512, so the
-  // read-modify-write of the right-hand side below is shared by two blocks)
-  // and forms dW_{I+1}. The A operand is the mirrored Lh above the diagonal,
-  // whose rows I*256 .. of blocks I and I+1 are consecutive.
-  auto fwd_launch = [&](const float* A, float* Ydst, const float* Ysrc, int M, const float* Bsum, int Ksum,
-                        int P, const float* Bp, int Kp) -> hipError_t {
-    GemmArgs g = {};
-    int j = 0;
-    if (M > 0) {
-      g.job[j] = GemmJob{A, Ydst, M, d, d_out, 1, Ysrc};
-      g.job[j].la = g.job[j].lc = ws;
-      g.job[j].B = Bsum;
-      g.job[j].K = Ksum;
-      ++j;
-    }
-    g.job[j] = GemmJob{pinv + (int64_t)P * kBb * kBb, delta_w + (int64_t)P * kBb * d_out, Kp, kBb, d_out, 0};
-    g.job[j].la = ws;
-    g.job[j].lc = dws;
-    g.job[j].B = Bp;
-    g.job[j].K = Kp;
-    ++j;
-    g.n_jobs = j;
-    g.lb = ws;
-    g.B = Bp;
-    g.N = d_out;
-    g.K = Kp;
-    g.ldb = d_out;
-    return launch_gemm(g, nl, stream);
-  };
+  // The sweeps treat each column of the right-hand side on its own, so from
+  // d = 4096 on the columns go in two halves, each on a stream of its own (the
+  // caller's and a second one), whose launches fill each other's last rounds
+  // of tiles and hide each other's short launches; every element's arithmetic
+  // is unchanged. Measured (one solve, alternating, medians of 10): d = 5120
+  // 4.75 -> 4.59 ms; d = 3072 1.70 -> 1.72, 2560 1.30 -> 1.34, 2048 0.91 ->
+  // 0.97, 1536 0.66 -> 0.69 ms (halves too small to fill the chip).
   auto yblk = [&](auto* base, int I) { return base + (int64_t)I * kBb * d_out; };
   auto kblk = [&](int I) { return min(kBb, d - I * kBb); };
   auto lup = [&](int I, int r) { return L + (int64_t)I * kBb * d + (int64_t)r * kBb; };  // rows of I, columns of r
-  {
-    // the first step reads the right-hand side C itself (Y = C before any update)
-    const hipError_t e = fwd_launch(lup(0, 1), yblk(Y, 1), yblk(C, 1), d - kBb, C, kblk(0), 0, C, kblk(0));
-    if (e != hipSuccess) return e;
-  }
-  for (int I = 1; I < nb; I += 2) {
+  auto sweeps = [&](int col0, int ncols, hipStream_t st) -> hipError_t {
+    // forward sweep: Y_r -= Lh_rI Y_I (r > I) and dW_I = P_I Y_I. After the first
+    // block the blocks go in pairs (I, I+1): one launch finishes Y_{I+1} and forms
+    // dW_I, the next updates every later block with both (depth 512, so the
+    // read-modify-write of the right-hand side below is shared by two blocks)
+    // and forms dW_{I+1}. The A operand is the mirrored Lh above the diagonal,
+    // whose rows I*256 .. of blocks I and I+1 are consecutive. Row pointers of
+    // the right-hand side, Y and dW are taken at column 0 and moved to col0 here.
+    auto fwd_launch = [&](const float* A, float* Ydst, const float* Ysrc, int M, const float* Bsum, int Ksum,
+                          int P, const float* Bp, int Kp) -> hipError_t {
+      GemmArgs g = {};
+      int j = 0;
+      if (M > 0) {
+        g.job[j] = GemmJob{A, Ydst + col0, M, d, d_out, 1, Ysrc + col0};
+        g.job[j].la = g.job[j].lc = ws;
+        g.job[j].B = Bsum + col0;
+        g.job[j].K = Ksum;
+        ++j;
+      }
+      g.job[j] = GemmJob{pinv + (int64_t)P * kBb * kBb, delta_w + (int64_t)P * kBb * d_out + col0, Kp, kBb, d_out, 0};
+      g.job[j].la = ws;
+      g.job[j].lc = dws;
+      g.job[j].B = Bp + col0;
+      g.job[j].K = Kp;
+      ++j;
+      g.n_jobs = j;
+      g.lb = ws;
+      g.B = Bp + col0;
+      g.N = ncols;
+      g.K = Kp;
+      g.ldb = d_out;
+      return launch_gemm(g, nl, st);
+    };
     hipError_t e;
-    if (I + 1 == nb) {
-      e = fwd_launch(nullptr, nullptr, nullptr, 0, nullptr, 0, I, yblk(Y, I), kblk(I));
+    // the first step reads the right-hand side C itself (Y = C before any update)
+    e = fwd_launch(lup(0, 1), yblk(Y, 1), yblk(C, 1), d - kBb, C, kblk(0), 0, C, kblk(0));
+    if (e != hipSuccess) return e;
+    for (int I = 1; I < nb; I += 2) {
+      if (I + 1 == nb) {
+        e = fwd_launch(nullptr, Y, Y, 0, Y, 0, I, yblk(Y, I), kblk(I));
+        if (e != hipSuccess) return e;
+        break;
+      }
+      e = fwd_launch(lup(I, I + 1), yblk(Y, I + 1), yblk(Y, I + 1), kblk(I + 1), yblk(Y, I), kBb, I, yblk(Y, I),
+                     kBb);
       if (e != hipSuccess) return e;
-      break;
+      const int below = d - (I + 2) * kBb;
+      e = fwd_launch(below > 0 ? lup(I, I + 2) : nullptr, below > 0 ? yblk(Y, I + 2) : Y,
+                     below > 0 ? yblk(Y, I + 2) : Y, max(below, 0), yblk(Y, I), kBb + kblk(I + 1), I + 1,
+                     yblk(Y, I + 1), kblk(I + 1));
+      if (e != hipSuccess) return e;
     }
-    e = fwd_launch(lup(I, I + 1), yblk(Y, I + 1), yblk(Y, I + 1), kblk(I + 1), yblk(Y, I), kBb, I, yblk(Y, I), kBb);
-    if (e != hipSuccess) return e;
-    const int below = d - (I + 2) * kBb;
-    e = fwd_launch(below > 0 ? lup(I, I + 2) : nullptr, yblk(Y, I + 2), yblk(Y, I + 2), max(below, 0), yblk(Y, I),
-                   kBb + kblk(I + 1), I + 1, yblk(Y, I + 1), kblk(I + 1));
-    if (e != hipSuccess) return e;
-  }
-  // backward sweep: dW_I -= Lh_JI^T dW_J (I < J), from the last block down in
-  // pairs (J, J-1): one launch finishes dW_{J-1}, the next updates every earlier
-  // block with both (rows (J-1)*256 .. of L, depth 512)
-  auto bwd_launch = [&](int J, int M, int K, float* Cdst) -> hipError_t {
-    GemmArgs g = {};
-    g.job[0] = GemmJob{L + (int64_t)J * kBb * d + (Cdst - delta_w) / d_out, Cdst, M, d, d_out, 1};
-    g.job[0].la = ws;
-    g.job[0].lc = dws;
-    g.lb = dws;
-    g.n_jobs = 1;
-    g.B = yblk(delta_w, J);
-    g.N = d_out;
-    g.K = K;
-    g.ldb = d_out;
-    return launch_gemm(g, nl, stream);
-  };
-  for (int J = nb - 1; J >= 1; J -= 2) {
-    hipError_t e = bwd_launch(J, kBb, kblk(J), yblk(delta_w, J - 1));
-    if (e != hipSuccess) return e;
-    if (J - 1 >= 1) {
-      e = bwd_launch(J - 1, (J - 1) * kBb, kBb + kblk(J), delta_w);
+    // backward sweep: dW_I -= Lh_JI^T dW_J (I < J), from the last block down in
+    // pairs (J, J-1): one launch finishes dW_{J-1}, the next updates every earlier
+    // block with both (rows (J-1)*256 .. of L, depth 512); rows from row0 on
+    auto bwd_launch = [&](int J, int M, int K, int row0) -> hipError_t {
+      GemmArgs g = {};
+      g.job[0] = GemmJob{L + (int64_t)J * kBb * d + row0, delta_w + (int64_t)row0 * d_out + col0, M, d, d_out, 1};
+      g.job[0].la = ws;
+      g.job[0].lc = dws;
+      g.lb = dws;
+      g.n_jobs = 1;
+      g.B = yblk(delta_w, J) + col0;
+      g.N = ncols;
+      g.K = K;
+      g.ldb = d_out;
+      return launch_gemm(g, nl, st);
+    };
+    for (int J = nb - 1; J >= 1; J -= 2) {
+      e = bwd_launch(J, kBb, kblk(J), (J - 1) * kBb);
       if (e != hipSuccess) return e;
+      if (J - 1 >= 1) {
+        e = bwd_launch(J - 1, (J - 1) * kBb, kBb + kblk(J), 0);
+        if (e != hipSuccess) return e;
+      }
+    }
+    return hipSuccess;
+  };
+  {
+    SideStream* side = d_out >= 2 * kSweepCols ? side_stream(d) : nullptr;
+    hipError_t e;
+    if (side != nullptr) {
+      std::lock_guard<std::mutex> lock(g_side_mu);
+      const int half = (d_out / 2 + kSweepCols - 1) / kSweepCols * kSweepCols;
+      if ((e = hipEventRecord(side->fork, stream)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(side->s, side->fork, 0)) != hipSuccess) return e;
+      if ((e = sweeps(0, half, stream)) != hipSuccess) return e;
+      if ((e = sweeps(half, d_out - half, side->s)) != hipSuccess) return e;
+      if ((e = hipEventRecord(side->join, side->s)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(stream, side->join, 0)) != hipSuccess) return e;
+    } else if ((e = sweeps(0, d_out, stream)) != hipSuccess) {
+      return e;
     }
   }
   // the P_I area is free once the forward sweep has run: it holds the partial sums

@@ -271,6 +271,28 @@ def test_look_ahead_factorisation_is_bitwise(d, monkeypatch):
     assert out["0"][1] == out["1"][1]
 
 
+@pytest.mark.parametrize("d,d_out", [(776, 328), (1288, 200), (600, 136), (304, 64)])
+def test_sweeps_on_two_streams_are_bitwise(d, d_out, monkeypatch):
+    # the sweeps split the right-hand side's columns in two halves on two
+    # streams (d_out >= 128; 64 stays on one): the same bits as one stream
+    n, lam = 2000, 1e-2
+    print(f"[solve] sweeps on one / two streams at d={d} d_out={d_out}", flush=True)
+    st = ispa.Stats(d, d_out, max_rows=n, device=DEV)
+    x = rows(40, 0, n, d)
+    yf = synth.normal((n, d_out), synth.seed_of(40, 0, synth.Y_FULL), DEV, dtype=torch.float32)
+    yl = synth.normal((n, d_out), synth.seed_of(40, 0, synth.Y_LOCAL), DEV, dtype=torch.float32)
+    st.accum(x, yf, yl)
+    out = {}
+    for v in ("0", "1"):
+        monkeypatch.setenv("ISPA_SOLVE_TWO_STREAMS", v)
+        dw, eps, status = st.solve_async(lam)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        out[v] = (dw.clone(), float(eps.item()))
+    assert torch.equal(out["0"][0].view(torch.int32), out["1"][0].view(torch.int32))
+    assert out["0"][1] == out["1"][1]
+
+
 @pytest.mark.timeout(900)
 def test_14b_absorption():
     # the 14B layer's absorption: G (5120 x 5120) and C from 4 warmup chunks of
