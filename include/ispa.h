@@ -153,7 +153,8 @@ size_t ispa_attn_workspace_bytes(int64_t cache_len, int64_t window, int64_t sink
  *   outputs for the same inputs).
  *   Returns ISPA_ERR_SCRATCH, before enqueueing anything, when the split needs
  *   more than ISPA_STATIC_SCRATCH_BYTES (ispa_attn_workspace_bytes with
- *   segments = 0 tells; the 1.3B-shaped dual-stream chunk needs 129 MiB).
+ *   segments = 0 tells; a dual-stream chunk of 4680 queries over 7 chunks of
+ *   cache that splits, e.g. with 10 heads x 128, needs 129 MiB).
  * Every call on one GPU uses the same array: calls that overlap on one GPU
  * (other streams, other threads) race and give undefined results. The array
  * needs no clearing: the call clears the counters it uses and writes every
@@ -265,6 +266,12 @@ int ispa_accum_stats(ispa_stats* handle, const void* x, int32_t x_dtype,
  * G and C are left unchanged, so the caller may solve again with another
  * lambda or keep accumulating. Waits for the handle's stream to finish; returns
  * ISPA_ERR_NOT_SPD (delta_w then unspecified) if a pivot is not positive.
+ * From d_in = 4096 on (with d_out >= 128) the triangular solves of half of
+ * C's columns run on a second stream that the library owns (one per device);
+ * it waits for the handle's stream before it starts and the handle's stream
+ * waits for it before the score, so the work stays ordered on the handle's
+ * stream as seen by the caller (ISPA_SOLVE_TWO_STREAMS=0 keeps everything on
+ * the handle's stream; the results are the same bits either way).
  */
 int ispa_solve_modulation(ispa_stats* handle, float lambda, float* delta_w, double* eps_out);
 
