@@ -323,15 +323,27 @@ __device__ __forceinline__ void tri_index(int t, int& ti, int& tj) {
   tj = t - ti * (ti + 1) / 2;
 }
 
-// L = lower(G) + lambda I (upper part zero), status = 0.
+// L = lower(G) + lambda I with zeros above the diagonal up to the end of the
+// row's 256-block (the part above the 256-block diagonal is never read before
+// the mirror of Lh overwrites it), status = 0. Row blockIdx.x, four columns per
+// thread (n is a multiple of 4); only G's lower triangle is read.
 __global__ void solve_init_kernel(const float* G, float* L, int n, float lambda, int* status, int64_t ws) {
   G = at_layer(G, ws, blockIdx.y);
   L = at_layer(L, ws, blockIdx.y);
   status = at_layer(status, ws, blockIdx.y);
-  const int64_t nn = (int64_t)n * n;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nn; i += (int64_t)gridDim.x * blockDim.x) {
-    const int r = (int)(i / n), c = (int)(i % n);
-    L[i] = c < r ? G[i] : (c == r ? G[i] + lambda : 0.f);
+  constexpr int kBlock = 256;  // the sweeps' block size
+  const int r = blockIdx.x;
+  const int end = min(n, (r / kBlock + 1) * kBlock);
+  const float* g = G + (int64_t)r * n;
+  float* l = L + (int64_t)r * n;
+  for (int c = threadIdx.x * 4; c < end; c += blockDim.x * 4) {
+    f32x4 v = c <= r ? *(const f32x4*)(g + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (c + j > r) v[j] = 0.f;
+      else if (c + j == r) v[j] += lambda;
+    }
+    *(f32x4*)(l + c) = v;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
@@ -1203,12 +1215,7 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
   // apart, the layers' dW `dws` bytes apart
   const int nl = w.n_layers;
   const int64_t ws = w.ws_stride, dws = w.dw_stride;
-  {
-    const int64_t total = (int64_t)d * d;
-    int grid = (int)((total + 255) / 256);
-    if (grid > 8192) grid = 8192;
-    hipLaunchKernelGGL(solve_init_kernel, dim3(grid, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
-  }
+  hipLaunchKernelGGL(solve_init_kernel, dim3(d, nl), dim3(256), 0, stream, G, L, d, lambda, w.status, ws);
   // Several layers: the panels are grouped kSup at a time (super-panels);
   // launch k applies panel k only to the columns of its own super-panel, and
   // the rest of the trailing triangle receives the super-panel's panels
