@@ -48,19 +48,25 @@ V_O = (128, 192)    # 64 each: O^T of block 0 / 1, dBlock db at +16 db
 A_Q = (0, 32)       # Q^T operands of block 0 / 1, slice kk at +4 kk
 A_K = 64            # K operands of one half, slice kk at +4 kk
 A_V = 96            # V^T operands of one half, slice s and dBlock db at +16 s + 4 db
-# the normaliser of O: "mfma", the sum of the bf16-rounded weights on the
-# matrix cores (an all-ones operand times P^T); "valu", that sum on the VALU
-# (v_dot2c per pair); "fp32", the fp32 sum l of the unrounded weights that
-# the LSE uses as well. "fp32" needs 8 fewer matrix instructions per 64 and
-# runs 6.7% faster at the chip's power limit, but the sum of the rounded
-# weights cancels their mean rounding error in O (the weights applied then
-# sum to exactly 1): without it the error on small windows grows by 10-45%,
-# past the 2e-2 of the output RMS that parity allows in one case
-NORM = "mfma"
-SUMS_ON_MFMA = NORM == "mfma"
-A_ONES = 128        # an all-ones bf16 operand: (ones) P^T sums the bf16 weights of each query
-A_LR = (132, 148)   # 16 each: those sums (every row of the 32 x 32 block holds them), per block
-N_AGPR = 164 if SUMS_ON_MFMA else 128
+# the normaliser of O: "mfma16", the sum of the bf16-rounded weights on the
+# matrix cores, two 16x16x32 MFMAs per block and half whose A operand selects
+# the lanes of one query (P^T in the 32x32x16 B layout read as a 16x16x32 B
+# operand: lanes 0-15 / 32-47 hold queries 0-15, lanes 16-31 / 48-63 queries
+# 16-31, so row 0 of the product sums queries 0-15 and row 1 queries 16-31);
+# "mfma", the same sum with 32x32x16 MFMAs and an all-ones operand (twice the
+# passes); "valu", that sum on the VALU (v_dot2c per pair); "fp32", the fp32
+# sum l of the unrounded weights that the LSE uses as well. "fp32" needs no
+# extra matrix instructions and runs 6.7% faster than "mfma" at the chip's
+# power limit, but the sum of the rounded weights cancels their mean rounding
+# error in O (the weights applied then sum to exactly 1): without it the
+# error on small windows grows by 10-45%, past the 2e-2 of the output RMS
+# that parity allows in one case
+NORM = "mfma16"
+SUMS_ON_MFMA = NORM in ("mfma", "mfma16")
+N_LR = 4 if NORM == "mfma16" else 16  # accumulator registers of the sums per block
+A_ONES = 128        # the bf16 A operand of the sum MFMAs (all ones, or the lane selector)
+A_LR = (132, 132 + N_LR)  # the sums, per block
+N_AGPR = 132 + 2 * N_LR if SUMS_ON_MFMA else 128
 BF16_ONES = "0x3f803f80"
 # phase schedule: spread the non-matrix instructions by estimated issue cost
 BALANCED = True
@@ -388,7 +394,22 @@ class Gen:
         # the P V instructions issued so far (old reference) have completed
         resc += ["s_nop 7", "s_nop 7", "s_nop 7"]
         resc += [f"v_mul_f32_e32 {vp(V_O[qb] + i)}, {vp(alpha)}, {vp(V_O[qb] + i)}" for i in range(64)]
-        if SUMS_ON_MFMA:
+        if NORM == "mfma16":
+            # register 0 of lane n (< 16) sums query n, register 1 query n + 16,
+            # whose alpha lane n + 16 holds; the other lanes and registers are 0
+            t, a16, adr = V_T + 8, V_T + 9, V_T + 10
+            resc += [f"v_add_u32_e32 {vp(adr)}, 16, {vp(V_LANE)}",
+                     f"v_and_b32_e32 {vp(adr)}, 63, {vp(adr)}",
+                     f"v_lshlrev_b32_e32 {vp(adr)}, 2, {vp(adr)}",
+                     f"ds_bpermute_b32 {vp(a16)}, {vp(adr)}, {vp(alpha)}",
+                     f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb])}",
+                     f"v_mul_f32_e32 {vp(t)}, {vp(alpha)}, {vp(t)}",
+                     f"v_accvgpr_write_b32 {ap(A_LR[qb])}, {vp(t)}",
+                     "s_waitcnt lgkmcnt(0)",
+                     f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb] + 1)}",
+                     f"v_mul_f32_e32 {vp(t)}, {vp(a16)}, {vp(t)}",
+                     f"v_accvgpr_write_b32 {ap(A_LR[qb] + 1)}, {vp(t)}"]
+        elif SUMS_ON_MFMA:
             for i in range(16):
                 t = V_T + 8 + (i & 7)
                 resc += [f"v_accvgpr_read_b32 {vp(t)}, {ap(A_LR[qb] + i)}",
@@ -425,8 +446,9 @@ class Gen:
                     out.append(f"v_mfma_f32_32x32x16_bf16 {o}, {ap(A_V + 16 * s + 4 * db, 4)}, "
                                f"{vp(p + 4 * s, 4)}, {o}")
             for s in range(2 if SUMS_ON_MFMA else 0):
-                acc = ap(A_LR[qb], 16)
-                out.append(f"v_mfma_f32_32x32x16_bf16 {acc}, {ap(A_ONES, 4)}, {vp(p + 4 * s, 4)}, {acc}")
+                acc = ap(A_LR[qb], N_LR)
+                shape = "16x16x32" if NORM == "mfma16" else "32x32x16"
+                out.append(f"v_mfma_f32_{shape}_bf16 {acc}, {ap(A_ONES, 4)}, {vp(p + 4 * s, 4)}, {acc}")
         return out
 
     @staticmethod
@@ -530,6 +552,23 @@ class Gen:
             self.emit(i)
 
     # ---------------------------------------------------------------- output
+    @staticmethod
+    def lr16(qb, dst, t1, t2):
+        """dst = the sum of the bf16-rounded weights of this lane's query
+        (lane & 31) from the 16x16 sum accumulator of block qb: register 0 of
+        lane q for q < 16, register 1 of lane q - 16 otherwise (the sum MFMAs
+        have completed)."""
+        return [f"v_accvgpr_read_b32 {vp(dst)}, {ap(A_LR[qb])}",
+                f"v_accvgpr_read_b32 {vp(t1)}, {ap(A_LR[qb] + 1)}",
+                f"v_and_b32_e32 {vp(t2)}, 15, {vp(V_LANE)}",
+                f"v_lshlrev_b32_e32 {vp(t2)}, 2, {vp(t2)}",
+                f"ds_bpermute_b32 {vp(dst)}, {vp(t2)}, {vp(dst)}",
+                f"ds_bpermute_b32 {vp(t1)}, {vp(t2)}, {vp(t1)}",
+                f"v_and_b32_e32 {vp(t2)}, 16, {vp(V_LANE)}",
+                f"v_cmp_ne_u32_e32 vcc, 0, {vp(t2)}",
+                "s_waitcnt lgkmcnt(0)",
+                f"v_cndmask_b32_e32 {vp(dst)}, {vp(dst)}, {vp(t1)}, vcc"]
+
     def write_state(self, rows, which):
         """Normalised O and LSE of both blocks. rows: to the output rows
         (out / lse, or out_local / lse_local when which = 1); else to partial
@@ -568,6 +607,8 @@ class Gen:
             m, l = V_ST[qb], V_ST[qb] + 3
             if NORM == "mfma":
                 self.emit(f"v_accvgpr_read_b32 {vp(T + 4)}, {ap(A_LR[qb])}")      # lr total
+            elif NORM == "mfma16":
+                self.emit(*self.lr16(qb, T + 4, T + 5, T + 6))                     # lr total
             elif NORM == "valu":
                 self.emit(f"v_mov_b32_e32 {vp(T + 4)}, {vp(V_ST[qb] + 1)}", f"v_mov_b32_e32 {vp(T + 5)}, {vp(V_ST[qb] + 1)}",
                           "s_nop 1",
@@ -806,6 +847,8 @@ class Gen:
             m, l = V_ST[qb], V_ST[qb] + 3
             if NORM == "mfma":
                 self.emit(f"v_accvgpr_read_b32 {vp(INV[qb])}, {ap(A_LR[qb])}")
+            elif NORM == "mfma16":
+                self.emit(*self.lr16(qb, INV[qb], T + 3, T + 2))
             elif NORM == "valu":
                 self.emit(f"v_mov_b32_e32 {vp(INV[qb])}, {vp(V_ST[qb] + 1)}", f"v_mov_b32_e32 {vp(T + 3)}, {vp(V_ST[qb] + 1)}",
                           "s_nop 1",
@@ -1179,7 +1222,7 @@ class Gen:
                 self.emit(f"v_mov_b32_e32 {vp(V_O[qb] + i)}, 0")
         self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0")
         for qb in range(2 if SUMS_ON_MFMA else 0):
-            for i in range(16):
+            for i in range(N_LR):
                 self.emit(f"v_accvgpr_write_b32 {ap(A_LR[qb] + i)}, {vp(V_T)}")
         # wait for tile ta and Q (the loads of tiles ta+1, ta+2 may stay in flight)
         self.emit("s_waitcnt vmcnt(16)", "s_barrier")
@@ -1260,7 +1303,21 @@ class Gen:
                   f"s_add_u32 {sp(S_BUDGET)}, {sp(S_BUDGET)}, 16",
                   f"s_mov_b32 {sp(S_SLOT)}, 0")
         self.lane_constants()
-        self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0x3f803f80")
+        if NORM == "mfma16":
+            # the selector: ones in lanes 0 and 32 (row 0, k-groups 0 and 2) and
+            # 17 and 49 (row 1, k-groups 1 and 3), zeros elsewhere
+            T = V_T
+            self.emit(f"v_and_b32_e32 {vp(T + 1)}, 15, {vp(V_LANE)}",              # row m
+                      f"v_bfe_u32 {vp(T + 2)}, {vp(V_LANE)}, 4, 1",                # k-group parity
+                      f"v_xor_b32_e32 {vp(T + 2)}, {vp(T + 1)}, {vp(T + 2)}",
+                      f"v_lshrrev_b32_e32 {vp(T + 1)}, 1, {vp(T + 1)}",
+                      f"v_or_b32_e32 {vp(T + 2)}, {vp(T + 2)}, {vp(T + 1)}",       # 0: m < 2, m = parity
+                      f"v_cmp_eq_u32_e32 vcc, 0, {vp(T + 2)}",
+                      f"v_mov_b32_e32 {vp(T)}, 0x3f803f80",
+                      "s_nop 1",
+                      f"v_cndmask_b32_e32 {vp(T)}, 0, {vp(T)}, vcc")
+        else:
+            self.emit(f"v_mov_b32_e32 {vp(V_T)}, 0x3f803f80")
         for i in range(4 if SUMS_ON_MFMA else 0):
             self.emit(f"v_accvgpr_write_b32 {ap(A_ONES + i)}, {vp(V_T)}")
         self.piece_start()
