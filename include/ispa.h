@@ -315,6 +315,21 @@ int ispa_solve_modulation_async(ispa_stats* handle, float lambda, float* delta_w
 int ispa_solve_modulation_batch(ispa_stats* const* handles, int32_t n_layers, float lambda, float* delta_w,
                                 double* eps_dev, int32_t* status_dev);
 
+/*
+ * Host-side check of the launch schedule of a single layer's Cholesky
+ * factorisation in its look-ahead form (Sec. 3.2, Eq. 5; the solve takes that
+ * form from 48 panels of 64 columns on): builds the schedule for n_panels
+ * panels on n_cu compute units and walks every launch through the same
+ * workgroup decode the kernel runs, checking that each 64 x 64 block on or
+ * below the diagonal receives every earlier panel exactly once, in panel
+ * order, after that panel was factored, that no block is written twice within
+ * a launch, and that each launch finds its panel column complete. For tests;
+ * touches no device. Returns 0 when the schedule is valid, a positive value
+ * (the failing launch + 2, or n_panels + 1 for an incomplete block at the end)
+ * otherwise, and -1 for n_panels < 1 or above 127 or n_cu < 1.
+ */
+int ispa_solve_lookahead_check(int32_t n_panels, int32_t n_cu);
+
 /* ---------------------------------------------------------- absorption */
 /*
  * Instance-specific layer selection (Sec. 3.3): the k layers with the lowest

@@ -47,6 +47,7 @@ _c_i32, _c_i64, _c_f32, _c_p, _c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_f
 _SIGNATURES = {
     "ispa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "ispa_abi_version": (ctypes.c_int, []),
+    "ispa_solve_lookahead_check": (ctypes.c_int, [_c_i32, _c_i32]),
     "ispa_attn_chunk": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,
                                        _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "ispa_attn_chunk_ws": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32,

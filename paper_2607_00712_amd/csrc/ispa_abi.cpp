@@ -421,6 +421,8 @@ int ispa_solve_modulation_async(ispa_stats* h, float lambda, float* delta_w, dou
   return enqueue_solve(h, lambda, delta_w, eps_dev, status_dev);
 }
 
+int ispa_solve_lookahead_check(int32_t n_panels, int32_t n_cu) { return ispa::solve_lookahead_check(n_panels, n_cu); }
+
 int ispa_solve_modulation_batch(ispa_stats* const* handles, int32_t n_layers, float lambda, float* delta_w,
                                 double* eps_dev, int32_t* status_dev) {
   if (!handles || n_layers < 1 || n_layers > 4096) return ISPA_ERR_INVALID_ARG;

@@ -165,6 +165,8 @@ struct SolveWork {
   int64_t dw_stride = 0;
 };
 size_t solve_dinv_bytes(int d);
+// host-only check of a single layer's look-ahead factorisation schedule (0: valid)
+int solve_lookahead_check(int nblk, int n_cu);
 hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float lambda,
                         float* delta_w, const SolveWork& w, hipStream_t stream);
 

@@ -459,6 +459,51 @@ struct CholExtra {
   int band[kMaxTasks], sp[kMaxTasks], groups[kMaxTasks];
 };
 
+// What workgroup wg of Cholesky launch k works on; the kernel and the host
+// check of the look-ahead schedule share this decode. kind 0: the block of the
+// next panel column in row R (column T = k + 1), which receives panel k when
+// the launch applies it; kind 1: the 2 x 2 group of blocks with top-left
+// (R, T), of which the blocks at or below the diagonal, inside the matrix and
+// left of column t_end receive the np panels p0 ..; kind -1: nothing.
+struct CholWork {
+  int kind, R, T, p0, np, t_end;
+};
+__host__ __device__ inline CholWork chol_work_of(int wg, int nblk, int k, int t_end, int split, const CholExtra& ex) {
+  CholWork w = {-1, 0, 0, 0, 0, 0};
+  const int m = split == 2 ? nblk - 2 - k : nblk - 1 - k;  // panel-column workgroups of this launch
+  if (ex.trail >= 0 && wg >= m + ex.trail) {
+    int idx = wg - m - ex.trail;
+    for (int t = 0; t < ex.n_tasks; ++t) {
+      if (idx < ex.groups[t]) {
+        const int e = ex.band[t] * kLa + 1, end = e + kLa < nblk ? e + kLa : nblk;
+        for (int T = e; T < end; T += 2) {
+          const int gr = (nblk - T + 1) / 2;  // groups of this group column
+          if (idx < gr) {
+            w = CholWork{1, T + 2 * idx, T, ex.sp[t] * kLa, kLa, end};
+            return w;
+          }
+          idx -= gr;
+        }
+        return w;
+      }
+      idx -= ex.groups[t];
+    }
+    return w;
+  }
+  if (wg >= m) {
+    const int rows = (nblk - k - 2 + 1) / 2;  // group rows of the trailing part
+    int idx = wg - m, gj = 0;
+    while (gj < rows && idx >= rows - gj) {
+      idx -= rows - gj;
+      ++gj;
+    }
+    if (gj < rows) w = CholWork{1, k + 2 + 2 * (gj + idx), k + 2 + 2 * gj, k, 1, t_end};
+    return w;
+  }
+  w = CholWork{0, k + 1 + (split == 2 ? 1 : 0) + wg, k + 1, k, 1, 0};
+  return w;
+}
+
 // Cholesky launch k (k = -1 .. nblk - 2): workgroups 0 .. m - 1 own the next
 // panel column, blocks (k + 1 + i, k + 1), and (when `apply`) first subtract
 // panel k from it; the others apply panel k to the trailing columns k + 2 ..
@@ -480,40 +525,19 @@ __global__ __launch_bounds__(kThreads) void chol_step_kernel(float* L, float* Di
   Dinv = at_layer(Dinv, ws, blockIdx.y);
   status = at_layer(status, ws, blockIdx.y);
   const int nblk = (n + kNb - 1) / kNb;
-  const int m = split == 2 ? nblk - 2 - k : nblk - 1 - k;  // panel-column workgroups of this launch
-  if (ex.trail >= 0 && (int)blockIdx.x >= m + ex.trail) {
-    int idx = (int)blockIdx.x - m - ex.trail;
-    for (int t = 0; t < ex.n_tasks; ++t) {
-      if (idx < ex.groups[t]) {
-        const int e = ex.band[t] * kLa + 1, end = min(nblk, e + kLa);
-        for (int T = e; T < end; T += 2) {
-          const int gr = (nblk - T + 1) / 2;  // groups of this group column
-          if (idx < gr) {
-            trailing_2x2<kLa>(L, n, nblk, ex.sp[t] * kLa, T + 2 * idx, T, end, tiles);
-            return;
-          }
-          idx -= gr;
-        }
-        return;
-      }
-      idx -= ex.groups[t];
+  const CholWork wk = chol_work_of((int)blockIdx.x, nblk, k, t_end, split, ex);
+  if (wk.kind < 0) return;
+  if (wk.kind == 1) {
+    if (wk.np == 1) {
+      trailing_2x2<1>(L, n, nblk, wk.p0, wk.R, wk.T, wk.t_end, tiles);
+    } else {
+      trailing_2x2<kLa>(L, n, nblk, wk.p0, wk.R, wk.T, wk.t_end, tiles);
     }
-    return;
-  }
-  if ((int)blockIdx.x >= m) {
-    const int rows = (nblk - k - 2 + 1) / 2;  // group rows of the trailing part
-    int idx = (int)blockIdx.x - m, gj = 0;
-    while (gj < rows && idx >= rows - gj) {
-      idx -= rows - gj;
-      ++gj;
-    }
-    if (gj >= rows) return;
-    trailing_2x2<1>(L, n, nblk, k, k + 2 + 2 * (gj + idx), k + 2 + 2 * gj, t_end, tiles);
     return;
   }
   apply = apply && k >= 0;
   Tile &S = tiles[0], &M = tiles[1], &T = tiles[2], &U = tiles[3], &V = tiles[4], &P = tiles[5];
-  const int r = k + 1 + (split == 2 ? 1 : 0) + (int)blockIdx.x, t = k + 1;  // block coordinates
+  const int r = wk.R, t = wk.T;  // block coordinates
   const int rr = min(kNb, n - r * kNb);
   float* Lrt = L + (int64_t)r * kNb * n + t * kNb;
   if (threadIdx.x == 0) bad = 0;
@@ -1192,6 +1216,110 @@ SideStream* side_stream(int d) {
 }
 }  // namespace
 
+// The launches of a single layer's look-ahead factorisation (launch k at
+// index k + 1): its workgroups, its t_end and its extra tasks (see launch_solve).
+struct LookaheadPlan {
+  std::vector<int> grid, t_end;
+  std::vector<CholExtra> extra;
+};
+static void lookahead_plan(int nblk, int n_cu, LookaheadPlan* plan) {
+  plan->grid.assign(nblk, 0);
+  plan->t_end.assign(nblk, 0);
+  plan->extra.assign(nblk, CholExtra{});
+  int next_sp[kMaxTasks] = {};               // per band: the next group it receives
+  const int n_bands = (nblk - 2) / kLa + 1;  // bands 1 .. n_bands - 1 start inside the matrix
+  auto band_groups = [&](int b) {
+    int g = 0;
+    for (int T = b * kLa + 1; T < min(nblk, b * kLa + kLa + 1); T += 2) g += (nblk - T + 1) / 2;
+    return g;
+  };
+  for (int k = -1; k <= nblk - 2; ++k) {
+    const int m = nblk - 1 - k;
+    const int t_end = k >= 0 ? min(nblk, k / kLa * kLa + kLa + 1) : 0;
+    const int rows = (nblk - k - 2 + 1) / 2;
+    const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;
+    CholExtra x;
+    memset(&x, 0, sizeof(x));
+    x.trail = cols * rows - cols * (cols - 1) / 2;
+    int cand[kMaxTasks][3], n_cand = 0;  // deadline, band, group
+    for (int b = 1; b < n_bands; ++b) {
+      const int sp = next_sp[b];
+      if (sp <= b - 1 && k >= sp * kLa + kLa - 1) {
+        cand[n_cand][0] = sp == b - 1 ? kLa * b - 1 : (kLa - 1) * b + sp;
+        cand[n_cand][1] = b;
+        cand[n_cand][2] = sp;
+        ++n_cand;
+      }
+    }
+    for (int i = 1; i < n_cand; ++i)  // by deadline, then band
+      for (int j = i; j > 0 && (cand[j][0] < cand[j - 1][0] ||
+                                (cand[j][0] == cand[j - 1][0] && cand[j][1] < cand[j - 1][1])); --j)
+        for (int f = 0; f < 3; ++f) std::swap(cand[j][f], cand[j - 1][f]);
+    // the rounds of workgroups the launch needs for its due tasks, filled up
+    int used = m + x.trail, due = used;
+    for (int i = 0; i < n_cand; ++i)
+      if (cand[i][0] == k) due += band_groups(cand[i][1]);
+    const int cap = (due + n_cu - 1) / n_cu * n_cu;
+    for (int i = 0; i < n_cand; ++i) {
+      const int b = cand[i][1];
+      const int g = band_groups(b);
+      if (cand[i][0] == k || used + g <= cap) {
+        x.band[x.n_tasks] = b;
+        x.sp[x.n_tasks] = cand[i][2];
+        x.groups[x.n_tasks] = g;
+        ++x.n_tasks;
+        used += g;
+        ++next_sp[b];
+      }
+    }
+    plan->grid[k + 1] = used;
+    plan->t_end[k + 1] = t_end;
+    plan->extra[k + 1] = x;
+  }
+}
+
+int solve_lookahead_check(int nblk, int n_cu) {
+  if (nblk < 1 || (nblk - 2) / kLa + 1 >= kMaxTasks || n_cu < 1) return -1;
+  LookaheadPlan plan;
+  lookahead_plan(nblk, n_cu, &plan);
+  // per block (r, c), r >= c: the next panel it must receive, and the last
+  // launch that wrote it
+  std::vector<int> next((size_t)nblk * nblk, 0), stamp((size_t)nblk * nblk, -2);
+  for (int k = -1; k <= nblk - 2; ++k) {
+    const int fail = k + 2;
+    auto receive = [&](int r, int c, int p0, int np) {
+      if (r < c || r >= nblk || c >= nblk) return false;
+      const size_t b = (size_t)r * nblk + c;
+      if (stamp[b] == k) return false;  // written twice in one launch
+      stamp[b] = k;
+      for (int p = p0; p < p0 + np; ++p) {
+        // in panel order, panel p factored already (by launch p - 1), left of c
+        if (p != next[b] || p > k || p >= c) return false;
+        ++next[b];
+      }
+      return true;
+    };
+    for (int wg = 0; wg < plan.grid[k + 1]; ++wg) {
+      const CholWork w = chol_work_of(wg, nblk, k, plan.t_end[k + 1], 0, plan.extra[k + 1]);
+      if (w.kind == 0) {
+        if (!receive(w.R, w.T, k, k >= 0 ? 1 : 0)) return fail;
+      } else if (w.kind == 1) {
+        for (int i = 0; i < 4; ++i) {
+          const int br = w.R + i / 2, bc = w.T + i % 2;
+          if (br < nblk && bc <= br && bc < w.t_end && !receive(br, bc, w.p0, w.np)) return fail;
+        }
+      }
+    }
+    // the launch has factored column k + 1: every block of it complete
+    for (int r = k + 1; r < nblk; ++r)
+      if (next[(size_t)r * nblk + k + 1] != k + 1) return fail;
+  }
+  for (int r = 0; r < nblk; ++r)
+    for (int c = 0; c <= r; ++c)
+      if (next[(size_t)r * nblk + c] != c) return nblk + 1;
+  return 0;
+}
+
 // A single layer's factorisation in the look-ahead form (below) from 48
 // panels on (measured: 80 panels 5.07 -> 4.74 ms per solve, 48 panels 1.76 ->
 // 1.70 ms, 24 panels 0.654 -> 0.656 ms); ISPA_SOLVE_LOOKAHEAD=0 / 1 switches
@@ -1249,54 +1377,11 @@ hipError_t launch_solve(const float* G, const float* C, int d, int d_out, float 
     // still receives every panel once, in panel order, with the same
     // arithmetic: bit for bit the factor of the other forms.
     const int n_cu = attn_cu_count() > 0 ? attn_cu_count() : 256;
-    int next_sp[kMaxTasks] = {};               // per band: the next group it receives
-    const int n_bands = (nblk - 2) / kLa + 1;  // bands 1 .. n_bands - 1 start inside the matrix
-    for (int k = -1; k <= nblk - 2; ++k) {
-      const int m = nblk - 1 - k;
-      const int t_end = k >= 0 ? min(nblk, k / kLa * kLa + kLa + 1) : 0;
-      const int rows = (nblk - k - 2 + 1) / 2;
-      const int cols = k >= 0 && t_end > k + 2 ? (t_end - k - 2 + 1) / 2 : 0;
-      CholExtra x = none;
-      x.trail = cols * rows - cols * (cols - 1) / 2;
-      int cand[kMaxTasks][3], n_cand = 0;  // deadline, band, group
-      for (int b = 1; b < n_bands; ++b) {
-        const int sp = next_sp[b];
-        if (sp <= b - 1 && k >= sp * kLa + kLa - 1) {
-          cand[n_cand][0] = sp == b - 1 ? kLa * b - 1 : (kLa - 1) * b + sp;
-          cand[n_cand][1] = b;
-          cand[n_cand][2] = sp;
-          ++n_cand;
-        }
-      }
-      for (int i = 1; i < n_cand; ++i)  // by deadline, then band
-        for (int j = i; j > 0 && (cand[j][0] < cand[j - 1][0] ||
-                                  (cand[j][0] == cand[j - 1][0] && cand[j][1] < cand[j - 1][1])); --j)
-          for (int f = 0; f < 3; ++f) std::swap(cand[j][f], cand[j - 1][f]);
-      auto band_groups = [&](int b) {
-        int g = 0;
-        for (int T = b * kLa + 1; T < min(nblk, b * kLa + kLa + 1); T += 2) g += (nblk - T + 1) / 2;
-        return g;
-      };
-      // the rounds of workgroups the launch needs for its due tasks, filled up
-      int used = m + x.trail, due = used;
-      for (int i = 0; i < n_cand; ++i)
-        if (cand[i][0] == k) due += band_groups(cand[i][1]);
-      const int cap = (due + n_cu - 1) / n_cu * n_cu;
-      for (int i = 0; i < n_cand; ++i) {
-        const int b = cand[i][1];
-        const int g = band_groups(b);
-        if (cand[i][0] == k || used + g <= cap) {
-          x.band[x.n_tasks] = b;
-          x.sp[x.n_tasks] = cand[i][2];
-          x.groups[x.n_tasks] = g;
-          ++x.n_tasks;
-          used += g;
-          ++next_sp[b];
-        }
-      }
-      hipLaunchKernelGGL(chol_step_kernel, dim3(used, 1), dim3(kThreads), 0, stream, L, w.dinv, d, k, t_end,
-                         k >= 0 ? 1 : 0, 0, w.status, ws, x);
-    }
+    LookaheadPlan plan;
+    lookahead_plan(nblk, n_cu, &plan);
+    for (int k = -1; k <= nblk - 2; ++k)
+      hipLaunchKernelGGL(chol_step_kernel, dim3(plan.grid[k + 1], 1), dim3(kThreads), 0, stream, L, w.dinv, d, k,
+                         plan.t_end[k + 1], k >= 0 ? 1 : 0, 0, w.status, ws, plan.extra[k + 1]);
   } else {
     const int c_def = nl > 1 ? nblk + sup : 0;
     for (int k = -1; k <= nblk - 2; ++k) {
