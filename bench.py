@@ -724,7 +724,7 @@ def main():
     ap.add_argument("--no-14b", action="store_true",
                     help="skip the 14B-shaped step that the default 1.3B run also times (breakdown_14b)")
     ap.add_argument("--only", choices=["all", "attn_dual", "attn_local", "accum_stats", "solve", "hbm_copy",
-                                       "discrepancy", "lib_ref", "project"],
+                                       "discrepancy", "lib_ref", "project", "attn_zero"],
                     default="all",
                     help="time one part of the step alone (for profiling); the JSON line then covers that part")
     args = ap.parse_args()
@@ -737,6 +737,15 @@ def main():
         return
     if args.only == "project":
         print(json.dumps(project_run(WORKLOADS[args.workload], args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "attn_zero":
+        # the dual call on all-zero inputs alone (for counters beside --only attn_dual)
+        import paper_2607_00712_amd as ispa
+        dev = torch.device("cuda", 0)
+        torch.cuda.set_device(dev)
+        rec = zero_inputs_run(ispa, WORKLOADS[args.workload], dev, reps=args.steps)
+        rec.update({"only": "attn_zero", "workload": args.workload, "steps": args.steps})
+        print(json.dumps(rec), flush=True)
         return
     if args.only == "lib_ref":
         print(json.dumps(lib_ref(args.steps, args.warmup)), flush=True)
