@@ -70,6 +70,35 @@ def test_planted_solution():
     assert abs(eps) < 1e-6 * float((t.double() ** 2).sum())
 
 
+@pytest.mark.parametrize("d_in,d_out,n", [(1536, 256, 4680), (5120, 256, 8192)])
+def test_eps_near_a_fit(d_in, d_out, n):
+    # The layer ranking of Sec. 3.3 keeps the layers whose eps is much smaller
+    # than s, where eps = s - <dW, C> - lambda ||dW||^2 (Eq. 6) cancels about
+    # three digits. R = X B plus noise of 1e-3 of its energy puts eps / s near
+    # (1 - d_in / n) 1e-3; eps must still agree with the oracle's to 1% of eps
+    # (G is well conditioned at n > d_in, so the fp32 solve's relative error
+    # of about 1e-6 moves eps by about 1e-3 of itself). 5120 takes the
+    # look-ahead factorisation and the two-stream sweeps.
+    lam = 0.5
+    x = rows(41, 0, n, d_in)
+    b = synth.normal((d_in, d_out), synth.seed_of(41, 1, synth.X), DEV, dtype=torch.float32,
+                     scale=d_in ** -0.5)
+    noise = synth.normal((n, d_out), synth.seed_of(41, 0, synth.Y_FULL), DEV, dtype=torch.float32,
+                         scale=0.032)
+    yf = x.float() @ b + noise
+    yl = torch.zeros_like(yf)
+    st = ispa.Stats(d_in, d_out, max_rows=n, device=DEV)
+    st.accum(x, yf, yl)
+    dw, eps = st.solve(lam)
+    ref = oracle.Stats(d_in, d_out)
+    ref.accumulate(f64(x), f64(yf).astype(np.float32), f64(yl).astype(np.float32))
+    dw_ref = oracle.solve_modulation(ref.G, ref.C, lam)
+    eps_ref = oracle.feasibility(ref.s, dw_ref, ref.C, lam)
+    assert 1e-4 * ref.s < eps_ref < 2e-3 * ref.s, (eps_ref, ref.s)
+    assert rel_fro(f64(dw), dw_ref) <= DW_TOL
+    assert abs(eps - eps_ref) <= 1e-2 * eps_ref, (eps, eps_ref)
+
+
 def tiny_chain(sink):
     """The tiny single-layer workload end to end: 2 warmup chunks of 64
     queries against a 256-key cache, local window of one chunk, lambda 1e-3."""
