@@ -221,6 +221,36 @@ def test_batch_solve_matches_single(d_in, d_out, n, layers):
     assert torch.equal(dw_again.view(torch.int32), dw_b.view(torch.int32))
 
 
+def test_batch_eps_ranks_near_fits():
+    # three layers whose R is X B plus noise of 1e-2, 1e-3 and 3e-3 of its
+    # energy (d_in = 1536): each layer's eps within 1% of the oracle's, and the
+    # lowest-eps selection of Sec. 3.3 orders them as the oracle does
+    lam, d_in, d_out, n = 0.5, 1536, 256, 4680
+    scales = (0.1, 0.032, 0.056)
+    print(f"[solve] near-fit batch of {len(scales)} at d_in={d_in}", flush=True)
+    sb = ispa.StatsBatch(len(scales), d_in, d_out, max_rows=n, device=DEV)
+    eps_ref = []
+    for i, (st, sc) in enumerate(zip(sb.layers, scales)):
+        x = rows(42, i, n, d_in)
+        b = synth.normal((d_in, d_out), synth.seed_of(42, i, synth.X, 1), DEV, dtype=torch.float32,
+                         scale=d_in ** -0.5)
+        noise = synth.normal((n, d_out), synth.seed_of(42, i, synth.Y_FULL), DEV, dtype=torch.float32,
+                             scale=sc)
+        yf = x.float() @ b + noise
+        yl = torch.zeros_like(yf)
+        st.accum(x, yf, yl)
+        ref = oracle.Stats(d_in, d_out)
+        ref.accumulate(f64(x), f64(yf).astype(np.float32), f64(yl).astype(np.float32))
+        eps_ref.append(oracle.feasibility(ref.s, oracle.solve_modulation(ref.G, ref.C, lam), ref.C, lam))
+    _, eps_b, status_b = sb.solve(lam)
+    torch.cuda.synchronize()
+    assert status_b.tolist() == [0] * len(scales)
+    eps = [float(e) for e in eps_b.tolist()]
+    for i in range(len(scales)):
+        assert abs(eps[i] - eps_ref[i]) <= 1e-2 * eps_ref[i], (i, eps[i], eps_ref[i])
+    assert oracle.select_layers(eps, 2).tolist() == oracle.select_layers(eps_ref, 2).tolist() == [1, 2]
+
+
 def test_batch_solve_reports_each_layer():
     # a zero column with lambda = 0 makes only layer 1 fail; the others solve
     d, n = 64, 80
